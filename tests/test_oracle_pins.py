@@ -1,0 +1,346 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-types the oracle's formulas: each compares it with a
+hand-worked fixture (tests/golden), a closed form, a textbook routine, an error
+bound, or brute force over sets derived independently (tests/oracle_shadow.py).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from oracle_shadow import Shadow, softmax_attend
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+U32 = 2.0 ** -24
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _tiny_spec(**kw):
+    base = dict(name="tiny", batch=2, num_kv_heads=2, group=2, head_dim=16, page_size=4,
+                budget=16, window=3, steps=40, dtype="f32", prefill=(61, 38), seed=11)
+    base.update(kw)
+    return W.Spec(**base)
+
+
+def _run(spec, steps=None, attend=True):
+    g = W.Generator(spec)
+    o = oracle.Oracle.for_spec(spec)
+    for b, (k, v) in enumerate(g.prefill()):
+        o.prefill(b, k, v)
+    qw = W.QueryWindow(spec)
+    outs = []
+    for t in range(spec.steps if steps is None else steps):
+        k, v, q = g.step(t)
+        win = qw.push(q).copy()
+        out = o.step(t, k, v, win, attend=attend)
+        out["q_window"] = win
+        outs.append(out)
+    return g, o, outs
+
+
+# ----------------------------------------------------------------------------- digests
+@pytest.mark.parametrize("tps", [1, 3])
+def test_digest_is_elementwise_min_max_of_stored_keys(tps):
+    spec = _tiny_spec(tokens_per_step=tps, steps=12)
+    g, o, _ = _run(spec, attend=False)
+    for b in range(spec.batch):
+        L = int(o.seq_lens[b])
+        for p in range(-(-L // spec.page_size)):
+            lo, hi = p * spec.page_size, min((p + 1) * spec.page_size, L)
+            keys = g.keys[b][lo:hi]                      # [n][h_k][d], the generator's copy
+            np.testing.assert_array_equal(o.kmin[b, :, p], keys.min(axis=0))
+            np.testing.assert_array_equal(o.kmax[b, :, p], keys.max(axis=0))
+
+
+# ----------------------------------------------------------------------------- score
+def _score_setup(dtype, d, G, seed):
+    spec = _tiny_spec(head_dim=d, group=G, dtype=dtype, prefill=(70, 70), steps=0, seed=seed)
+    g = W.Generator(spec)
+    o = oracle.Oracle.for_spec(spec)
+    for b, (k, v) in enumerate(g.prefill()):
+        o.prefill(b, k, v)
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((spec.batch, spec.num_q_heads, d)).astype(np.float32) * 3
+    if dtype == "bf16":
+        q = W.round_bf16(q)
+    return spec, g, o, q
+
+
+@pytest.mark.parametrize("dtype,d,G", [("f32", 16, 2), ("bf16", 64, 4), ("f32", 128, 8),
+                                       ("bf16", 128, 1)])
+def test_score_within_fp32_error_bound_of_exact_value(dtype, d, G):
+    """eq. (quest_score) over the reals vs the fp32 evaluation: the error of a
+    pairwise sum of d terms plus a sequential sum of G terms (plus one rounding
+    per product for fp32 inputs) is at most (log2 d + G + 1) u sum|terms|."""
+    spec, g, o, q = _score_setup(dtype, d, G, seed=d + G)
+    s = o.score(q)
+    for b in range(spec.batch):
+        n = -(-int(o.seq_lens[b]) // spec.page_size)
+        for h in range(spec.num_kv_heads):
+            qq = q[b, h * G:(h + 1) * G].astype(np.float64)          # [G][d]
+            lo = o.kmin[b, h, :n].astype(np.float64)                   # [n][d]
+            hi = o.kmax[b, h, :n].astype(np.float64)
+            terms = np.maximum(qq[None] * lo[:, None], qq[None] * hi[:, None])  # [n][G][d]
+            exact = terms.sum(axis=(1, 2))
+            bound = (math.log2(d) + G + 1) * U32 * np.abs(terms).sum(axis=(1, 2)) * 1.01
+            err = np.abs(s[b, h, :n].astype(np.float64) - exact)
+            assert np.all(err <= bound + 1e-30), (err - bound).max()
+
+
+def test_score_of_single_token_page_is_sum_of_dot_products():
+    """A page holding one key k has Kmin = Kmax = k, so eq. (quest_score) reduces
+    to sum_g q_g . k."""
+    spec = _tiny_spec(prefill=(1,), batch=1, steps=0, head_dim=32, group=3)
+    g = W.Generator(spec)
+    o = oracle.Oracle.for_spec(spec)
+    k, v = g.prefill()[0]
+    o.prefill(0, k, v)
+    rng = np.random.default_rng(5)
+    q = rng.standard_normal((1, spec.num_q_heads, 32)).astype(np.float32)
+    s = o.score(q)
+    for h in range(spec.num_kv_heads):
+        qq = q[0, h * 3:(h + 1) * 3].astype(np.float64)
+        kk = k[0, h].astype(np.float64)
+        exact = float((qq @ kk).sum())
+        assert abs(float(s[0, h, 0]) - exact) <= (5 + 3 + 1) * U32 * float(np.abs(qq * kk).sum())
+
+
+def test_score_upper_bounds_every_key_of_the_page():
+    """For every key l of page j and every query, Q.k_l <= score_j(Q): each term
+    Q_i k_{l,i} lies between Q_i Kmin_i and Q_i Kmax_i (Quest's upper bound)."""
+    spec, g, o, q = _score_setup("f32", 64, 4, seed=3)
+    s = o.score(q)
+    for b in range(spec.batch):
+        L = int(o.seq_lens[b])
+        for h in range(spec.num_kv_heads):
+            qq = q[b, h * 4:(h + 1) * 4].astype(np.float64)
+            keys = g.keys[b][:L, h].astype(np.float64)                # [L][d]
+            dots = (keys @ qq.T).sum(axis=1)                           # [L]
+            pages = np.arange(L) // spec.page_size
+            slack = (6 + 4 + 1) * U32 * (np.abs(keys) @ np.abs(qq).T).sum(axis=1)
+            assert np.all(dots <= s[b, h, pages].astype(np.float64) + 2 * slack)
+
+
+def test_score_evaluation_order_golden():
+    gold = _load("score_order.json")
+    d = gold["head_dim"]
+    o = oracle.Oracle(batch=1, num_kv_heads=1, group=1, head_dim=d, page_size=1, budget=1,
+                      window=0, max_tokens=1)
+    key = np.array(gold["key"], np.float32).reshape(1, 1, d)
+    o.prefill(0, key, np.zeros_like(key))
+    s = o.score(np.array(gold["q"], np.float32).reshape(1, 1, d))
+    assert float(s[0, 0, 0]) == gold["expected_fp32"]
+    assert math.copysign(1.0, float(s[0, 0, 0])) == 1.0      # never a negative zero
+
+
+# ----------------------------------------------------------------------------- top-k
+@pytest.mark.parametrize("n,budget_pages", [(37, 8), (129, 16), (5, 16), (64, 64), (300, 1)])
+def test_select_equals_stable_sort_by_score_then_index(n, budget_pages):
+    P = 4
+    o = oracle.Oracle(batch=2, num_kv_heads=3, group=1, head_dim=8, page_size=P,
+                      budget=budget_pages * P, window=0, max_tokens=400 * P)
+    rng = np.random.default_rng(n)
+    scores = np.zeros((2, 3, o.max_pages), np.float32)
+    # heavy ties, signed zeros included
+    scores[:, :, :n] = rng.integers(-3, 4, size=(2, 3, n)).astype(np.float32)
+    scores[0, 0, :n:7] = -0.0
+    o.seq_lens[:] = [n * P - 1, (n - 1) * P + 1]
+    sel, num = o.select(scores)
+    for b in range(2):
+        nb = -(-int(o.seq_lens[b]) // P)
+        k = min(budget_pages, nb)
+        for h in range(3):
+            idx = np.arange(nb)
+            order = np.lexsort((idx, -scores[b, h, :nb].astype(np.float64)))
+            want = np.sort(order[:k])
+            assert num[b, h] == k
+            np.testing.assert_array_equal(sel[b, h, :k], want)
+            assert np.all(sel[b, h, k:] == -1)
+
+
+# ----------------------------------------------------------------------------- Alg. 2
+def test_alg2_golden_walk():
+    gold = _load("alg2_walk.json")
+    P, W_ = gold["page_size"], gold["window"]
+    o = oracle.Oracle(batch=1, num_kv_heads=1, group=1, head_dim=2, page_size=P,
+                      budget=3 * P, window=W_, max_tokens=gold["prefill_tokens"] + 5)
+    z = np.zeros((gold["prefill_tokens"], 1, 2), np.float32)
+    o.prefill(0, z, z)
+    for st in gold["steps"]:
+        t = st["t"]
+        o.append(t, np.zeros((1, 1, 2), np.float32), np.zeros((1, 1, 2), np.float32))
+        assert (int(o.seq_lens[0]) - 1) // P == st["p_curr"]
+        sel = np.full((1, 1, o.k_max), -1, np.int32)
+        sel[0, 0, :3] = st["S"]
+        num = np.array([[3]], np.int32)
+        M = o.build_mask(t, sel, num)
+        assert list(M[0, 0, :3]) == st["M"], t
+        assert list(o.A[0, 0, :7]) == st["A_after"], t
+        st["_M"] = dict(zip(st["S"], st["M"]))
+    for e in gold["eligible_past"]:
+        st = gold["steps"][e["t"]]
+        got = sorted(p for p, m in st["_M"].items() if m < e["tau"])   # the paper's mask rule
+        assert got == e["pages"], e
+
+
+@pytest.mark.parametrize("tps,P,W_", [(1, 4, 3), (3, 4, 5), (1, 8, 1), (5, 4, 2)])
+def test_mask_rule_equals_set_semantics_and_never_double_counts(tps, P, W_):
+    """Alg. 2's A/M bookkeeping (M_p < tau) selects exactly the pages of
+    eq. (update-sup) minus those holding keys newer than tau, for every past
+    query of every step; and no token reaches a query twice."""
+    spec = _tiny_spec(tokens_per_step=tps, page_size=P, window=W_, steps=48,
+                      budget=4 * P, prefill=(9 * P + 1, 5 * P + 3))
+    _, o, outs = _run(spec, attend=False)
+    sh = Shadow(spec.batch, spec.num_kv_heads, P, W_)
+    for t, out in enumerate(outs):
+        want = sh.record(t, out["selected"], out["num_selected"], out["seq_lens"])
+        for b in range(spec.batch):
+            for h in range(spec.num_kv_heads):
+                k = out["num_selected"][b, h]
+                sel = out["selected"][b, h, :k]
+                M = out["mask"][b, h, :k]
+                for tau in range(max(0, t - W_), t):
+                    got = set(int(p) for p, m in zip(sel, M) if m < tau)
+                    assert got == want[(b, h, tau)], (t, b, h, tau)
+
+
+# ----------------------------------------------------------------------------- attention
+def test_attention_and_merge_closed_form_golden():
+    gold = _load("attention_closed_form.json")
+    d, P = gold["head_dim"], gold["page_size"]
+    o = oracle.Oracle(batch=1, num_kv_heads=1, group=1, head_dim=d, page_size=P, budget=2 * P,
+                      window=1, max_tokens=4, sm_scale=gold["sm_scale"])
+    k = np.array(gold["keys"], np.float32).reshape(4, 1, d)
+    v = np.array(gold["values"], np.float32).reshape(4, 1, d)
+    o.prefill(0, k, v)
+    qw = np.zeros((1, 2, 1, d), np.float32)
+    qw[0, :, 0] = gold["q"]             # same query at both window rows
+    tol = 1e-6
+    for sel_pages, M, key in [([0, 1], [-1, -1], "both"), ([0], [-1], "page0"), ([1], [-1], "page1")]:
+        sel = np.full((1, 1, 2), -1, np.int32)
+        sel[0, 0, :len(sel_pages)] = sel_pages
+        Mm = np.full((1, 1, 2), -1, np.int32)
+        Mm[0, 0, :len(M)] = M
+        op, zp = o.attend(1, qw, sel, np.array([[len(sel_pages)]], np.int32), Mm)
+        np.testing.assert_allclose(op[0, 1, 0], gold[key]["O"], atol=tol)
+        assert abs(zp[0, 1, 0] - gold[key]["Z_value"]) < tol
+    # Past row tau=0 at step 1: page 0 was loaded at step 0 (M=0, skipped),
+    # page 1 is new (M=-1): the supplement is page 1 alone...
+    sel = np.array([[[0, 1]]], np.int32)
+    op, zp = o.attend(1, qw, sel, np.array([[2]], np.int32), np.array([[[0, -1]]], np.int32))
+    np.testing.assert_allclose(op[0, 0, 0], gold["page1"]["O"], atol=tol)
+    # ...and merging it into the cached page-0 output gives attention over both.
+    om, zm = oracle.lse_merge(gold["page0"]["O"], gold["page0"]["Z_value"], op[0, 0, 0], zp[0, 0, 0])
+    np.testing.assert_allclose(om, gold["both"]["O"], atol=tol)
+    assert abs(zm - gold["both"]["Z_value"]) < tol
+
+
+def test_lse_merge_identity_commutativity_associativity():
+    rng = np.random.default_rng(0)
+    d = 8
+    a, b, c = (rng.standard_normal(d) for _ in range(3))
+    za, zb, zc = 1.5, -0.25, 3.0
+    o, z = oracle.lse_merge(a, za, b, -np.inf)
+    np.testing.assert_array_equal(o, a)
+    assert z == za
+    o, z = oracle.lse_merge(a, -np.inf, b, -np.inf)
+    assert np.all(o == 0) and z == -np.inf
+    o1, z1 = oracle.lse_merge(a, za, b, zb)
+    o2, z2 = oracle.lse_merge(b, zb, a, za)
+    np.testing.assert_allclose(o1, o2, rtol=0, atol=1e-14)
+    assert abs(z1 - z2) < 1e-14
+    l, zl = oracle.lse_merge(*oracle.lse_merge(a, za, b, zb), c, zc)
+    r, zr = oracle.lse_merge(a, za, *oracle.lse_merge(b, zb, c, zc))
+    np.testing.assert_allclose(l, r, atol=1e-13)
+    assert abs(zl - zr) < 1e-13
+    # weights are the normalisers e^Z (eq. merged_attn)
+    ea, eb = math.exp(za), math.exp(zb)
+    np.testing.assert_allclose(o1, (ea * a + eb * b) / (ea + eb), atol=1e-14)
+    assert abs(z1 - math.log(ea + eb)) < 1e-14
+
+
+@pytest.mark.parametrize("tps,W_", [(1, 3), (2, 5), (1, 1)])
+def test_every_window_row_equals_softmax_over_its_attended_union(tps, W_):
+    """After any number of supplements, a past query's cached output equals plain
+    softmax attention over the union of the (disjoint) token sets it has attended,
+    so the merged output at finalisation equals attention over the whole union."""
+    spec = _tiny_spec(tokens_per_step=tps, window=W_, steps=30)
+    g, o, outs = _run(spec)
+    sh = Shadow(spec.batch, spec.num_kv_heads, spec.page_size, W_)
+    qs = {}
+    for t, out in enumerate(outs):
+        sh.record(t, out["selected"], out["num_selected"], out["seq_lens"])
+        qs[t] = out["q_window"][:, -1].copy()
+        for b in range(spec.batch):
+            for qh in range(spec.num_q_heads):
+                h = qh // spec.group
+                for r in range(W_ + 1):
+                    tau = t - W_ + r
+                    if tau < 0:
+                        assert out["lse_out"][b, r, qh] == -np.inf
+                        assert np.all(out["o_out"][b, r, qh] == 0)
+                        continue
+                    toks = sh.seen[(b, h, tau)]
+                    O, Z = softmax_attend(qs[tau][b, qh], g.keys[b][:, h], _values(o, b, h), toks,
+                                          o.dims.sm_scale)
+                    np.testing.assert_allclose(out["o_out"][b, r, qh], O, atol=1e-10)
+                    assert abs(out["lse_out"][b, r, qh] - Z) < 1e-10
+
+
+def _values(o, b, h):
+    return o.V[b, h]
+
+
+def test_full_budget_current_row_is_dense_causal_attention():
+    """With a budget covering the whole context every page is selected, so the
+    current query's output is dense causal attention (softmax(qK^T/sqrt d)V over
+    all stored tokens) and no past query ever gets a supplement."""
+    spec = _tiny_spec(budget=4 * 200, steps=10, window=3)
+    g, o, outs = _run(spec)
+    for t, out in enumerate(outs):
+        for b in range(spec.batch):
+            L = int(out["seq_lens"][b])
+            for qh in range(spec.num_q_heads):
+                h = qh // spec.group
+                q = out["q_window"][b, -1, qh].astype(np.float64)
+                k = g.keys[b][:L, h].astype(np.float64)
+                v = o.V[b, h, :L].astype(np.float64)
+                s = (k @ q) / math.sqrt(spec.head_dim)
+                w = np.exp(s - s.max())
+                np.testing.assert_allclose(out["o_out"][b, -1, qh], w @ v / w.sum(), atol=1e-6)
+                assert abs(out["lse_out"][b, -1, qh] - (s.max() + math.log(w.sum()))) < 1e-6
+                for r in range(spec.window):
+                    if t - spec.window + r >= 0:
+                        assert out["lse_part"][b, r, qh] == -np.inf
+
+
+def test_window_zero_is_plain_quest_sparse_attention():
+    """W = 0 leaves only the current query: its output is softmax attention over
+    the tokens of the k best pages (eq. update-org), pages chosen here with an
+    independent numpy sort of the page scores."""
+    spec = _tiny_spec(window=0, steps=12)
+    g, o, outs = _run(spec)
+    for out in outs:
+        for b in range(spec.batch):
+            L = int(out["seq_lens"][b])
+            n = -(-L // spec.page_size)
+            k = min(spec.budget // spec.page_size, n)
+            for qh in range(spec.num_q_heads):
+                h = qh // spec.group
+                sc = out["scores"][b, h, :n].astype(np.float64)
+                pages = np.lexsort((np.arange(n), -sc))[:k]
+                toks = [p * spec.page_size + s for p in pages for s in range(spec.page_size)
+                        if p * spec.page_size + s < L]
+                O, Z = softmax_attend(out["q_window"][b, 0, qh], g.keys[b][:, h], o.V[b, h], toks,
+                                      o.dims.sm_scale)
+                np.testing.assert_allclose(out["o_out"][b, 0, qh], O, atol=1e-10)
+                assert abs(out["lse_out"][b, 0, qh] - Z) < 1e-10
