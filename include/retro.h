@@ -1,0 +1,212 @@
+/*
+ * retro.h — C ABI of an MI355X (gfx950) library for one decode step of
+ * retrospective sparse attention ("Retrospective Sparse Attention for
+ * Efficient Long-Context Generation", Alg. 1 without its UpdateKV line).
+ *
+ * One step of one attention layer, for a batch of sequences:
+ *   1. append the step's key/value to a paged KV cache and keep per-page key
+ *      min/max digests (Sec. 2.1, "Dynamic Sparse Attention");
+ *   2. score every page against the current query, eq. (quest_score), and keep
+ *      the top-k pages under a token budget (PageSelect);
+ *   3. record, per KV head and page, the last step the page was loaded, and hand
+ *      the previous value to the attention kernel (Alg. 2, UpdateAndBuildMask);
+ *   4. one attention pass over the selected pages for the current query and the
+ *      W past queries of the retrospective window, a past query taking only the
+ *      pages it has not seen (eq. update-org, eq. update-sup, "Retrospective
+ *      Mask" paragraph);
+ *   5. merge the past queries' supplementary outputs into an output cache of
+ *      (output, log-sum-exp) per past query, eq. (merged_attn_general), and
+ *      return the finished output of the query leaving the window.
+ *
+ * Window convention: W counts PAST queries.  A step processes W+1 queries:
+ * row r of the window is the query of step tau = t - W + r, row W the current
+ * one.  (The paper's window w counts the current query too: W = w - 1.)
+ * W = 0 is plain query-aware sparse attention without retrospection.
+ *
+ * Conventions for every entry point
+ *   - All buffers are caller-owned DEVICE memory, contiguous, row-major, with
+ *     the layouts given below.  The library allocates nothing and keeps no state
+ *     between calls; scratch lives in the caller's `workspace`.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *     and is asynchronous: no call synchronises the host.
+ *   - Argument errors are detected on the host before anything is enqueued and
+ *     return RETRO_EINVAL / RETRO_EUNSUPPORTED / RETRO_EWORKSPACE; a failed
+ *     launch returns RETRO_EHIP.  No C++ exception crosses the ABI.
+ *   - Device-side contract (not checkable on the host): seq_lens, page_table,
+ *     selections and the mask hold values produced by this library or obeying
+ *     the ranges documented here.  Out-of-range page numbers are skipped by the
+ *     kernels instead of being dereferenced.
+ *   - Calls that share buffers must be ordered by the caller (same stream).
+ */
+#ifndef RETRO_H
+#define RETRO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RETRO_OK = 0,
+  RETRO_EINVAL = -1,        /* null pointer, negative size, inconsistent dimension */
+  RETRO_EUNSUPPORTED = -2,  /* well-formed but outside the supported shapes */
+  RETRO_EHIP = -3,          /* a HIP launch or query failed */
+  RETRO_EWORKSPACE = -4     /* workspace null or smaller than retro_workspace_size() */
+} retro_status;
+
+typedef enum { RETRO_F32 = 0, RETRO_BF16 = 1 } retro_dtype;
+
+/* Problem statement of one layer.  Supported: head_dim 64 or 128; page_size
+ * 16 or 32; 1 <= group <= 16; 0 <= window <= 64; (window+1)*group <= 1024;
+ * page_size <= budget_tokens; max_pages <= 16384. */
+typedef struct retro_dims {
+  int32_t batch;           /* sequences in the batch                                   */
+  int32_t num_kv_heads;    /* h_k                                                      */
+  int32_t group;           /* G query heads per KV head; h_q = h_k * G (GQA)            */
+  int32_t head_dim;        /* d                                                        */
+  int32_t page_size;       /* P tokens per page                                        */
+  int32_t budget_tokens;   /* B; each step keeps k = min(B / P, pages of the sequence) */
+  int32_t window;          /* W past queries revisited per step                        */
+  int32_t max_pages;       /* length of a page-table row (logical pages per sequence)  */
+  int32_t num_phys_pages;  /* physical pages in k_cache / v_cache / digest             */
+  int32_t dtype;           /* retro_dtype of queries, keys, values and digests         */
+  float sm_scale;          /* softmax scale applied to q.k; 0 selects 1/sqrt(d)         */
+} retro_dims;
+
+/* The paged KV cache of one layer (Sec. 2.1; pages as in a vLLM-style pool).
+ *   k_cache     [num_phys_pages][h_k][P][d]   dtype  key page, token-major
+ *   v_cache     [num_phys_pages][h_k][d][P]   dtype  value page, stored transposed
+ *                                                    (d-major) so that the token
+ *                                                    contraction reads contiguously
+ *   digest      [num_phys_pages][h_k][2][d]   dtype  [0] = element-wise key minimum,
+ *                                                    [1] = maximum over the page's
+ *                                                    stored tokens (Quest digest)
+ *   page_table  [batch][max_pages]            int32  logical page -> physical page
+ *   seq_lens    [batch]                       int32  tokens stored per sequence
+ *   last_loaded [batch][h_k][max_pages]       int32  A of Alg. 2: last decode step in
+ *                                                    which each logical page was
+ *                                                    loaded; the caller initialises it
+ *                                                    to -1 before the first step.
+ * Slots beyond seq_lens are never read as keys; their values are zeroed before use. */
+typedef struct retro_kv_cache {
+  void* k_cache;
+  void* v_cache;
+  void* digest;
+  const int32_t* page_table;
+  int32_t* seq_lens;
+  int32_t* last_loaded;
+} retro_kv_cache;
+
+/* Output of page selection (PageSelect + UpdateAndBuildMask).
+ *   selected     [batch][h_k][k_max]  int32  logical page ids in ascending order,
+ *                                            -1 after the first num_selected entries
+ *   mask         [batch][h_k][k_max]  int32  M of Alg. 2: last_loaded of each selected
+ *                                            page before this step (-1 padding)
+ *   num_selected [batch][h_k]         int32
+ * with k_max = retro_k_max(dims). */
+typedef struct retro_selection {
+  int32_t* selected;
+  int32_t* mask;
+  int32_t* num_selected;
+} retro_selection;
+
+/* The attention output cache (Sec. 2.3, "Attention Output Cache"): for each of the
+ * last W steps tau, the output of tau's query merged over every supplement so
+ * far, in ring slot tau mod W.
+ *   o_cache   [batch][W][h_q][d]  fp32
+ *   lse_cache [batch][W][h_q]     fp32 natural-log normaliser (log of alpha)
+ * Slots are only read after the step that wrote them; no initialisation needed.
+ * Both may be NULL when W == 0. */
+typedef struct retro_output_cache {
+  float* o_cache;
+  float* lse_cache;
+} retro_output_cache;
+
+/* Library version string. */
+const char* retro_version(void);
+
+/* Human-readable name of a status code. */
+const char* retro_status_string(int32_t status);
+
+/* Validate dims; on success write k_max = min(budget_tokens / page_size, max_pages). */
+retro_status retro_k_max(const retro_dims* dims, int32_t* k_max);
+
+/* Bytes of scratch the select / attend / step calls need for these dims. */
+retro_status retro_workspace_size(const retro_dims* dims, size_t* bytes);
+
+/* Bulk-store n_tokens tokens of sequence `seq` at positions start_pos ..
+ * start_pos+n_tokens-1 (k_src, v_src: [n_tokens][h_k][d] dtype, device) and
+ * rebuild the digests of the pages they touch.  start_pos must equal the
+ * sequence's current seq_lens entry, which becomes start_pos + n_tokens.  For the
+ * prefill that precedes the first decode step: last_loaded is not touched. */
+retro_status retro_prefill_kv(const retro_dims* dims, const retro_kv_cache* cache, int32_t seq,
+                              int32_t start_pos, int32_t n_tokens, const void* k_src,
+                              const void* v_src, void* stream);
+
+/* AppendKV (Alg. 1) of one token per sequence (k_new, v_new: [batch][h_k][d] dtype)
+ * at position seq_lens[b], which is then incremented.  The page's digest widens to
+ * the new key (or starts at it for the page's first slot), and last_loaded of that
+ * page is set to step-1 for every head: the first line of Alg. 2, applied when a
+ * page receives a key newer than every past query.  May be called several times
+ * per step (several tokens per step).  A token whose logical page is not mapped
+ * (page_table entry < 0 or >= num_phys_pages, or position >= max_pages*P) is
+ * dropped and seq_lens is left unchanged. */
+retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_kv_cache* cache,
+                             const void* k_new, const void* v_new, void* stream);
+
+/* PageSelect + UpdateAndBuildMask (Alg. 1, Alg. 2) for the current query
+ * q_cur [batch][h_q][d] (dtype).
+ *   score of page p of KV head h = sum over the G query heads g of h of
+ *     sum_i max(q_gi * Kmin_pi, q_gi * Kmax_pi)                  eq. (quest_score)
+ *   evaluated in fp32: products rounded to fp32, the d terms summed as a perfect
+ *   binary tree over index order, the G head sums added in order, then + 0.0f.
+ *   The k = min(B/P, ceil(seq_len/P)) best pages by (score descending, page index
+ *   ascending) are written in ascending order; then for each selected page p, in
+ *   order: mask = last_loaded[p]; last_loaded[p] = step.
+ * Page selection is exact: it depends on no floating-point reduction order other
+ * than the one stated. */
+retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void* q_cur,
+                                const retro_kv_cache* cache, const retro_selection* sel,
+                                void* workspace, size_t ws_bytes, void* stream);
+
+/* Attention of the W+1 window queries q_window [batch][W+1][h_q][d] (dtype; row W
+ * is step t) over the selected pages.  Row r (tau = t-W+r) uses page p iff tau >= 0
+ * and (r == W or mask[p] < tau); every stored token of a used page counts.
+ * Output per row and query head: o_part [batch][W+1][h_q][d] fp32 (softmax-weighted
+ * values) and lse_part [batch][W+1][h_q] fp32 = ln sum exp(sm_scale * q.k);
+ * an empty set gives (0, -inf).  Reads only; writes o_part, lse_part, workspace. */
+retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const void* q_window,
+                                 const retro_kv_cache* cache, const retro_selection* sel,
+                                 float* o_part, float* lse_part, void* workspace,
+                                 size_t ws_bytes, void* stream);
+
+/* MergeOutput + CacheOutput (Alg. 1; eq. merged_attn_general) for step t.
+ * For each query head and row r with tau = t-W+r >= 0:
+ *   r == W   : out = part; pushed to slot t mod W;
+ *   0 < r < W: out = merge(slot tau mod W, part); written back to the slot;
+ *   r == 0   : out = merge(slot, part) is final (the query leaves the window), and
+ *              the slot (t-W) mod W = t mod W is then reused by row W;
+ * where merge((O_a,Z_a),(O_b,Z_b)) = ((e^Za O_a + e^Zb O_b)/(e^Za + e^Zb),
+ * ln(e^Za + e^Zb)), a -inf side contributing nothing.  Rows with tau < 0 give
+ * o_out = 0, lse_out = -inf and touch no slot.
+ *   o_out [batch][W+1][h_q][d] fp32, lse_out [batch][W+1][h_q] fp32. */
+retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, const float* o_part,
+                                      const float* lse_part, const retro_output_cache* ocache,
+                                      float* o_out, float* lse_out, void* stream);
+
+/* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
+ * q_window), retro_decode_attend, retro_merge_output_cache, with the same
+ * semantics, without materialising o_part / lse_part. */
+retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
+                        const void* k_new, const void* v_new, const retro_kv_cache* cache,
+                        const retro_selection* sel, const retro_output_cache* ocache,
+                        float* o_out, float* lse_out, void* workspace, size_t ws_bytes,
+                        void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RETRO_H */

@@ -1,0 +1,245 @@
+// C ABI entry points: argument validation, geometry and workspace sizing, and the
+// launch sequences of each call.  Nothing here allocates device memory.
+#include <math.h>
+
+#include "internal.h"
+
+namespace retro {
+
+int attend_min_waves(int dtype, int D);
+
+namespace {
+
+constexpr int kTargetWorkgroups = 256;   // attention workgroups aimed for per call
+constexpr int kMaxChunksPerSplit = 32;   // pages per split <= 64 (LDS page list)
+constexpr int kMaxWaves = 8;
+constexpr int kMaxRtw = 2;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace
+
+retro_status make_geometry(const retro_dims* d, Geometry* g) {
+  if (!d || !g) return RETRO_EINVAL;
+  if (d->batch < 1 || d->num_kv_heads < 1 || d->group < 1 || d->head_dim < 1 ||
+      d->page_size < 1 || d->budget_tokens < 1 || d->window < 0 || d->max_pages < 1 ||
+      d->num_phys_pages < 1)
+    return RETRO_EINVAL;
+  if (d->dtype != RETRO_F32 && d->dtype != RETRO_BF16) return RETRO_EINVAL;
+  if (!(d->sm_scale >= 0.f) || isinf(d->sm_scale)) return RETRO_EINVAL;
+  if (d->head_dim != 64 && d->head_dim != 128) return RETRO_EUNSUPPORTED;
+  if (d->page_size != 16 && d->page_size != 32) return RETRO_EUNSUPPORTED;
+  if (d->group > 16 || d->window > 64) return RETRO_EUNSUPPORTED;
+  if ((int64_t)(d->window + 1) * d->group > 1024) return RETRO_EUNSUPPORTED;
+  if (d->budget_tokens < d->page_size) return RETRO_EINVAL;
+  if (d->max_pages > 16384) return RETRO_EUNSUPPORTED;
+  if ((int64_t)d->batch * d->num_kv_heads > 65535) return RETRO_EUNSUPPORTED;
+
+  Geometry x{};
+  x.batch = d->batch;
+  x.hk = d->num_kv_heads;
+  x.G = d->group;
+  x.hq = d->num_kv_heads * d->group;
+  x.D = d->head_dim;
+  x.P = d->page_size;
+  x.budget = d->budget_tokens;
+  x.W = d->window;
+  x.R = (d->window + 1) * d->group;
+  x.max_pages = d->max_pages;
+  x.num_phys = d->num_phys_pages;
+  x.dtype = d->dtype;
+  x.elt = d->dtype == RETRO_BF16 ? 2 : 4;
+  x.k_max = std::min(d->budget_tokens / d->page_size, d->max_pages);
+  x.sm_scale = d->sm_scale > 0.f ? d->sm_scale : 1.0f / sqrtf((float)d->head_dim);
+
+  x.chunk_pages = 32 / x.P;
+  x.chunks_max = (x.k_max + x.chunk_pages - 1) / x.chunk_pages;
+  const int bh = x.batch * x.hk;
+  const int want_splits = std::max(1, (kTargetWorkgroups + bh - 1) / bh);
+  x.chunks_per_split =
+      std::min(kMaxChunksPerSplit, std::max(1, (x.chunks_max + want_splits - 1) / want_splits));
+  x.n_splits = (x.chunks_max + x.chunks_per_split - 1) / x.chunks_per_split;
+  x.pages_per_split = x.chunks_per_split * x.chunk_pages;
+  if (x.n_splits > 65535) return RETRO_EUNSUPPORTED;
+
+  x.row_tiles = (x.R + 15) / 16;
+  x.n_rgroups = (x.row_tiles + kMaxWaves * kMaxRtw - 1) / (kMaxWaves * kMaxRtw);
+  x.tiles_per_group = (x.row_tiles + x.n_rgroups - 1) / x.n_rgroups;
+  x.rtw = (x.tiles_per_group + kMaxWaves - 1) / kMaxWaves;
+  x.waves = std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D));
+  if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
+
+  const size_t bhs = (size_t)bh;
+  x.ws_scores = 0;
+  size_t off = align256(bhs * x.max_pages * sizeof(float));
+  x.ws_opart = off;
+  off += align256(bhs * x.n_splits * x.R * x.D * sizeof(float));
+  x.ws_lpart = off;
+  off += align256(bhs * x.n_splits * x.R * sizeof(float));
+  x.ws_total = off;
+  *g = x;
+  return RETRO_OK;
+}
+
+}  // namespace retro
+
+using retro::Geometry;
+
+namespace {
+
+retro_status from_hip(hipError_t e) { return e == hipSuccess ? RETRO_OK : RETRO_EHIP; }
+
+bool cache_ok(const retro_kv_cache* c) {
+  return c && c->k_cache && c->v_cache && c->digest && c->page_table && c->seq_lens &&
+         c->last_loaded;
+}
+
+bool sel_ok(const retro_selection* s) { return s && s->selected && s->mask && s->num_selected; }
+
+retro_status prepare(const retro_dims* dims, int32_t step, Geometry* g) {
+  retro_status st = retro::make_geometry(dims, g);
+  if (st != RETRO_OK) return st;
+  if (step < 0) return RETRO_EINVAL;
+  return RETRO_OK;
+}
+
+retro_status check_ws(const Geometry& g, void* ws, size_t ws_bytes) {
+  if (!ws || ws_bytes < g.ws_total) return RETRO_EWORKSPACE;
+  return RETRO_OK;
+}
+
+float* ws_at(void* ws, size_t off) { return reinterpret_cast<float*>((char*)ws + off); }
+
+}  // namespace
+
+extern "C" {
+
+const char* retro_version(void) { return "retro-mi355x 0.1.0 (gfx950)"; }
+
+const char* retro_status_string(int32_t status) {
+  switch (status) {
+    case RETRO_OK: return "RETRO_OK";
+    case RETRO_EINVAL: return "RETRO_EINVAL: invalid argument";
+    case RETRO_EUNSUPPORTED: return "RETRO_EUNSUPPORTED: shape outside the supported range";
+    case RETRO_EHIP: return "RETRO_EHIP: HIP launch failed";
+    case RETRO_EWORKSPACE: return "RETRO_EWORKSPACE: workspace missing or too small";
+    default: return "unknown retro_status";
+  }
+}
+
+retro_status retro_k_max(const retro_dims* dims, int32_t* k_max) {
+  Geometry g;
+  if (!k_max) return RETRO_EINVAL;
+  retro_status st = retro::make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  *k_max = g.k_max;
+  return RETRO_OK;
+}
+
+retro_status retro_workspace_size(const retro_dims* dims, size_t* bytes) {
+  Geometry g;
+  if (!bytes) return RETRO_EINVAL;
+  retro_status st = retro::make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  *bytes = g.ws_total;
+  return RETRO_OK;
+}
+
+retro_status retro_prefill_kv(const retro_dims* dims, const retro_kv_cache* cache, int32_t seq,
+                              int32_t start_pos, int32_t n_tokens, const void* k_src,
+                              const void* v_src, void* stream) {
+  Geometry g;
+  retro_status st = retro::make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  if (!cache_ok(cache) || !k_src || !v_src) return RETRO_EINVAL;
+  if (seq < 0 || seq >= g.batch || start_pos < 0 || n_tokens < 0) return RETRO_EINVAL;
+  if ((int64_t)start_pos + n_tokens > (int64_t)g.max_pages * g.P) return RETRO_EINVAL;
+  return from_hip(retro::launch_prefill(g, *cache, seq, start_pos, n_tokens, k_src, v_src,
+                                        (hipStream_t)stream));
+}
+
+retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_kv_cache* cache,
+                             const void* k_new, const void* v_new, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!cache_ok(cache) || !k_new || !v_new) return RETRO_EINVAL;
+  return from_hip(retro::launch_append(g, step, *cache, k_new, v_new, (hipStream_t)stream));
+}
+
+retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void* q_cur,
+                                const retro_kv_cache* cache, const retro_selection* sel,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!q_cur || !cache_ok(cache) || !sel_ok(sel)) return RETRO_EINVAL;
+  if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  float* scores = ws_at(workspace, g.ws_scores);
+  hipError_t e = retro::launch_score(g, q_cur, (int64_t)g.hq * g.D, *cache, scores, s);
+  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, s);
+  return from_hip(e);
+}
+
+retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const void* q_window,
+                                 const retro_kv_cache* cache, const retro_selection* sel,
+                                 float* o_part, float* lse_part, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!q_window || !cache_ok(cache) || !sel_ok(sel) || !o_part || !lse_part) return RETRO_EINVAL;
+  if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  float* o_ws = ws_at(workspace, g.ws_opart);
+  float* l_ws = ws_at(workspace, g.ws_lpart);
+  hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, o_ws, l_ws, s);
+  if (e == hipSuccess)
+    e = retro::launch_combine_merge(g, step, 0, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
+                                    o_part, lse_part, nullptr, nullptr, nullptr, s);
+  return from_hip(e);
+}
+
+retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, const float* o_part,
+                                      const float* lse_part, const retro_output_cache* ocache,
+                                      float* o_out, float* lse_out, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!o_part || !lse_part || !o_out || !lse_out) return RETRO_EINVAL;
+  if (g.W > 0 && (!ocache || !ocache->o_cache || !ocache->lse_cache)) return RETRO_EINVAL;
+  return from_hip(retro::launch_combine_merge(g, step, 1, nullptr, nullptr, nullptr, o_part,
+                                              lse_part, nullptr, nullptr, ocache, o_out, lse_out,
+                                              (hipStream_t)stream));
+}
+
+retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
+                        const void* k_new, const void* v_new, const retro_kv_cache* cache,
+                        const retro_selection* sel, const retro_output_cache* ocache,
+                        float* o_out, float* lse_out, void* workspace, size_t ws_bytes,
+                        void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!q_window || !k_new || !v_new || !cache_ok(cache) || !sel_ok(sel) || !o_out || !lse_out)
+    return RETRO_EINVAL;
+  if (g.W > 0 && (!ocache || !ocache->o_cache || !ocache->lse_cache)) return RETRO_EINVAL;
+  if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  float* scores = ws_at(workspace, g.ws_scores);
+  float* o_ws = ws_at(workspace, g.ws_opart);
+  float* l_ws = ws_at(workspace, g.ws_lpart);
+  const int64_t qbs = (int64_t)(g.W + 1) * g.hq * g.D;
+  const char* q_cur = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
+  hipError_t e = retro::launch_append(g, step, *cache, k_new, v_new, s);
+  if (e == hipSuccess) e = retro::launch_score(g, q_cur, qbs, *cache, scores, s);
+  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, s);
+  if (e == hipSuccess) e = retro::launch_attend(g, step, q_window, *cache, *sel, o_ws, l_ws, s);
+  if (e == hipSuccess)
+    e = retro::launch_combine_merge(g, step, 2, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
+                                    nullptr, nullptr, ocache, o_out, lse_out, s);
+  return from_hip(e);
+}
+
+}  // extern "C"

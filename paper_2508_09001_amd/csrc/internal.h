@@ -1,0 +1,71 @@
+// Private declarations shared by the library's HIP translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "retro.h"
+
+namespace retro {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 values are carried as raw 16-bit patterns outside the MFMA code.
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) {
+  return __uint_as_float(static_cast<uint32_t>(x.bits) << 16);
+}
+
+// Validated, derived dimensions of one call.
+struct Geometry {
+  int batch, hk, G, hq, D, P, budget, W, R, max_pages, num_phys, dtype, elt;
+  int k_max;          // selection row length
+  float sm_scale;     // resolved (never 0)
+  // attention split geometry
+  int chunk_pages;    // pages per 32-token chunk (2 for P=16, 1 for P=32)
+  int chunks_max;     // chunks needed for k_max pages
+  int chunks_per_split;
+  int n_splits;       // splits per (b, h_k)
+  int pages_per_split;
+  int row_tiles;      // ceil(R / 16)
+  int n_rgroups;      // row groups (workgroups sharing a split's pages)
+  int tiles_per_group;
+  int rtw;            // row tiles per wave
+  int waves;          // waves per attention workgroup
+  // workspace layout (bytes)
+  size_t ws_scores, ws_opart, ws_lpart, ws_total;
+};
+
+retro_status make_geometry(const retro_dims* d, Geometry* g);
+int attend_min_waves(int dtype, int D);
+
+// ---- launchers (return hipSuccess or the launch error) ----
+hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
+                         const void* v_new, hipStream_t s);
+hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
+                          const void* k_src, const void* v_src, hipStream_t s);
+hipError_t launch_score(const Geometry& g, const void* q_cur, int64_t q_batch_stride,
+                        const retro_kv_cache& c, float* scores, hipStream_t s);
+hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
+                            const retro_kv_cache& c, const retro_selection& sel, hipStream_t s);
+hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
+                         const retro_kv_cache& c, const retro_selection& sel, float* o_ws,
+                         float* l_ws, hipStream_t s);
+// mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
+hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
+                                const float* l_ws, const int32_t* num_selected,
+                                const float* o_part, const float* l_part, float* o_part_out,
+                                float* l_part_out, const retro_output_cache* oc, float* o_out,
+                                float* lse_out, hipStream_t s);
+
+}  // namespace retro

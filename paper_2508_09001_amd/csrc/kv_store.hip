@@ -1,0 +1,146 @@
+// KV storage: AppendKV (Alg. 1) and bulk prefill, keeping the Quest page digests
+// (element-wise key min / max of each page, Sec. 2.1) and, on append, the
+// retrospective-mask override of Alg. 2's first line.
+#include "internal.h"
+
+namespace retro {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ bool less(T a, T b) { return to_f32(a) < to_f32(b); }
+
+// One workgroup per sequence: every thread reads seq_lens[b] before thread 0
+// advances it, so the whole token lands at one position.
+template <typename T>
+__global__ void __launch_bounds__(256) append_kernel(Geometry g, int step, T* __restrict__ kc,
+                                                     T* __restrict__ vc, T* __restrict__ dg,
+                                                     const int32_t* __restrict__ pt,
+                                                     int32_t* __restrict__ seq_lens,
+                                                     int32_t* __restrict__ A,
+                                                     const T* __restrict__ k_new,
+                                                     const T* __restrict__ v_new) {
+  const int b = blockIdx.x;
+  const int pos = seq_lens[b];
+  const int lp = pos / g.P, slot = pos - lp * g.P;
+  int phys = -1;
+  if (pos >= 0 && lp < g.max_pages) phys = pt[(int64_t)b * g.max_pages + lp];
+  const bool ok = phys >= 0 && phys < g.num_phys;
+  __syncthreads();
+  if (ok) {
+    const int n = g.hk * g.D;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+      const int h = e / g.D, i = e - h * g.D;
+      const T kv = k_new[(int64_t)b * n + e];
+      const T vv = v_new[(int64_t)b * n + e];
+      const int64_t ph = (int64_t)phys * g.hk + h;
+      kc[(ph * g.P + slot) * g.D + i] = kv;
+      vc[(ph * g.D + i) * g.P + slot] = vv;
+      T* lo = dg + (ph * 2) * g.D + i;
+      T* hi = lo + g.D;
+      if (slot == 0) {
+        *lo = kv;
+        *hi = kv;
+      } else {
+        if (less(kv, *lo)) *lo = kv;
+        if (less(*hi, kv)) *hi = kv;
+      }
+    }
+    for (int h = threadIdx.x; h < g.hk; h += blockDim.x)
+      A[((int64_t)b * g.hk + h) * g.max_pages + lp] = step - 1;
+  }
+  __syncthreads();
+  if (ok && threadIdx.x == 0) seq_lens[b] = pos + 1;
+}
+
+// Prefill, pass 1: one workgroup per token copies its keys (token-major page) and
+// values (d-major page).
+template <typename T>
+__global__ void __launch_bounds__(256) prefill_write_kernel(Geometry g, int seq, int start,
+                                                            T* __restrict__ kc,
+                                                            T* __restrict__ vc,
+                                                            const int32_t* __restrict__ pt,
+                                                            const T* __restrict__ k_src,
+                                                            const T* __restrict__ v_src) {
+  const int j = blockIdx.x;
+  const int pos = start + j;
+  const int lp = pos / g.P, slot = pos - lp * g.P;
+  if (lp >= g.max_pages) return;
+  const int phys = pt[(int64_t)seq * g.max_pages + lp];
+  if (phys < 0 || phys >= g.num_phys) return;
+  const int n = g.hk * g.D;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int h = e / g.D, i = e - h * g.D;
+    const int64_t ph = (int64_t)phys * g.hk + h;
+    kc[(ph * g.P + slot) * g.D + i] = k_src[(int64_t)j * n + e];
+    vc[(ph * g.D + i) * g.P + slot] = v_src[(int64_t)j * n + e];
+  }
+}
+
+// Prefill, pass 2: digest of every touched page = min / max over its stored slots.
+template <typename T>
+__global__ void __launch_bounds__(128) prefill_digest_kernel(Geometry g, int seq, int start,
+                                                             int end, const T* __restrict__ kc,
+                                                             T* __restrict__ dg,
+                                                             const int32_t* __restrict__ pt,
+                                                             int32_t* __restrict__ seq_lens) {
+  const int lp = start / g.P + blockIdx.x;
+  const int h = blockIdx.y;
+  if (blockIdx.x == 0 && h == 0 && threadIdx.x == 0) seq_lens[seq] = end;
+  if (lp >= g.max_pages) return;
+  const int phys = pt[(int64_t)seq * g.max_pages + lp];
+  if (phys < 0 || phys >= g.num_phys) return;
+  const int filled = min(g.P, end - lp * g.P);
+  const int64_t ph = (int64_t)phys * g.hk + h;
+  for (int i = threadIdx.x; i < g.D; i += blockDim.x) {
+    T lo = kc[(ph * g.P) * g.D + i], hi = lo;
+    for (int s = 1; s < filled; ++s) {
+      const T v = kc[(ph * g.P + s) * g.D + i];
+      if (less(v, lo)) lo = v;
+      if (less(hi, v)) hi = v;
+    }
+    dg[(ph * 2) * g.D + i] = lo;
+    dg[(ph * 2 + 1) * g.D + i] = hi;
+  }
+}
+
+template <typename T>
+hipError_t append_t(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
+                    const void* v_new, hipStream_t s) {
+  append_kernel<T><<<g.batch, 256, 0, s>>>(g, step, (T*)c.k_cache, (T*)c.v_cache, (T*)c.digest,
+                                           c.page_table, c.seq_lens, c.last_loaded,
+                                           (const T*)k_new, (const T*)v_new);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t prefill_t(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
+                     const void* k_src, const void* v_src, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  prefill_write_kernel<T><<<n, 256, 0, s>>>(g, seq, start, (T*)c.k_cache, (T*)c.v_cache,
+                                            c.page_table, (const T*)k_src, (const T*)v_src);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int end = start + n;
+  const int pages = (end - 1) / g.P - start / g.P + 1;
+  prefill_digest_kernel<T><<<dim3(pages, g.hk), 128, 0, s>>>(g, seq, start, end,
+                                                             (const T*)c.k_cache,
+                                                             (T*)c.digest, c.page_table,
+                                                             c.seq_lens);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
+                         const void* v_new, hipStream_t s) {
+  return g.dtype == RETRO_BF16 ? append_t<bf16_t>(g, step, c, k_new, v_new, s)
+                               : append_t<float>(g, step, c, k_new, v_new, s);
+}
+
+hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
+                          const void* k_src, const void* v_src, hipStream_t s) {
+  return g.dtype == RETRO_BF16 ? prefill_t<bf16_t>(g, c, seq, start, n, k_src, v_src, s)
+                               : prefill_t<float>(g, c, seq, start, n, k_src, v_src, s);
+}
+
+}  // namespace retro

@@ -1,0 +1,89 @@
+"""GPU parity: the HIP library against the CPU oracle on the five workloads.
+
+Selections, masks, the retrospective mask A and sequence lengths must match
+bit for bit every step; outputs and log-normalisers within 2e-3 max-abs for
+bf16 inputs (fp32 accumulation) and 1e-5 for fp32 inputs.  Steps are fewer
+than the full workloads where the oracle would take minutes; each run still
+spans many tiles, splits and a ragged last page, and covers the window's
+ramp-up and several wraps of the output-cache ring.
+"""
+import pytest
+
+import workloads as W
+from gpu_harness import run_parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2508_09001_amd import binding
+    binding.load_library()
+
+
+def test_tiny_fp32_all_steps():
+    run_parity(W.config(0), W.config(0).steps)
+
+
+def test_tiny_fp32_separate_entry_points():
+    run_parity(W.config(0), 12, split_calls=True, label="tiny-fp32 split calls")
+
+
+def test_tiny_fp32_shuffled_page_table():
+    run_parity(W.config(0), 12, page_perm_seed=5, label="tiny-fp32 shuffled pages")
+
+
+def test_llama_layer_32k():
+    spec = W.config(1)
+    run_parity(spec, 40)
+
+
+def test_llama_layer_32k_split_calls_shuffled():
+    spec = W.config(1)
+    run_parity(spec, 20, split_calls=True, page_perm_seed=1, label="32k split+shuffled")
+
+
+def test_batched_serving_ragged():
+    spec = W.config(2)
+    run_parity(spec, 12, page_perm_seed=2, label="batch16 ragged shuffled")
+
+
+def test_long_generation_multi_token_steps():
+    # 8 tokens appended per step (16384 -> 49152 over 4096 steps); batch 2 of 4
+    spec = W.config(3).replace(batch=2, prefill=(16384, 16384))
+    run_parity(spec, 40, label="long-generation b2 8 tok/step")
+
+
+@pytest.mark.parametrize("budget,window", [(1024, 0), (2048, 4), (4096, 16), (8192, 64)])
+def test_extreme_context_sweep(budget, window):
+    spec = W.config(4).replace(budget=budget, window=window)
+    run_parity(spec, 10, label=f"131k B={budget} W={window}")
+
+
+@pytest.mark.parametrize("window", [0, 4])
+def test_extreme_context_full_budget_is_dense(window):
+    # budget covering the whole context: every page selected, current row = dense
+    spec = W.config(4).replace(budget=131072 + 4096, window=window)
+    run_parity(spec, 3, label=f"131k dense W={window}")
+
+
+def test_short_sequences_and_partial_pages():
+    # sequences shorter than one page and budgets above the context
+    spec = W.Spec("edge-short", batch=3, num_kv_heads=2, group=3, head_dim=64, page_size=16,
+                  budget=64, window=5, steps=20, dtype="bf16", prefill=(1, 17, 40), seed=9)
+    run_parity(spec, 20, page_perm_seed=3, label="edge short")
+
+
+def test_group_one_wide_window():
+    spec = W.Spec("edge-w64-g1", batch=2, num_kv_heads=1, group=1, head_dim=128, page_size=32,
+                  budget=256, window=64, steps=70, dtype="bf16", prefill=(500, 900), seed=10)
+    run_parity(spec, 70, label="edge W=64 G=1")
+
+
+def test_fp32_head_dim_128_many_rows():
+    spec = W.Spec("edge-f32-d128", batch=1, num_kv_heads=2, group=8, head_dim=128, page_size=16,
+                  budget=512, window=20, steps=24, dtype="f32", prefill=(3000,), seed=12)
+    run_parity(spec, 24, label="edge f32 d128 R=168")
