@@ -1,0 +1,271 @@
+#!/usr/bin/env python
+"""Benchmark of one retrospective sparse-attention decode step per layer on one GPU.
+
+Workload (default): a Llama-3-8B-shaped attention layer, batch 1, 8 KV heads,
+32 query heads, head_dim 128, bf16, 32K-token context in pages of 16, token
+budget 2048 (128 pages), retrospective window W = 16 past queries.  Seeded
+synthetic keys / values / queries (no dataset or weights are needed).
+
+A "step" is one whole decode step (append, page scoring, top-k + mask,
+attention over the W+1 window queries, merge into the output cache) for each of
+--layers independent layer replicas: with 32 replicas (an 8B model's layer
+count) the data touched per step is far above the 256 MB Infinity Cache, so the
+bytes really come from HBM.  Steps are captured as HIP graphs (one per step) and
+replayed back to back in the timed region.
+
+Prints one JSON line with the throughput (effective HBM GB/s of the whole step,
+algorithmic bytes / time), microseconds per layer per step, the roofline of the
+dominant kernel (the page-gather attention kernel, timed alone with HIP events)
+and the CPU oracle's rate on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "retro_step µs/layer/decode-step + effective HBM GB/s (% peak), 32K ctx B=2048 W=16"
+PEAK_HBM_GBS = 8000.0
+ATTEND_SRC = os.path.join(ROOT, "paper_2508_09001_amd", "csrc", "attend.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "attend_kernel_llama3-8b-32k_counters.json")
+
+
+def _args():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=16, help="timed decode steps")
+    p.add_argument("--warmup", type=int, default=4, help="untimed decode steps")
+    p.add_argument("--layers", type=int, default=32, help="layer replicas rotated per step")
+    p.add_argument("--config", type=int, default=1, help="workload index (1 = headline)")
+    p.add_argument("--attend-reps", type=int, default=4,
+                   help="attention-kernel launches per layer in the roofline measurement")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="budget of the CPU oracle sample (0 skips it)")
+    p.add_argument("--calib-copy", action="store_true",
+                   help="only run a 512 MiB device copy (counter calibration) and exit")
+    return p.parse_args()
+
+
+def _sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def algorithmic_bytes(spec, seq_lens, num_selected):
+    """Bytes one layer-step must move at minimum (per the step's definition)."""
+    elt = 2 if spec.dtype == "bf16" else 4
+    b, hk, hq, d, P, W = spec.batch, spec.num_kv_heads, spec.num_q_heads, spec.head_dim, \
+        spec.page_size, spec.window
+    n_pages = sum(-(-int(L) // P) for L in seq_lens)
+    k_sum = int(sum(int(x) for x in num_selected.reshape(-1)))     # over (b, h)
+    digest = n_pages * hk * 2 * d * elt
+    gather = k_sum * P * 2 * d * elt
+    queries = b * (W + 1) * hq * d * elt
+    ring = 2 * b * W * hq * (d + 1) * 4
+    out = b * (W + 1) * hq * (d + 1) * 4
+    mask = 12 * k_sum
+    append = b * hk * d * elt * 2 + b * hk * 2 * d * elt * 2
+    return dict(total=digest + gather + queries + ring + out + mask + append, digest=digest,
+                gather=gather, queries=queries, ring=ring, out=out, mask=mask, append=append)
+
+
+def _calib_copy():
+    import torch
+    n = 512 << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes": n, "launches": 3}))
+
+
+def main():
+    args = _args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the step shards "
+              "by KV head or sequence with no communication, see the design notes", file=sys.stderr)
+        sys.exit(2)
+    from paper_2508_09001_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2508_09001_amd.layer import RetroLayer
+
+    if args.calib_copy:
+        _calib_copy()
+        return
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    base_spec = W.config(args.config)
+    need = args.warmup + 2 * args.steps
+    spec = base_spec if need <= base_spec.steps else base_spec.replace(steps=need)
+    L = args.layers
+
+    # ---- inputs: prefill + per-step tokens and query windows, resident on the GPU
+    gen = W.Generator(spec)
+    pre = gen.prefill()
+    qw = W.QueryWindow(spec)
+    steps_in = []
+    for t in range(need):
+        k_new, v_new, q = gen.step(t)
+        win = qw.push(q).copy()
+        steps_in.append(tuple(torch.from_numpy(np.ascontiguousarray(x)).to(
+            "cuda", dtype=torch.bfloat16 if spec.dtype == "bf16" else torch.float32)
+            for x in (win, k_new, v_new)))
+    layers = [RetroLayer.for_spec(spec) for _ in range(L)]
+    for b, (k, v) in enumerate(pre):
+        layers[0].prefill(b, k, v)
+    for lay in layers[1:]:
+        for name in ("k_cache", "v_cache", "digest", "seq_lens", "last_loaded"):
+            getattr(lay, name).copy_(getattr(layers[0], name))
+        lay._lens = list(layers[0]._lens)
+    torch.cuda.synchronize()
+
+    def run_step(t):
+        win, k_new, v_new = steps_in[t]
+        for lay in layers:
+            for j in range(k_new.shape[0] - 1):
+                lay.append(t, k_new[j], v_new[j])
+            lay.step(t, win, k_new[-1], v_new[-1])
+
+    for t in range(args.warmup):
+        run_step(t)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps replayed from HIP graphs
+    t0 = args.warmup
+    graphs = []
+    for t in range(t0, t0 + args.steps):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run_step(t)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for g in graphs:
+        g.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_graph = ev0.elapsed_time(ev1)
+    seq_mid = layers[0].seq_lens.cpu().numpy()
+    nsel = layers[0].num_selected.cpu().numpy()
+
+    # ---- eager launches of the next K steps, for comparison
+    t1 = t0 + args.steps
+    ev0.record()
+    for t in range(t1, t1 + args.steps):
+        run_step(t)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_eager = ev0.elapsed_time(ev1)
+
+    # ---- dominant kernel: the attention kernel alone, graph of L * reps launches
+    last = t1 + args.steps - 1
+    win_last = steps_in[last][0]
+    ga = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(ga):
+        for _ in range(args.attend_reps):
+            for lay in layers:
+                lay.attend_partials(last, win_last)
+    torch.cuda.synchronize()
+    ev0.record()
+    ga.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    n_att = args.attend_reps * L
+    us_attend = ev0.elapsed_time(ev1) * 1000.0 / n_att
+
+    nbytes = algorithmic_bytes(spec, seq_mid, nsel)
+    us_layer_step = ms_graph * 1000.0 / (args.steps * L)
+    gbs = nbytes["total"] / (us_layer_step * 1e-6) / 1e9
+    gather_gbs = nbytes["gather"] / (us_attend * 1e-6) / 1e9
+
+    traffic = None
+    if os.path.exists(COUNTERS):
+        with open(COUNTERS) as f:
+            cnt = json.load(f)
+        if cnt.get("attend_source_sha256") == _sha(ATTEND_SRC):
+            traffic = cnt.get("hbm_bytes_per_launch")
+
+    result = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_graph / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic",
+        "config": {"workload": spec.name, "batch": spec.batch, "kv_heads": spec.num_kv_heads,
+                   "q_heads": spec.num_q_heads, "head_dim": spec.head_dim,
+                   "context": int(spec.prefill[0]), "page_size": spec.page_size,
+                   "budget_tokens": spec.budget, "window": spec.window, "layers_rotated": L,
+                   "launch": "hip-graph per step"},
+        "us_per_layer_step": round(us_layer_step, 3),
+        "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
+        "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
+        "bytes_per_layer_step": nbytes,
+        "roofline": {"bound": "hbm", "kernel": "attend_kernel", "achieved": round(gather_gbs, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gather_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                     "bytes_per_launch": nbytes["gather"], "us_per_launch": round(us_attend, 3),
+                     "launches": n_att},
+    }
+
+    if args.cpu_seconds > 0:
+        result["cpu_baseline"] = cpu_baseline(spec, pre, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(spec, pre, budget_s):
+    """The CPU oracle on the same workload: untimed ramp-up of the window, then
+    decode steps of one layer until the time budget is used."""
+    import numpy as np
+
+    import oracle
+    import workloads as W
+    gen = W.Generator(spec)
+    gen.prefill()          # regenerates the same prefill (keeps the generator's key store)
+    orc = oracle.Oracle.for_spec(spec)
+    for b, (k, v) in enumerate(pre):
+        orc.prefill(b, k, v)
+    qw = W.QueryWindow(spec)
+    t = 0
+    for t in range(spec.window):
+        k_new, v_new, q = gen.step(t)
+        orc.step(t, k_new, v_new, qw.push(q).copy())
+    n, spent, last = 0, 0.0, None
+    while spent < budget_s and t + 1 < spec.steps:
+        t += 1
+        k_new, v_new, q = gen.step(t)
+        win = qw.push(q).copy()
+        s0 = time.perf_counter()
+        last = orc.step(t, k_new, v_new, win)
+        spent += time.perf_counter() - s0
+        n += 1
+    us = spent / max(n, 1) * 1e6
+    nb = algorithmic_bytes(spec, orc.seq_lens, last["num_selected"])
+    return {"value": round(nb["total"] / (us * 1e-6) / 1e9, 4), "unit": "GB/s",
+            "us_per_layer_step": round(us, 1), "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{n} decode steps of one layer of {spec.name} with a full window "
+                      f"(steps {spec.window + 1}..{t}), fp64 attention, OpenMP"}
+
+
+if __name__ == "__main__":
+    main()

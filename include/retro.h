@@ -80,9 +80,12 @@ typedef struct retro_dims {
  *   v_cache     [num_phys_pages][h_k][d][P]   dtype  value page, stored transposed
  *                                                    (d-major) so that the token
  *                                                    contraction reads contiguously
- *   digest      [num_phys_pages][h_k][2][d]   dtype  [0] = element-wise key minimum,
+ *   digest      [batch][h_k][max_pages][2][d] dtype  per LOGICAL page of each sequence:
+ *                                                    [0] = element-wise key minimum,
  *                                                    [1] = maximum over the page's
- *                                                    stored tokens (Quest digest)
+ *                                                    stored tokens (Quest digest); a
+ *                                                    head's digests are one contiguous
+ *                                                    stream for the page scan
  *   page_table  [batch][max_pages]            int32  logical page -> physical page
  *   seq_lens    [batch]                       int32  tokens stored per sequence
  *   last_loaded [batch][h_k][max_pages]       int32  A of Alg. 2: last decode step in
@@ -181,6 +184,16 @@ retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const voi
                                  const retro_kv_cache* cache, const retro_selection* sel,
                                  float* o_part, float* lse_part, void* workspace,
                                  size_t ws_bytes, void* stream);
+
+/* The attention pass of retro_decode_attend alone, as one kernel launch: each
+ * split's partial (O, LSE) stays in the workspace (library-private layout) and
+ * nothing else is written.  Meant for timing the page-gather attention kernel in
+ * isolation (the paper's kernel-level breakdown separates it from the merge);
+ * callers wanting outputs use retro_decode_attend or retro_step. */
+retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
+                                          const void* q_window, const retro_kv_cache* cache,
+                                          const retro_selection* sel, void* workspace,
+                                          size_t ws_bytes, void* stream);
 
 /* MergeOutput + CacheOutput (Alg. 1; eq. merged_attn_general) for step t.
  * For each query head and row r with tau = t-W+r >= 0:

@@ -69,6 +69,8 @@ def _load():
         lib.oracle_merge.restype = None
         lib.oracle_lse_merge.argtypes = [i32, P, C.c_double, P, C.c_double, P, P]
         lib.oracle_lse_merge.restype = None
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = i32
         _lib = lib
     return _lib
 
@@ -76,6 +78,11 @@ def _load():
 def _p(a: np.ndarray) -> int:
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().oracle_num_threads())
 
 
 def lse_merge(oa, za, ob, zb):

@@ -407,3 +407,15 @@ void oracle_lse_merge(int32_t d, const double* oa, double za, const double* ob, 
                       double* o, double* z) {
   lse_merge(d, oa, za, ob, zb, o, z);
 }
+
+/* Threads the parallel loops above use (for reporting the CPU baseline). */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int32_t oracle_num_threads(void) {
+#ifdef _OPENMP
+  return (int32_t)omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -72,6 +72,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   const size_t bhs = (size_t)bh;
   x.ws_scores = 0;
   size_t off = align256(bhs * x.max_pages * sizeof(float));
+  x.ws_phys = off;
+  off += align256(bhs * x.k_max * sizeof(int32_t));
   x.ws_opart = off;
   off += align256(bhs * x.n_splits * x.R * x.D * sizeof(float));
   x.ws_lpart = off;
@@ -178,7 +180,7 @@ retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void
   hipStream_t s = (hipStream_t)stream;
   float* scores = ws_at(workspace, g.ws_scores);
   hipError_t e = retro::launch_score(g, q_cur, (int64_t)g.hq * g.D, *cache, scores, s);
-  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, s);
+  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, nullptr, s);
   return from_hip(e);
 }
 
@@ -194,11 +196,25 @@ retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const voi
   hipStream_t s = (hipStream_t)stream;
   float* o_ws = ws_at(workspace, g.ws_opart);
   float* l_ws = ws_at(workspace, g.ws_lpart);
-  hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, o_ws, l_ws, s);
+  hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, nullptr, o_ws, l_ws, s);
   if (e == hipSuccess)
     e = retro::launch_combine_merge(g, step, 0, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
                                     o_part, lse_part, nullptr, nullptr, nullptr, s);
   return from_hip(e);
+}
+
+retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
+                                          const void* q_window, const retro_kv_cache* cache,
+                                          const retro_selection* sel, void* workspace,
+                                          size_t ws_bytes, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!q_window || !cache_ok(cache) || !sel_ok(sel)) return RETRO_EINVAL;
+  if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
+  return from_hip(retro::launch_attend(g, step, q_window, *cache, *sel, nullptr,
+                                       ws_at(workspace, g.ws_opart), ws_at(workspace, g.ws_lpart),
+                                       (hipStream_t)stream));
 }
 
 retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, const float* o_part,
@@ -232,10 +248,12 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   float* l_ws = ws_at(workspace, g.ws_lpart);
   const int64_t qbs = (int64_t)(g.W + 1) * g.hq * g.D;
   const char* q_cur = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
+  int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
   hipError_t e = retro::launch_append(g, step, *cache, k_new, v_new, s);
   if (e == hipSuccess) e = retro::launch_score(g, q_cur, qbs, *cache, scores, s);
-  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, s);
-  if (e == hipSuccess) e = retro::launch_attend(g, step, q_window, *cache, *sel, o_ws, l_ws, s);
+  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, phys, s);
+  if (e == hipSuccess)
+    e = retro::launch_attend(g, step, q_window, *cache, *sel, phys, o_ws, l_ws, s);
   if (e == hipSuccess)
     e = retro::launch_combine_merge(g, step, 2, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
                                     nullptr, nullptr, ocache, o_out, lse_out, s);

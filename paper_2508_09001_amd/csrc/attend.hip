@@ -66,6 +66,7 @@ struct AttendArgs {
   const int32_t* sel;
   const int32_t* msk;
   const int32_t* nsel;
+  const int32_t* sel_phys;  // physical ids of the selected pages, or null (page-table lookup)
   float* o_ws;
   float* l_ws;
 };
@@ -81,8 +82,16 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
   __shared__ int s_mask[MAX_SPLIT_PAGES];
 
   const Geometry& g = a.g;
-  const int split = blockIdx.x, b = blockIdx.z;
-  const int h = blockIdx.y / g.n_rgroups, rg = blockIdx.y - h * g.n_rgroups;
+  // Work units are ordered (sequence, KV head, row group, split), split fastest,
+  // and spread so that the units of one KV head share an XCD (workgroups go to
+  // the 8 XCDs round-robin): its partial outputs then stay in that XCD's L2 for
+  // the combine.
+  int u = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = u % g.n_splits;
+  u /= g.n_splits;
+  const int rg = u % g.n_rgroups;
+  u /= g.n_rgroups;
+  const int h = u % g.hk, b = u / g.hk;
   const int bh = b * g.hk + h;
   const int k_eff = a.nsel[bh];
   const int first = split * g.pages_per_split;
@@ -98,10 +107,12 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
   for (int i = tid; i < np; i += nthreads) {
     const int lp = a.sel[(int64_t)bh * g.k_max + first + i];
     int phys = -1;
-    if (lp >= 0 && lp < g.max_pages) {
+    if (a.sel_phys) {
+      phys = a.sel_phys[(int64_t)bh * g.k_max + first + i];
+    } else if (lp >= 0 && lp < g.max_pages) {
       phys = a.pt[(int64_t)b * g.max_pages + lp];
-      if (phys < 0 || phys >= g.num_phys) phys = -1;
     }
+    if (lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
     s_phys[i] = phys;
     s_page[i] = lp;
     s_mask[i] = a.msk[(int64_t)bh * g.k_max + first + i];
@@ -158,7 +169,10 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
 
   // ---- chunk staging: global -> registers -> LDS ----------------------------
   const int pieces_per_thread = (TL::PIECES + nthreads - 1) / nthreads;
-  uint4 stage[kMaxPieces];
+  // Chunks whose loads are in flight ahead of the computation: two when a
+  // wavefront owns one row tile, one when it owns two (register budget).
+  constexpr int DEPTH = RTW == 1 ? 2 : 1;
+  uint4 stage[DEPTH][kMaxPieces];
   const T* kc = reinterpret_cast<const T*>(a.kc);
   const T* vc = reinterpret_cast<const T*>(a.vc);
 
@@ -172,7 +186,7 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
     return c;
   };
 
-  auto load_chunk = [&](int c) {
+  auto load_chunk = [&](int c, uint4* stage) {
 #pragma unroll
     for (int i = 0; i < kMaxPieces; ++i) {
       const int e = tid + i * nthreads;
@@ -222,7 +236,7 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
     }
   };
 
-  auto store_chunk = [&](int buf) {
+  auto store_chunk = [&](int buf, const uint4* stage) {
     T* base = lds + buf * TL::BUF_ELEMS;
 #pragma unroll
     for (int i = 0; i < kMaxPieces; ++i) {
@@ -244,14 +258,7 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
     }
   };
 
-  load_chunk(0);
-  store_chunk(0);
-
-#pragma unroll 1
-  for (int c = 0; c < nchunks; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < nchunks) load_chunk(c + 1);
-    __syncthreads();
+  auto compute_chunk = [&](int c, int buf) {
     const T* Ks = lds + buf * TL::BUF_ELEMS;
     const T* Vs = Ks + TL::K_ELEMS;
 
@@ -363,7 +370,37 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
       }
     }
 
-    if (c + 1 < nchunks) store_chunk((c + 1) & 1);
+  };
+
+  // Chunk c goes through LDS buffer c & 1.  That buffer was last read while
+  // computing chunk c - 2, and every wavefront has since passed the barrier of
+  // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
+  // compile-time constants (two chunks per trip when DEPTH == 2).
+  if constexpr (DEPTH == 2) {
+    load_chunk(0, stage[0]);
+    if (nchunks > 1) load_chunk(1, stage[DEPTH - 1]);
+#pragma unroll 1
+    for (int c = 0; c < nchunks; c += 2) {
+      store_chunk(0, stage[0]);
+      if (c + 2 < nchunks) load_chunk(c + 2, stage[0]);
+      __syncthreads();
+      compute_chunk(c, 0);
+      if (c + 1 < nchunks) {
+        store_chunk(1, stage[DEPTH - 1]);
+        if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1]);
+        __syncthreads();
+        compute_chunk(c + 1, 1);
+      }
+    }
+  } else {
+    load_chunk(0, stage[0]);
+#pragma unroll 1
+    for (int c = 0; c < nchunks; ++c) {
+      store_chunk(c & 1, stage[0]);
+      if (c + 1 < nchunks) load_chunk(c + 1, stage[0]);
+      __syncthreads();
+      compute_chunk(c, c & 1);
+    }
   }
 
   // ---- normalise and write this split's partial (O, LSE) per row -------------
@@ -393,8 +430,8 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
 template <typename T, int D, int RTW>
 hipError_t attend_t(const AttendArgs& a, hipStream_t s) {
   const Geometry& g = a.g;
-  dim3 grid(g.n_splits, g.hk * g.n_rgroups, g.batch);
-  attend_kernel<T, D, RTW><<<grid, 64 * g.waves, 0, s>>>(a);
+  const int64_t n = (int64_t)g.n_splits * g.n_rgroups * g.hk * g.batch;
+  attend_kernel<T, D, RTW><<<(unsigned)n, 64 * g.waves, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -415,8 +452,8 @@ int attend_min_waves(int dtype, int D) {
 }
 
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
-                         const retro_kv_cache& c, const retro_selection& sel, float* o_ws,
-                         float* l_ws, hipStream_t s) {
+                         const retro_kv_cache& c, const retro_selection& sel,
+                         const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s) {
   AttendArgs a;
   a.g = g;
   a.step = step;
@@ -429,6 +466,7 @@ hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
   a.sel = sel.selected;
   a.msk = sel.mask;
   a.nsel = sel.num_selected;
+  a.sel_phys = sel_phys;
   a.o_ws = o_ws;
   a.l_ws = l_ws;
   if (g.dtype == RETRO_BF16) return g.D == 128 ? attend_d<bf16_t, 128>(a, s) : attend_d<bf16_t, 64>(a, s);

@@ -21,6 +21,14 @@ struct bf16_t {
   uint16_t bits;
 };
 
+// Workgroups are dispatched to the 8 XCDs round-robin.  Renumber them so that
+// consecutive work units land on one XCD: unit u of n goes to XCD u / (n / 8).
+// (Identity when n is not a multiple of 8.)
+__device__ __forceinline__ int xcd_remap(int i, int n) {
+  if (n % 8 != 0) return i;
+  return (i % 8) * (n / 8) + i / 8;
+}
+
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16_t x) {
   return __uint_as_float(static_cast<uint32_t>(x.bits) << 16);
@@ -43,7 +51,7 @@ struct Geometry {
   int rtw;            // row tiles per wave
   int waves;          // waves per attention workgroup
   // workspace layout (bytes)
-  size_t ws_scores, ws_opart, ws_lpart, ws_total;
+  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_total;
 };
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
@@ -57,10 +65,11 @@ hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, i
 hipError_t launch_score(const Geometry& g, const void* q_cur, int64_t q_batch_stride,
                         const retro_kv_cache& c, float* scores, hipStream_t s);
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
-                            const retro_kv_cache& c, const retro_selection& sel, hipStream_t s);
+                            const retro_kv_cache& c, const retro_selection& sel,
+                            int32_t* sel_phys, hipStream_t s);
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
-                         const retro_kv_cache& c, const retro_selection& sel, float* o_ws,
-                         float* l_ws, hipStream_t s);
+                         const retro_kv_cache& c, const retro_selection& sel,
+                         const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s);
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
 hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
                                 const float* l_ws, const int32_t* num_selected,

@@ -9,8 +9,10 @@ namespace {
 template <typename T>
 __device__ __forceinline__ bool less(T a, T b) { return to_f32(a) < to_f32(b); }
 
-// One workgroup per sequence: every thread reads seq_lens[b] before thread 0
-// advances it, so the whole token lands at one position.
+// One workgroup per sequence.  The token's keys / values and the digest row of
+// its logical page are fetched together with the page-table entry (the digest is
+// indexed by logical page, so it does not wait for the lookup).  Every thread
+// reads seq_lens[b] before thread 0 advances it.
 template <typename T>
 __global__ void __launch_bounds__(256) append_kernel(Geometry g, int step, T* __restrict__ kc,
                                                      T* __restrict__ vc, T* __restrict__ dg,
@@ -19,35 +21,53 @@ __global__ void __launch_bounds__(256) append_kernel(Geometry g, int step, T* __
                                                      int32_t* __restrict__ A,
                                                      const T* __restrict__ k_new,
                                                      const T* __restrict__ v_new) {
+  constexpr int kPer = 8;
   const int b = blockIdx.x;
+  const int n = g.hk * g.D;
   const int pos = seq_lens[b];
   const int lp = pos / g.P, slot = pos - lp * g.P;
+  const bool lp_ok = pos >= 0 && lp < g.max_pages;
   int phys = -1;
-  if (pos >= 0 && lp < g.max_pages) phys = pt[(int64_t)b * g.max_pages + lp];
-  const bool ok = phys >= 0 && phys < g.num_phys;
-  __syncthreads();
-  if (ok) {
-    const int n = g.hk * g.D;
-    for (int e = threadIdx.x; e < n; e += blockDim.x) {
-      const int h = e / g.D, i = e - h * g.D;
-      const T kv = k_new[(int64_t)b * n + e];
-      const T vv = v_new[(int64_t)b * n + e];
-      const int64_t ph = (int64_t)phys * g.hk + h;
-      kc[(ph * g.P + slot) * g.D + i] = kv;
-      vc[(ph * g.D + i) * g.P + slot] = vv;
-      T* lo = dg + (ph * 2) * g.D + i;
-      T* hi = lo + g.D;
-      if (slot == 0) {
-        *lo = kv;
-        *hi = kv;
-      } else {
-        if (less(kv, *lo)) *lo = kv;
-        if (less(*hi, kv)) *hi = kv;
+  if (lp_ok) phys = pt[(int64_t)b * g.max_pages + lp];
+  for (int base = 0; base < n; base += kPer * blockDim.x) {
+    T kv[kPer], vv[kPer], lo[kPer], hi[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int e = base + threadIdx.x + j * blockDim.x;
+      if (e < n && lp_ok) {
+        const int h = e / g.D, i = e - h * g.D;
+        kv[j] = k_new[(int64_t)b * n + e];
+        vv[j] = v_new[(int64_t)b * n + e];
+        const T* d = dg + ((((int64_t)b * g.hk + h) * g.max_pages + lp) * 2) * g.D + i;
+        if (slot != 0) {
+          lo[j] = d[0];
+          hi[j] = d[g.D];
+        }
       }
     }
+    const bool ok = lp_ok && phys >= 0 && phys < g.num_phys;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int e = base + threadIdx.x + j * blockDim.x;
+      if (e >= n || !ok) continue;
+      const int h = e / g.D, i = e - h * g.D;
+      const int64_t ph = (int64_t)phys * g.hk + h;
+      kc[(ph * g.P + slot) * g.D + i] = kv[j];
+      vc[(ph * g.D + i) * g.P + slot] = vv[j];
+      T* d = dg + ((((int64_t)b * g.hk + h) * g.max_pages + lp) * 2) * g.D + i;
+      if (slot == 0) {
+        d[0] = kv[j];
+        d[g.D] = kv[j];
+      } else {
+        if (less(kv[j], lo[j])) d[0] = kv[j];
+        if (less(hi[j], kv[j])) d[g.D] = kv[j];
+      }
+    }
+  }
+  const bool ok = lp_ok && phys >= 0 && phys < g.num_phys;
+  if (ok)
     for (int h = threadIdx.x; h < g.hk; h += blockDim.x)
       A[((int64_t)b * g.hk + h) * g.max_pages + lp] = step - 1;
-  }
   __syncthreads();
   if (ok && threadIdx.x == 0) seq_lens[b] = pos + 1;
 }
@@ -91,6 +111,7 @@ __global__ void __launch_bounds__(128) prefill_digest_kernel(Geometry g, int seq
   if (phys < 0 || phys >= g.num_phys) return;
   const int filled = min(g.P, end - lp * g.P);
   const int64_t ph = (int64_t)phys * g.hk + h;
+  T* drow = dg + ((((int64_t)seq * g.hk + h) * g.max_pages + lp) * 2) * g.D;
   for (int i = threadIdx.x; i < g.D; i += blockDim.x) {
     T lo = kc[(ph * g.P) * g.D + i], hi = lo;
     for (int s = 1; s < filled; ++s) {
@@ -98,8 +119,8 @@ __global__ void __launch_bounds__(128) prefill_digest_kernel(Geometry g, int seq
       if (less(v, lo)) lo = v;
       if (less(hi, v)) hi = v;
     }
-    dg[(ph * 2) * g.D + i] = lo;
-    dg[(ph * 2 + 1) * g.D + i] = hi;
+    drow[i] = lo;
+    drow[g.D + i] = hi;
   }
 }
 

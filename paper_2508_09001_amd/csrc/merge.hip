@@ -5,19 +5,27 @@
 // evaluated relative to max(Z_a, Z_b); a side with Z = -inf contributes nothing.
 // The same merge combines the per-split partial outputs of one row.
 //
-// Output cache ring: row tau lives in slot tau mod W.  One workgroup per
-// (sequence, query head, row) updates its own slot; rows 0 and W share a slot
-// ((t-W) mod W == t mod W), so one workgroup handles both, reading the slot for
-// row 0 before row W overwrites it.
+// One wavefront per (sequence, query head, row slot); lane l owns elements
+// [l*E, l*E+E) of the d outputs.  Split normalisers are read one per lane and
+// reduced across the wavefront; split outputs and the cache slot are all
+// requested before any is used.
+//
+// Output cache ring: row tau lives in slot tau mod W.  Slot x of a wavefront:
+// x in [1, W) -> row x; x == 0 -> rows 0 and W, which share a slot
+// ((t-W) mod W == t mod W): the slot is read for row 0 before row W overwrites
+// it, in program order of the same lanes.
 #include "internal.h"
 
 namespace retro {
 namespace {
 
+constexpr int kWaves = 4;  // wavefronts (work units) per workgroup
+
 struct MergeArgs {
   Geometry g;
   int step;
   int mode;  // 0: splits -> part; 1: part -> cache; 2: splits -> cache
+  int xs;    // row slots per query head
   const float* o_ws;
   const float* l_ws;
   const int32_t* nsel;
@@ -33,45 +41,71 @@ struct MergeArgs {
 
 template <int D>
 struct Row {
-  static constexpr int E = D / 64;  // elements per thread
+  static constexpr int E = D / 64;
   float o[E];
   float z;
 };
 
-// The partial (O, Z) of row r for this workgroup's query head.
-template <int D>
-__device__ Row<D> partial(const MergeArgs& a, int b, int qh, int r) {
-  const Geometry& g = a.g;
-  Row<D> res;
-  const int e0 = threadIdx.x * Row<D>::E;
-  if (a.mode == 1) {
-    const int64_t idx = ((int64_t)b * (g.W + 1) + r) * g.hq + qh;
+__device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
-    for (int e = 0; e < Row<D>::E; ++e) res.o[e] = a.o_part[idx * D + e0 + e];
-    res.z = a.l_part[idx];
-    return res;
-  }
-  const int h = qh / g.G, gq = qh - h * g.G;
-  const int bh = b * g.hk + h;
-  const int rho = r * g.G + gq;
-  const int nvs = (a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split;
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+
+// Combine the splits of row rho of (b, h): sum_s e^{Z_s} O_s / sum_s e^{Z_s}.
+template <int D>
+__device__ Row<D> combine_splits(const MergeArgs& a, int bh, int rho) {
+  const Geometry& g = a.g;
+  const int lane = threadIdx.x & 63;
+  const int e0 = lane * Row<D>::E;
+  const int nvs = min((a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split, g.n_splits);
   const int64_t base = (int64_t)bh * g.n_splits * g.R + rho;
-  float zmax = -INFINITY;
-  for (int s = 0; s < nvs; ++s) zmax = fmaxf(zmax, a.l_ws[base + (int64_t)s * g.R]);
+  Row<D> res;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) res.o[e] = 0.f;
+  float zmax = -INFINITY;
+  for (int s0 = 0; s0 < nvs; s0 += 64) {
+    const float z = (s0 + lane < nvs) ? a.l_ws[base + (int64_t)(s0 + lane) * g.R] : -INFINITY;
+    zmax = fmaxf(zmax, z);
+  }
+  zmax = wave_max(zmax);
   if (zmax == -INFINITY) {
     res.z = -INFINITY;
     return res;
   }
   float wsum = 0.f;
-  for (int s = 0; s < nvs; ++s) {
-    const int64_t ri = base + (int64_t)s * g.R;
-    const float w = __expf(a.l_ws[ri] - zmax);
+  for (int s0 = 0; s0 < nvs; s0 += 64) {
+    const int s = s0 + lane;
+    const float w = (s < nvs) ? __expf(a.l_ws[base + (int64_t)s * g.R] - zmax) : 0.f;
     wsum += w;
+    const int cnt = min(64, nvs - s0);
+    // 8 split rows in flight at a time
+    for (int j0 = 0; j0 < cnt; j0 += 8) {
+      float v[8][Row<D>::E];
 #pragma unroll
-    for (int e = 0; e < Row<D>::E; ++e) res.o[e] += w * a.o_ws[ri * D + e0 + e];
+      for (int j = 0; j < 8; ++j) {
+        const int ss = s0 + min(j0 + j, cnt - 1);
+#pragma unroll
+        for (int e = 0; e < Row<D>::E; ++e)
+          v[j][e] = a.o_ws[(base + (int64_t)ss * g.R) * D + e0 + e];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float wj = __shfl(w, j0 + j);
+        if (j0 + j < cnt) {
+#pragma unroll
+          for (int e = 0; e < Row<D>::E; ++e) res.o[e] += wj * v[j][e];
+        }
+      }
+    }
   }
+  wsum = wave_sum(wsum);
   const float inv = 1.f / wsum;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) res.o[e] *= inv;
@@ -99,16 +133,16 @@ __device__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
 
 template <int D>
 __device__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
-  const int e0 = threadIdx.x * Row<D>::E;
+  const int e0 = (threadIdx.x & 63) * Row<D>::E;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) o[idx * D + e0 + e] = v.o[e];
-  if (threadIdx.x == 0) z[idx] = v.z;
+  if ((threadIdx.x & 63) == 0) z[idx] = v.z;
 }
 
 template <int D>
 __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
   Row<D> v;
-  const int e0 = threadIdx.x * Row<D>::E;
+  const int e0 = (threadIdx.x & 63) * Row<D>::E;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) v.o[e] = o[idx * D + e0 + e];
   v.z = z[idx];
@@ -116,15 +150,31 @@ __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
 }
 
 template <int D>
-__global__ void __launch_bounds__(64) combine_merge_kernel(MergeArgs a) {
+__device__ Row<D> partial(const MergeArgs& a, int b, int h, int gq, int r) {
+  const Geometry& g = a.g;
+  if (a.mode == 1) return get<D>(a.o_part, a.l_part, ((int64_t)b * (g.W + 1) + r) * g.hq + h * g.G + gq);
+  return combine_splits<D>(a, b * g.hk + h, r * g.G + gq);
+}
+
+template <int D>
+__global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
   const Geometry& g = a.g;
   const int W = g.W;
-  const int x = blockIdx.x, qh = blockIdx.y, b = blockIdx.z;
-  const int64_t out_row = (int64_t)b * (W + 1);  // first row index of this sequence
+  // units ordered (sequence, KV head, query head of the group, row slot), spread
+  // so that a KV head's units share the XCD its attention splits ran on
+  const int nunits = g.batch * g.hq * a.xs;
+  int u = xcd_remap(blockIdx.x, gridDim.x) * kWaves + (threadIdx.x >> 6);
+  if (u >= nunits) return;  // uniform per wavefront; no barrier below
+  const int x = u % a.xs;
+  u /= a.xs;
+  const int gq = u % g.G;
+  u /= g.G;
+  const int h = u % g.hk, b = u / g.hk;
+  const int qh = h * g.G + gq;
+  const int64_t out_row = (int64_t)b * (W + 1);
 
   if (a.mode == 0) {  // plain combine of the splits for row x
-    const Row<D> v = partial<D>(a, b, qh, x);
-    put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, v);
+    put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, partial<D>(a, b, h, gq, x));
     return;
   }
 
@@ -133,30 +183,25 @@ __global__ void __launch_bounds__(64) combine_merge_kernel(MergeArgs a) {
   for (int e = 0; e < Row<D>::E; ++e) zero.o[e] = 0.f;
   zero.z = -INFINITY;
 
-  // rows handled here: x in [1, W) -> row x; x == 0 -> rows 0 and W
-  const int rows[2] = {x, W};
-  const int nrows = (x == 0 && W > 0) ? 2 : 1;
-  for (int k = 0; k < nrows; ++k) {
-    const int r = rows[k];
-    const int tau = a.step - W + r;
-    const int64_t oi = (out_row + r) * g.hq + qh;
-    if (tau < 0) {
-      put<D>(a.o_out, a.l_out, oi, zero);
-      continue;
-    }
-    const Row<D> part = partial<D>(a, b, qh, r);
-    if (r == W) {
-      put<D>(a.o_out, a.l_out, oi, part);
-      if (W > 0) {
-        __syncthreads();  // row 0 of this workgroup has read the shared slot
-        put<D>(a.o_cache, a.l_cache, ((int64_t)b * W + (a.step % W)) * g.hq + qh, part);
-      }
-      continue;
-    }
-    const int64_t ci = ((int64_t)b * W + (tau % W)) * g.hq + qh;
-    const Row<D> merged = lse_merge<D>(get<D>(a.o_cache, a.l_cache, ci), part);
-    put<D>(a.o_out, a.l_out, oi, merged);
-    if (r > 0) put<D>(a.o_cache, a.l_cache, ci, merged);
+  const int r0 = x;
+  const int tau0 = a.step - W + r0;
+  if (r0 == W) {  // W == 0: the current row only
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, partial<D>(a, b, h, gq, r0));
+    return;
+  }
+  if (tau0 < 0) {
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, zero);
+  } else {
+    const int64_t ci = ((int64_t)b * W + (tau0 % W)) * g.hq + qh;
+    const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
+    const Row<D> merged = lse_merge<D>(cached, partial<D>(a, b, h, gq, r0));
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, merged);
+    if (r0 > 0) put<D>(a.o_cache, a.l_cache, ci, merged);
+  }
+  if (r0 == 0) {  // the current row: output, and push into slot t mod W
+    const Row<D> cur = partial<D>(a, b, h, gq, W);
+    put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, cur);
+    put<D>(a.o_cache, a.l_cache, ((int64_t)b * W + (a.step % W)) * g.hq + qh, cur);
   }
 }
 
@@ -171,6 +216,7 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
   a.g = g;
   a.step = step;
   a.mode = mode;
+  a.xs = (mode == 0) ? g.W + 1 : (g.W > 0 ? g.W : 1);
   a.o_ws = o_ws;
   a.l_ws = l_ws;
   a.nsel = num_selected;
@@ -182,12 +228,12 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
   a.l_cache = oc ? oc->lse_cache : nullptr;
   a.o_out = o_out;
   a.l_out = lse_out;
-  const int gx = (mode == 0) ? g.W + 1 : (g.W > 0 ? g.W : 1);
-  dim3 grid(gx, g.hq, g.batch);
+  const int64_t units = (int64_t)g.batch * g.hq * a.xs;
+  const unsigned blocks = (unsigned)((units + kWaves - 1) / kWaves);
   if (g.D == 128)
-    combine_merge_kernel<128><<<grid, 64, 0, s>>>(a);
+    combine_merge_kernel<128><<<blocks, 64 * kWaves, 0, s>>>(a);
   else
-    combine_merge_kernel<64><<<grid, 64, 0, s>>>(a);
+    combine_merge_kernel<64><<<blocks, 64 * kWaves, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -6,9 +6,10 @@
 // index order (pairwise summation), the per-head sums added in head order, and
 // + 0.0f at the end.
 //
-// Layout of the work: a page's digest row (d elements of Kmin, then d of Kmax)
-// is read as 16-byte vectors by LPP = d / VEC consecutive lanes, lane c holding
-// elements [c*VEC, (c+1)*VEC).  The tree's first log2(VEC) levels are in-lane,
+// Layout of the work: digests are stored per logical page, so a KV head's
+// digests form one contiguous stream.  A page's digest row (d elements of Kmin,
+// then d of Kmax) is read as 16-byte vectors by LPP = d / VEC consecutive lanes,
+// lane c holding elements [c*VEC, (c+1)*VEC).  The tree's first log2(VEC) levels are in-lane,
 // the remaining log2(LPP) levels pair neighbouring lanes (xor 1, 2, 4, ...), so
 // the order is the pairwise order over all d terms.  A wavefront covers
 // 64 / LPP pages per iteration; a workgroup of four wavefronts scores a block
@@ -21,11 +22,10 @@ namespace {
 constexpr int kScoreIters = 4;
 
 template <typename T>
-__device__ __forceinline__ void load_vec(const T* p, float* out);
+__device__ __forceinline__ void unpack(const uint4& u, float* out);
 
 template <>
-__device__ __forceinline__ void load_vec<bf16_t>(const bf16_t* p, float* out) {
-  const uint4 u = *reinterpret_cast<const uint4*>(p);
+__device__ __forceinline__ void unpack<bf16_t>(const uint4& u, float* out) {
   const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -35,18 +35,16 @@ __device__ __forceinline__ void load_vec<bf16_t>(const bf16_t* p, float* out) {
 }
 
 template <>
-__device__ __forceinline__ void load_vec<float>(const float* p, float* out) {
-  const float4 u = *reinterpret_cast<const float4*>(p);
-  out[0] = u.x;
-  out[1] = u.y;
-  out[2] = u.z;
-  out[3] = u.w;
+__device__ __forceinline__ void unpack<float>(const uint4& u, float* out) {
+  out[0] = __uint_as_float(u.x);
+  out[1] = __uint_as_float(u.y);
+  out[2] = __uint_as_float(u.z);
+  out[3] = __uint_as_float(u.w);
 }
 
 template <typename T, int D>
 __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restrict__ q,
                                                    int64_t q_bstride, const T* __restrict__ dg,
-                                                   const int32_t* __restrict__ pt,
                                                    const int32_t* __restrict__ seq_lens,
                                                    float* __restrict__ scores) {
 #pragma clang fp contract(off)
@@ -57,32 +55,35 @@ __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restr
   extern __shared__ float sq[];  // [G][D] the group's current queries, as fp32
 
   const int b = blockIdx.z, h = blockIdx.y;
-  const int n_pages = min((seq_lens[b] + g.P - 1) / g.P, g.max_pages);
-  if ((int)blockIdx.x * PPB >= n_pages) return;  // uniform over the workgroup
-
-  const T* qb = q + (int64_t)b * q_bstride + (int64_t)h * g.G * D;
-  for (int e = threadIdx.x; e < g.G * D; e += blockDim.x) sq[e] = to_f32(qb[e]);
-  __syncthreads();
-
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane % LPP;
-#pragma unroll 1
+  // Every load of the block is issued before any is waited on: the digest rows
+  // (in bounds of the [max_pages] row whatever the sequence length), the queries
+  // and the sequence length.
+  const T* drow = dg + ((int64_t)b * g.hk + h) * g.max_pages * 2 * D;
+  uint4 raw[kScoreIters][2];
+#pragma unroll
   for (int it = 0; it < kScoreIters; ++it) {
     const int page = blockIdx.x * PPB + (wave * kScoreIters + it) * PPW + lane / LPP;
-    const bool valid = page < n_pages;
-    float lo[VEC], hi[VEC];
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) lo[v] = hi[v] = 0.f;
-    bool mapped = false;
-    if (valid) {
-      const int phys = pt[(int64_t)b * g.max_pages + page];
-      if (phys >= 0 && phys < g.num_phys) {
-        const T* row = dg + ((int64_t)phys * g.hk + h) * 2 * D + c * VEC;
-        load_vec<T>(row, lo);
-        load_vec<T>(row + D, hi);
-        mapped = true;
-      }
+    if (page < g.max_pages) {
+      const T* row = drow + (int64_t)page * 2 * D + c * VEC;
+      raw[it][0] = *reinterpret_cast<const uint4*>(row);
+      raw[it][1] = *reinterpret_cast<const uint4*>(row + D);
+    } else {
+      raw[it][0] = raw[it][1] = make_uint4(0u, 0u, 0u, 0u);
     }
+  }
+  const T* qb = q + (int64_t)b * q_bstride + (int64_t)h * g.G * D;
+  for (int e = threadIdx.x; e < g.G * D; e += blockDim.x) sq[e] = to_f32(qb[e]);
+  const int n_pages = min((seq_lens[b] + g.P - 1) / g.P, g.max_pages);
+  __syncthreads();
+
+#pragma unroll
+  for (int it = 0; it < kScoreIters; ++it) {
+    const int page = blockIdx.x * PPB + (wave * kScoreIters + it) * PPW + lane / LPP;
+    float lo[VEC], hi[VEC];
+    unpack<T>(raw[it][0], lo);
+    unpack<T>(raw[it][1], hi);
     float S = 0.f;
     for (int gq = 0; gq < g.G; ++gq) {
       float t[VEC];
@@ -102,10 +103,7 @@ __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restr
       for (int m = 1; m < LPP; m *= 2) s = s + __shfl_xor(s, m);
       S = (gq == 0) ? s : S + s;
     }
-    // An unmapped logical page (outside the caller's contract) holds no tokens:
-    // it ranks below every real page.
-    if (valid && c == 0)
-      scores[((int64_t)b * g.hk + h) * g.max_pages + page] = mapped ? S + 0.0f : -INFINITY;
+    if (page < n_pages && c == 0) scores[((int64_t)b * g.hk + h) * g.max_pages + page] = S + 0.0f;
   }
 }
 
@@ -116,8 +114,8 @@ hipError_t score_t(const Geometry& g, const void* q, int64_t qbs, const retro_kv
   constexpr int PPB = 4 * (64 / (D / VEC)) * kScoreIters;
   dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
   const size_t lds = sizeof(float) * g.G * D;
-  score_kernel<T, D><<<grid, 256, lds, s>>>(g, (const T*)q, qbs, (const T*)c.digest, c.page_table,
-                                             c.seq_lens, scores);
+  score_kernel<T, D><<<grid, 256, lds, s>>>(g, (const T*)q, qbs, (const T*)c.digest, c.seq_lens,
+                                             scores);
   return hipGetLastError();
 }
 

@@ -1,24 +1,29 @@
 // PageSelect + UpdateAndBuildMask (Alg. 1, Alg. 2) for one (sequence, KV head) per
-// workgroup of 1024 threads.
+// workgroup.
 //
-// 1. Each thread holds a contiguous run of at most kPer page scores, mapped to
-//    order-preserving 32-bit keys (larger float -> larger key, -0 == +0).
-// 2. Radix select, most significant byte first (four passes of an LDS histogram
-//    plus a suffix scan), finds T, the k-th largest key, and `need`, how many
-//    keys equal to T belong to the top k.
-// 3. Compaction in page order: a page is kept if its key is above T, or equal
-//    to T and among the first `need` such pages (ties go to the lower page
-//    index).  Two block-wide exclusive scans give each kept page its output slot,
+// 1. Each thread owns a contiguous run of logical pages and loads, all at once,
+//    their scores (mapped to order-preserving 32-bit keys: larger float ->
+//    larger key, -0 == +0), their last_loaded values and their page-table
+//    entries.  Loads do not wait for the sequence length: runs are laid out over
+//    the row's max_pages entries, which are all in bounds.
+// 2. Radix select over rel = key - min_key, with 11-bit digits taken from the
+//    top of rel's actual bit length (score keys span a narrow range, so even the
+//    first digit spreads them over the 2048 bins and the LDS histogram atomics
+//    rarely collide).  Each pass histograms the digit of the keys still in the
+//    running, a suffix scan over the bins fixes the digit of T, the k-th
+//    largest key, and `need` becomes the number of keys to take from T's bin.
+//    The search stops as soon as that bin is taken whole or all bits are fixed.
+// 3. Compaction in page order: a page is kept if its rel is above T's prefix,
+//    or ties with it and is among the first `need` such pages (ties go to the
+//    lower page index).  Two block-wide exclusive scans give each kept page its output slot,
 //    so the output is in ascending page order.
 // 4. Alg. 2 for the kept pages: mask = last_loaded[p]; last_loaded[p] = step.
-//    Kept pages are distinct, so every thread updates its own pages.
+//    Kept pages are distinct, so each thread updates its own.  The physical page
+//    of every kept page is written too (for the attention kernel).
 #include "internal.h"
 
 namespace retro {
 namespace {
-
-constexpr int kThreads = 1024;
-constexpr int kPer = 16;  // pages per thread: max_pages <= 16384
 
 __device__ __forceinline__ uint32_t order_key(float s) {
   uint32_t u = __float_as_uint(s);
@@ -26,7 +31,8 @@ __device__ __forceinline__ uint32_t order_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exclusive prefix sum over the workgroup (1024 threads, 16 wavefronts).
+// Exclusive prefix sum over the workgroup.
+template <int NW>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int x = v;
@@ -37,140 +43,170 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* sh) {
   }
   if (lane == 63) sh[wave] = x;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int nw = blockDim.x >> 6;
-    int w = threadIdx.x < nw ? sh[threadIdx.x] : 0;
-    int incl = w;
+  int off = 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o);
-      if (threadIdx.x >= o) incl += y;
-    }
-    if (threadIdx.x < nw) sh[threadIdx.x] = incl - w;
-  }
+  for (int w = 0; w < NW; ++w)
+    if (w < wave) off += sh[w];
   __syncthreads();
-  const int res = x - v + sh[wave];
-  __syncthreads();
-  return res;
+  return off + x - v;
 }
 
-__global__ void __launch_bounds__(kThreads) topk_mask_kernel(Geometry g, int step,
-                                                             const float* __restrict__ scores,
-                                                             const int32_t* __restrict__ seq_lens,
-                                                             int32_t* __restrict__ A,
-                                                             int32_t* __restrict__ selected,
-                                                             int32_t* __restrict__ mask,
-                                                             int32_t* __restrict__ num_selected) {
-  __shared__ uint32_t hist[256];
-  __shared__ int scan_sh[64];
-  __shared__ uint32_t sel_digit, sel_above;
+template <int THREADS, int PER>
+__global__ void __launch_bounds__(THREADS) topk_mask_kernel(Geometry g, int step,
+                                                            const float* __restrict__ scores,
+                                                            const int32_t* __restrict__ seq_lens,
+                                                            const int32_t* __restrict__ pt,
+                                                            int32_t* __restrict__ A,
+                                                            int32_t* __restrict__ selected,
+                                                            int32_t* __restrict__ mask,
+                                                            int32_t* __restrict__ num_selected,
+                                                            int32_t* __restrict__ sel_phys) {
+  constexpr int NW = THREADS / 64;
+  constexpr int NB = 2048;             // bins of an 11-bit digit
+  constexpr int BPT = NB / THREADS;    // bins per thread in the suffix scan
+  __shared__ uint32_t hist[NB];
+  __shared__ int scan_sh[NW];
+  __shared__ uint32_t red_sh[2 * NW];
+  __shared__ uint32_t s_digit, s_above, s_count;
 
   const int bh = blockIdx.x;
   const int b = bh / g.hk;
   const int tid = threadIdx.x;
-  const int n = min((seq_lens[b] + g.P - 1) / g.P, g.max_pages);
-  const int k = min(g.budget / g.P, n);
-  const int per = (n + kThreads - 1) / kThreads;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int per = (g.max_pages + THREADS - 1) / THREADS;
   const int base = tid * per;
   const float* srow = scores + (int64_t)bh * g.max_pages;
+  int32_t* a_row = A + (int64_t)bh * g.max_pages;
+  const int32_t* p_row = pt + (int64_t)b * g.max_pages;
 
-  uint32_t key[kPer];
+  uint32_t key[PER];
+  int32_t a_old[PER], phys[PER];
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
+  for (int j = 0; j < PER; ++j) {
     const int idx = base + j;
-    key[j] = (j < per && idx < n) ? order_key(srow[idx]) : 0u;
+    if (j < per && idx < g.max_pages) {
+      key[j] = order_key(srow[idx]);
+      a_old[j] = a_row[idx];
+      phys[j] = p_row[idx];
+    } else {
+      key[j] = 0u;
+      a_old[j] = -1;
+      phys[j] = -1;
+    }
   }
+  const int n = min((seq_lens[b] + g.P - 1) / g.P, g.max_pages);
+  const int k = min(g.budget / g.P, n);
   auto valid = [&](int j) { return j < per && base + j < n; };
 
-  uint32_t T = 0u;
+  // rel = key - kmin over the valid keys; T is searched among rel values.
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (valid(j)) {
+      kmin = min(kmin, key[j]);
+      kmax = max(kmax, key[j]);
+    }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, m));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, m));
+  }
+  if (lane == 0) {
+    red_sh[wave] = kmin;
+    red_sh[NW + wave] = kmax;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    kmin = min(kmin, red_sh[w]);
+    kmax = max(kmax, red_sh[NW + w]);
+  }
+  const uint32_t range = kmax - kmin;
+  const int nbits = range ? 32 - __clz((int)range) : 1;
+  uint64_t prefix = 0u;  // chosen digits of T's rel, bits [lo, nbits)
+  int lo = nbits;
   int need = k;
   if (k > 0 && k < n) {
-    uint32_t prefix = 0u, pmask = 0u;
 #pragma unroll 1
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      if (tid < 256) hist[tid] = 0u;
+    for (int hi = nbits; hi > 0; hi = lo) {
+      lo = max(hi - 11, 0);
+      const uint32_t dmask = (1u << (hi - lo)) - 1u;
+      for (int i = tid; i < NB; i += THREADS) hist[i] = 0u;
       __syncthreads();
 #pragma unroll
-      for (int j = 0; j < kPer; ++j)
-        if (valid(j) && (key[j] & pmask) == prefix) atomicAdd(&hist[(key[j] >> shift) & 255u], 1u);
+      for (int j = 0; j < PER; ++j) {
+        const uint64_t rel = key[j] - kmin;
+        if (valid(j) && (rel >> hi) == prefix) atomicAdd(&hist[(rel >> lo) & dmask], 1u);
+      }
       __syncthreads();
-      // inclusive scan of hist[255], hist[254], ... gives suffix sums
-      uint32_t hv = 0u, x = 0u;
-      if (tid < 256) {
-        const int lane = tid & 63;
-        hv = hist[255 - tid];
-        x = hv;
+      // suffix scan: thread t owns bins [NB - BPT*(t+1), NB - BPT*t), descending
+      uint32_t local = 0u;
 #pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const uint32_t y = __shfl_up(x, o);
-          if (lane >= o) x += y;
+      for (int i = 0; i < BPT; ++i) local += hist[NB - 1 - (tid * BPT + i)];
+      uint32_t cum = (uint32_t)block_exclusive_scan<NW>((int)local, scan_sh);
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) {
+        const int bin = NB - 1 - (tid * BPT + i);
+        const uint32_t c = hist[bin];
+        if (cum < (uint32_t)need && cum + c >= (uint32_t)need) {
+          s_digit = (uint32_t)bin;
+          s_above = cum;
+          s_count = c;
         }
-        if (lane == 63) scan_sh[tid >> 6] = (int)x;
+        cum += c;
       }
       __syncthreads();
-      if (tid < 256) {
-        uint32_t off = 0u;
-        for (int w = 0; w < (tid >> 6); ++w) off += (uint32_t)scan_sh[w];
-        const uint32_t suffix = x + off;            // keys with digit >= 255 - tid
-        const uint32_t above = suffix - hv;         // keys with digit >  255 - tid
-        if (suffix >= (uint32_t)need && above < (uint32_t)need) {
-          sel_digit = 255u - tid;
-          sel_above = above;
-        }
-      }
-      __syncthreads();
-      need -= (int)sel_above;
-      prefix |= sel_digit << shift;
-      pmask |= 0xFFu << shift;
-      __syncthreads();
+      need -= (int)s_above;
+      prefix = (prefix << (hi - lo)) | s_digit;
+      if ((int)s_count == need) break;  // the whole bin is kept: T's prefix suffices
     }
-    T = prefix;
   }
-
   // compaction in page order
   int c_eq = 0;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j)
-    if (valid(j) && key[j] == T) ++c_eq;
-  const int eq_before = block_exclusive_scan(c_eq, scan_sh);
-  bool take[kPer];
+  for (int j = 0; j < PER; ++j)
+    if (valid(j) && ((uint64_t)(key[j] - kmin) >> lo) == prefix) ++c_eq;
+  const int eq_before = block_exclusive_scan<NW>(c_eq, scan_sh);
+  uint32_t take = 0u;
   int n_take = 0, eq_seen = 0;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
+  for (int j = 0; j < PER; ++j) {
     bool t = false;
     if (valid(j)) {
       if (k >= n) {
         t = true;
       } else if (k > 0) {
-        if (key[j] > T) {
+        const uint64_t km = (uint64_t)(key[j] - kmin) >> lo;
+        if (km > prefix) {
           t = true;
-        } else if (key[j] == T) {
+        } else if (km == prefix) {
           t = (eq_before + eq_seen) < need;
           ++eq_seen;
         }
       }
     }
-    take[j] = t;
+    take |= (t ? 1u : 0u) << j;
     n_take += t ? 1 : 0;
   }
-  int pos = block_exclusive_scan(n_take, scan_sh);
+  int pos = block_exclusive_scan<NW>(n_take, scan_sh);
   int32_t* sel_row = selected + (int64_t)bh * g.k_max;
   int32_t* m_row = mask + (int64_t)bh * g.k_max;
-  int32_t* a_row = A + (int64_t)bh * g.max_pages;
+  int32_t* ph_row = sel_phys ? sel_phys + (int64_t)bh * g.k_max : nullptr;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    if (take[j]) {
+  for (int j = 0; j < PER; ++j) {
+    if (take & (1u << j)) {
       const int p = base + j;
       sel_row[pos] = p;
-      m_row[pos] = a_row[p];
+      m_row[pos] = a_old[j];
       a_row[p] = step;
+      if (ph_row) ph_row[pos] = (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1;
       ++pos;
     }
   }
-  for (int i = k + tid; i < g.k_max; i += kThreads) {
+  for (int i = k + tid; i < g.k_max; i += THREADS) {
     sel_row[i] = -1;
     m_row[i] = -1;
+    if (ph_row) ph_row[i] = -1;
   }
   if (tid == 0) num_selected[bh] = k;
 }
@@ -178,10 +214,17 @@ __global__ void __launch_bounds__(kThreads) topk_mask_kernel(Geometry g, int ste
 }  // namespace
 
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
-                            const retro_kv_cache& c, const retro_selection& sel, hipStream_t s) {
-  topk_mask_kernel<<<g.batch * g.hk, kThreads, 0, s>>>(g, step, scores, c.seq_lens,
-                                                        c.last_loaded, sel.selected, sel.mask,
-                                                        sel.num_selected);
+                            const retro_kv_cache& c, const retro_selection& sel,
+                            int32_t* sel_phys, hipStream_t s) {
+  if (g.max_pages <= 256 * 24) {
+    topk_mask_kernel<256, 24><<<g.batch * g.hk, 256, 0, s>>>(
+        g, step, scores, c.seq_lens, c.page_table, c.last_loaded, sel.selected, sel.mask,
+        sel.num_selected, sel_phys);
+  } else {
+    topk_mask_kernel<1024, 16><<<g.batch * g.hk, 1024, 0, s>>>(
+        g, step, scores, c.seq_lens, c.page_table, c.last_loaded, sel.selected, sel.mask,
+        sel.num_selected, sel_phys);
+  }
   return hipGetLastError();
 }
 

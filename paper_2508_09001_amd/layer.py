@@ -105,6 +105,11 @@ class RetroLayer:
                               self.lse_part, self.workspace, self.ws_bytes, stream)
         self._keep = q_window
 
+    def attend_partials(self, step: int, q_window: torch.Tensor, stream=None) -> None:
+        """Attention kernel only (partials stay in the workspace); q_window on device."""
+        B.retro_decode_attend_partials(self.dims, step, q_window, self.cache, self.sel,
+                                       self.workspace, self.ws_bytes, stream)
+
     def merge(self, step: int, stream=None) -> None:
         B.retro_merge_output_cache(self.dims, step, self.o_part, self.lse_part, self.ocache,
                                    self.o_out, self.lse_out, stream)
