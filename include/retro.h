@@ -211,7 +211,14 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
- * semantics, without materialising o_part / lse_part. */
+ * semantics, without materialising o_part / lse_part.
+ * With RETRO_STEP_FUSED=1 in the environment (read on every call) the step runs
+ * as one launch whose workgroups hand work to each other through counters kept
+ * in `workspace`: the workspace must then be zero-filled once before its first
+ * use, and every such call leaves those counters at zero again on completion.
+ * A workspace is used by one call at a time (calls sharing it are ordered on
+ * one stream).  If a hand-off wait ever exceeds its bound the launch completes
+ * with unspecified outputs instead of hanging. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,

@@ -58,6 +58,12 @@ def load_library(path: str = LIB_PATH):
     global _lib
     if _lib is not None:
         return _lib
+    # PyTorch-ROCm ships its own HIP runtime under the same soname; load it first
+    # so that this library binds to the runtime that owns torch's streams.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it first (__graft_entry__.build())")
     lib = C.CDLL(path)

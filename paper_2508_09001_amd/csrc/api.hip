@@ -1,5 +1,6 @@
 // C ABI entry points: argument validation, geometry and workspace sizing, and the
 // launch sequences of each call.  Nothing here allocates device memory.
+#include <cstdlib>
 #include <math.h>
 
 #include "internal.h"
@@ -69,6 +70,13 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.waves = std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D));
   if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
 
+  x.fA = (x.max_pages + fused_score_pages_per_block(x.dtype, x.D, x.waves) - 1) /
+         fused_score_pages_per_block(x.dtype, x.D, x.waves);
+  x.fC = x.n_rgroups * x.n_splits;
+  x.fD = (x.G * (x.W > 0 ? x.W : 1) + x.waves - 1) / x.waves;
+  x.f_grid = (int64_t)8 * ((bh + 7) / 8) * (x.fA + 1 + x.fC + x.fD);
+  x.fused = fused_supported(x) && x.f_grid < (1LL << 31);
+
   const size_t bhs = (size_t)bh;
   x.ws_scores = 0;
   size_t off = align256(bhs * x.max_pages * sizeof(float));
@@ -78,6 +86,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * x.n_splits * x.R * x.D * sizeof(float));
   x.ws_lpart = off;
   off += align256(bhs * x.n_splits * x.R * sizeof(float));
+  x.ws_ctl = off;
+  off += align256((kCtlCounts + 3 * bhs) * sizeof(int32_t));
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -230,6 +240,19 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
                                               (hipStream_t)stream));
 }
 
+}  // extern "C"
+
+namespace {
+// The single-launch step is chosen with RETRO_STEP_FUSED=1 in the environment
+// (read on every call); otherwise the step runs as five dependent launches.
+bool fused_requested() {
+  const char* v = std::getenv("RETRO_STEP_FUSED");
+  return v && v[0] == '1';
+}
+}  // namespace
+
+extern "C" {
+
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,
@@ -243,6 +266,9 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   if (g.W > 0 && (!ocache || !ocache->o_cache || !ocache->lse_cache)) return RETRO_EINVAL;
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
+  if (g.fused && fused_requested())
+    return from_hip(retro::launch_step_fused(g, step, q_window, k_new, v_new, *cache, *sel, ocache,
+                                             o_out, lse_out, workspace, s));
   float* scores = ws_at(workspace, g.ws_scores);
   float* o_ws = ws_at(workspace, g.ws_opart);
   float* l_ws = ws_at(workspace, g.ws_lpart);

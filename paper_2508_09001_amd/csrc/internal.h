@@ -50,12 +50,29 @@ struct Geometry {
   int tiles_per_group;
   int rtw;            // row tiles per wave
   int waves;          // waves per attention workgroup
+  // fused step plan: tasks per KV head of each role, grid size, availability
+  int fA, fC, fD;
+  int64_t f_grid;
+  bool fused;
   // workspace layout (bytes)
-  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_total;
+  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_total;
 };
+
+// Synchronisation words of the fused step in the workspace (int32 offsets):
+// 8 lane ticket counters kCtlStride apart, the exit counter, a sticky error
+// word (a bounded wait ran out), then per-head counters of the score, top-k and
+// attention roles.  All zero between launches.
+constexpr int kCtlTicket = 0;
+constexpr int kCtlStride = 32;
+constexpr int kCtlExit = 256;
+constexpr int kCtlError = 257;
+constexpr int kCtlCounts = 512;
+constexpr int kFusedScoreIters = 4;
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
 int attend_min_waves(int dtype, int D);
+int fused_score_pages_per_block(int dtype, int D, int waves);
+bool fused_supported(const Geometry& g);
 
 // ---- launchers (return hipSuccess or the launch error) ----
 hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
@@ -70,6 +87,10 @@ hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
                          const retro_kv_cache& c, const retro_selection& sel,
                          const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s);
+hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
+                             const void* v_new, const retro_kv_cache& c,
+                             const retro_selection& sel, const retro_output_cache* oc,
+                             float* o_out, float* lse_out, void* workspace, hipStream_t s);
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
 hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
                                 const float* l_ws, const int32_t* num_selected,

@@ -1,0 +1,1071 @@
+// Device-side building blocks ("roles") of the decode step, shared by the
+// one-phase kernels behind the separate entry points and by the fused step
+// kernel.  Every role uses all threads of its workgroup (any multiple of 64
+// threads unless stated) and takes its LDS from the caller.
+#pragma once
+
+#include "internal.h"
+
+namespace retro {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kMaxPieces = 4;       // 16-byte staging registers per thread per chunk
+constexpr int kMaxSplitPages = 64;  // selected pages per attention split
+
+
+// Order-preserving map of a float to 32 bits: larger float -> larger key; -0 == +0.
+__device__ __forceinline__ uint32_t order_key(float s) {
+  uint32_t u = __float_as_uint(s);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ---- cross-lane moves without the LDS crossbar (DPP, gfx950 permlane swaps)
+template <int CTRL, int ROW_MASK = 0xF, bool BOUND_ZERO = true>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROW_MASK, 0xF, BOUND_ZERO);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppXor1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kDppShl4 = 0x104;      // lane i reads lane i+4 of its 16-lane row
+constexpr int kDppShl8 = 0x108;
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+// Values of the other 16-lane rows at the same column: {even row, odd row} of
+// each row pair, then {rows 0-1, rows 2-3}.
+__device__ __forceinline__ float rows_pair_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+__device__ __forceinline__ float rows_half_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+__device__ __forceinline__ float rows_pair_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+__device__ __forceinline__ float rows_half_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+// max / sum of one column over the four 16-lane rows, in every lane
+__device__ __forceinline__ float col_max4(float x) { return rows_half_max(rows_pair_max(x)); }
+__device__ __forceinline__ float col_sum4(float x) { return rows_half_sum(rows_pair_sum(x)); }
+
+// max / sum over the whole wavefront, in every lane
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmaxf(x, dpp_f<kDppXor1>(x));
+  x = fmaxf(x, dpp_f<kDppXor2>(x));
+  x = fmaxf(x, dpp_f<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp_f<kDppMirror>(x));
+  return col_max4(x);
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x = x + dpp_f<kDppXor1>(x);
+  x = x + dpp_f<kDppXor2>(x);
+  x = x + dpp_f<kDppHalfMirror>(x);
+  x = x + dpp_f<kDppMirror>(x);
+  return col_sum4(x);
+}
+__device__ __forceinline__ uint32_t wave_umin(uint32_t x) {
+  x = min(x, (uint32_t)dpp_i<kDppXor1, 0xF, false>((int)x));
+  x = min(x, (uint32_t)dpp_i<kDppXor2, 0xF, false>((int)x));
+  x = min(x, (uint32_t)dpp_i<kDppHalfMirror, 0xF, false>((int)x));
+  x = min(x, (uint32_t)dpp_i<kDppMirror, 0xF, false>((int)x));
+  auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = min((uint32_t)a[0], (uint32_t)a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return min((uint32_t)b[0], (uint32_t)b[1]);
+}
+__device__ __forceinline__ uint32_t wave_umax(uint32_t x) {
+  x = max(x, (uint32_t)dpp_i<kDppXor1, 0xF, false>((int)x));
+  x = max(x, (uint32_t)dpp_i<kDppXor2, 0xF, false>((int)x));
+  x = max(x, (uint32_t)dpp_i<kDppHalfMirror, 0xF, false>((int)x));
+  x = max(x, (uint32_t)dpp_i<kDppMirror, 0xF, false>((int)x));
+  auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = max((uint32_t)a[0], (uint32_t)a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return max((uint32_t)b[0], (uint32_t)b[1]);
+}
+
+// Inclusive prefix sum over a wavefront: within 16-lane rows (shift right by
+// 1, 2, 4, 8; missing lanes read 0), then across rows (row broadcasts).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += dpp_i<0x111>(x);
+  x += dpp_i<0x112>(x);
+  x += dpp_i<0x114>(x);
+  x += dpp_i<0x118>(x);
+  x += dpp_i<0x142, 0xA, false>(x);  // rows 1, 3 add the last lane of rows 0, 2
+  x += dpp_i<0x143, 0xC, false>(x);  // rows 2, 3 add lane 31
+  return x;
+}
+
+// Exclusive prefix sum over the workgroup (at most 16 wavefronts); sh >= 16 ints.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int x = wave_inclusive_scan(v);
+  if (lane == 63) sh[wave] = x;
+  __syncthreads();
+  int off = 0;
+  for (int w = 0; w < nw; ++w)
+    if (w < wave) off += sh[w];
+  __syncthreads();
+  return off + x - v;
+}
+
+// ============================================================================
+// Score role: eq. (quest_score) for a block of consecutive logical pages of one
+// (sequence, KV head), in the fixed fp32 order (products rounded, pairwise sum
+// over the d terms in index order, head sums in order, + 0.0f).  A page's digest
+// row is read as 16-byte vectors by LPP = d / VEC consecutive lanes, lane c
+// holding elements [c*VEC, (c+1)*VEC): the first log2(VEC) tree levels are
+// in-lane, the rest pair neighbouring lanes (xor 1, 2, ...).
+// ============================================================================
+template <typename T, int D>
+struct ScoreShape {
+  static constexpr int LPP = 16;                    // lanes per page: one DPP row
+  static constexpr int VEC = D / LPP;               // digest elements per lane
+  static constexpr int WORDS = VEC * sizeof(T) / 4; // 32-bit words per lane per digest half
+  static constexpr int PPW = 64 / LPP;              // pages per wavefront and pass
+};
+
+template <int WORDS>
+__device__ __forceinline__ void load_words(const void* p, uint32_t* w) {
+  if constexpr (WORDS == 2) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    w[0] = u.x;
+    w[1] = u.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < WORDS; i += 4) {
+      const uint4 u = reinterpret_cast<const uint4*>(p)[i / 4];
+      w[i] = u.x;
+      w[i + 1] = u.y;
+      w[i + 2] = u.z;
+      w[i + 3] = u.w;
+    }
+  }
+}
+
+template <int WORDS>
+__device__ __forceinline__ void store_words(void* p, const uint32_t* w) {
+  if constexpr (WORDS == 2) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < WORDS; i += 4)
+      reinterpret_cast<uint4*>(p)[i / 4] = make_uint4(w[i], w[i + 1], w[i + 2], w[i + 3]);
+  }
+}
+
+template <typename T, int WORDS>
+__device__ __forceinline__ void words_to_f32(const uint32_t* w, float* out) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < WORDS; ++i) {
+      out[2 * i] = __uint_as_float(w[i] << 16);
+      out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < WORDS; ++i) out[i] = __uint_as_float(w[i]);
+  }
+}
+
+// inverse of words_to_f32 for values exactly representable in T
+template <typename T, int WORDS>
+__device__ __forceinline__ void f32_to_words(const float* in, uint32_t* w) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < WORDS; ++i)
+      w[i] = (__float_as_uint(in[2 * i]) >> 16) | (__float_as_uint(in[2 * i + 1]) & 0xFFFF0000u);
+  } else {
+#pragma unroll
+    for (int i = 0; i < WORDS; ++i) w[i] = __float_as_uint(in[i]);
+  }
+}
+
+// The step's own token, appended by the score block whose pages include it
+// (fused step): AppendKV, the digest update and Alg. 2's first line.
+template <typename T>
+struct StepToken {
+  int lp;            // logical page of the token (-1: none)
+  int slot;          // slot in the page
+  const T* k;        // [d] key of this KV head
+  const T* v;        // [d] value of this KV head
+  T* k_row;          // the slot's key row (token-major page)
+  T* v_col;          // the slot's value column (d-major page): element i at v_col[i * P]
+  int32_t* a_entry;  // last_loaded entry of the page
+  int step;
+};
+
+// Scores pages [page0, page0 + blockDim/64 * PPW * ITERS) of one (sequence, KV
+// head).  A page is handled by one 16-lane row, lane c holding elements
+// [c*VEC, (c+1)*VEC): the first log2(VEC) levels of the pairwise tree are
+// in-lane, the last four pair lane c with c+1, c+2, c+4, c+8 through DPP (the
+// left operand is always the lower index).  tok.lp < 0: no token to append.
+template <typename T, int D, int ITERS>
+__device__ __forceinline__ void score_role(const Geometry& g, int page0, const T* q,
+                                           T* drow, int n_pages, float* srow, float* sq,
+                                           const StepToken<T> tok) {
+#pragma clang fp contract(off)
+  using S = ScoreShape<T, D>;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int c = lane % S::LPP;
+  // every load before any wait: digest rows (in bounds of the [max_pages] row
+  // whatever the sequence length), the queries, the token's key
+  uint32_t raw[ITERS][2][S::WORDS];
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int page = page0 + (wave * ITERS + it) * S::PPW + lane / S::LPP;
+    if (page < g.max_pages) {
+      const T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
+      load_words<S::WORDS>(row, raw[it][0]);
+      load_words<S::WORDS>(row + D, raw[it][1]);
+    } else {
+#pragma unroll
+      for (int w = 0; w < S::WORDS; ++w) raw[it][0][w] = raw[it][1][w] = 0u;
+    }
+  }
+  for (int e = threadIdx.x; e < g.G * D; e += blockDim.x) sq[e] = to_f32(q[e]);
+  const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page0 + nw * S::PPW * ITERS;
+  float kv[S::VEC];
+  if (has_tok) {
+    uint32_t kw[S::WORDS];
+    load_words<S::WORDS>(tok.k + c * S::VEC, kw);
+    words_to_f32<T, S::WORDS>(kw, kv);
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int page = page0 + (wave * ITERS + it) * S::PPW + lane / S::LPP;
+    float lo[S::VEC], hi[S::VEC];
+    words_to_f32<T, S::WORDS>(raw[it][0], lo);
+    words_to_f32<T, S::WORDS>(raw[it][1], hi);
+    if (has_tok && page == tok.lp) {  // widen (or start) the digest with the new key
+#pragma unroll
+      for (int v = 0; v < S::VEC; ++v) {
+        if (tok.slot == 0) {
+          lo[v] = kv[v];
+          hi[v] = kv[v];
+        } else {
+          if (kv[v] < lo[v]) lo[v] = kv[v];
+          if (hi[v] < kv[v]) hi[v] = kv[v];
+        }
+      }
+      T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
+      uint32_t w[S::WORDS];
+      f32_to_words<T, S::WORDS>(lo, w);
+      store_words<S::WORDS>(row, w);
+      f32_to_words<T, S::WORDS>(hi, w);
+      store_words<S::WORDS>(row + D, w);
+    }
+    float Ssum = 0.f;
+    for (int gq = 0; gq < g.G; ++gq) {
+      float t[S::VEC];
+#pragma unroll
+      for (int v = 0; v < S::VEC; ++v) {
+        const float qv = sq[gq * D + c * S::VEC + v];
+        const float a0 = qv * lo[v];
+        const float a1 = qv * hi[v];
+        t[v] = a0 > a1 ? a0 : a1;
+      }
+#pragma unroll
+      for (int w = 1; w < S::VEC; w *= 2)
+#pragma unroll
+        for (int i = 0; i + w < S::VEC; i += 2 * w) t[i] = t[i] + t[i + w];
+      float s = t[0];
+      s = s + dpp_f<kDppXor1>(s);
+      s = s + dpp_f<kDppXor2>(s);
+      s = s + dpp_f<kDppShl4>(s);
+      s = s + dpp_f<kDppShl8>(s);
+      Ssum = (gq == 0) ? s : Ssum + s;
+    }
+    if (page < n_pages && c == 0) srow[page] = Ssum + 0.0f;
+  }
+  if (has_tok) {
+    for (int i = threadIdx.x; i < D; i += blockDim.x) {
+      tok.k_row[i] = tok.k[i];
+      tok.v_col[(int64_t)i * g.P] = tok.v[i];
+    }
+    if (threadIdx.x == 0) *tok.a_entry = tok.step - 1;
+  }
+}
+
+// ============================================================================
+// Top-k + mask role: PageSelect and UpdateAndBuildMask (Alg. 1, Alg. 2) for
+// one (sequence, KV head); see topk.hip for the algorithm.
+// ============================================================================
+struct TopkArgs {
+  Geometry g;
+  int step;
+  const float* scores;
+  const int32_t* pt;
+  int32_t* A;
+  int32_t* selected;
+  int32_t* mask;
+  int32_t* num_selected;
+  int32_t* sel_phys;  // physical ids of the kept pages, or null
+};
+
+constexpr int kTopkBins = 2048;  // bins of an 11-bit digit
+constexpr int kTopkSmall = 64;   // ints of small LDS scratch
+
+// hist: kTopkBins uint32 of LDS; small: kTopkSmall ints of LDS.  n: pages of the
+// sequence.  Needs ceil(max_pages / blockDim.x) <= PER.
+template <int PER>
+__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, uint32_t* hist,
+                                          int* small) {
+  const Geometry& g = ta.g;
+  const int step = ta.step;
+  const float* scores = ta.scores;
+  const int32_t* pt = ta.pt;
+  int32_t* A = ta.A;
+  int32_t* selected = ta.selected;
+  int32_t* mask = ta.mask;
+  int32_t* num_selected = ta.num_selected;
+  int32_t* sel_phys = ta.sel_phys;
+  const int THREADS = blockDim.x;
+  const int NW = THREADS >> 6;
+  constexpr int NB = kTopkBins;
+  const int BPT = (NB + THREADS - 1) / THREADS;  // bins per thread in the suffix scan
+  int* scan_sh = small;                                        // [16]
+  uint32_t* red_sh = reinterpret_cast<uint32_t*>(small + 16);  // [32]
+  uint32_t* s_sel = reinterpret_cast<uint32_t*>(small + 48);   // digit, above, count
+
+  const int b = bh / g.hk;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int per = (g.max_pages + THREADS - 1) / THREADS;
+  const int base = tid * per;
+  const float* srow = scores + (int64_t)bh * g.max_pages;
+  int32_t* a_row = A + (int64_t)bh * g.max_pages;
+  const int32_t* p_row = pt + (int64_t)b * g.max_pages;
+
+  uint32_t key[PER];
+  int32_t a_old[PER], phys[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int idx = base + j;
+    if (j < per && idx < g.max_pages) {
+      key[j] = order_key(srow[idx]);
+      a_old[j] = a_row[idx];
+      phys[j] = p_row[idx];
+    } else {
+      key[j] = 0u;
+      a_old[j] = -1;
+      phys[j] = -1;
+    }
+  }
+  const int k = min(g.budget / g.P, n);
+  auto valid = [&](int j) { return j < per && base + j < n; };
+
+  // rel = key - kmin over the valid keys; T is searched among rel values.
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (valid(j)) {
+      kmin = min(kmin, key[j]);
+      kmax = max(kmax, key[j]);
+    }
+  kmin = wave_umin(kmin);
+  kmax = wave_umax(kmax);
+  if (lane == 0) {
+    red_sh[wave] = kmin;
+    red_sh[16 + wave] = kmax;
+  }
+  __syncthreads();
+  for (int w = 0; w < NW; ++w) {
+    kmin = min(kmin, red_sh[w]);
+    kmax = max(kmax, red_sh[16 + w]);
+  }
+  const uint32_t range = kmax - kmin;
+  const int nbits = range ? 32 - __clz((int)range) : 1;
+  uint64_t prefix = 0u;  // chosen digits of T's rel, bits [lo, nbits)
+  int lo = nbits;
+  int need = k;
+  if (k > 0 && k < n) {
+#pragma unroll 1
+    for (int hi = nbits; hi > 0; hi = lo) {
+      lo = max(hi - 11, 0);
+      const uint32_t dmask = (1u << (hi - lo)) - 1u;
+      for (int i = tid; i < NB; i += THREADS) hist[i] = 0u;
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const uint64_t rel = key[j] - kmin;
+        if (valid(j) && (rel >> hi) == prefix) atomicAdd(&hist[(rel >> lo) & dmask], 1u);
+      }
+      __syncthreads();
+      // suffix scan: thread t owns bins [NB - BPT*(t+1), NB - BPT*t), descending
+      uint32_t local = 0u;
+      for (int i = 0; i < BPT; ++i) {
+        const int bin = NB - 1 - (tid * BPT + i);
+        if (bin >= 0) local += hist[bin];
+      }
+      uint32_t cum = (uint32_t)block_exclusive_scan((int)local, scan_sh);
+      for (int i = 0; i < BPT; ++i) {
+        const int bin = NB - 1 - (tid * BPT + i);
+        if (bin < 0) break;
+        const uint32_t c = hist[bin];
+        if (cum < (uint32_t)need && cum + c >= (uint32_t)need) {
+          s_sel[0] = (uint32_t)bin;
+          s_sel[1] = cum;
+          s_sel[2] = c;
+        }
+        cum += c;
+      }
+      __syncthreads();
+      need -= (int)s_sel[1];
+      prefix = (prefix << (hi - lo)) | s_sel[0];
+      if ((int)s_sel[2] == need) break;  // the whole bin is kept: T's prefix suffices
+    }
+  }
+  // compaction in page order
+  int c_eq = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (valid(j) && ((uint64_t)(key[j] - kmin) >> lo) == prefix) ++c_eq;
+  const int eq_before = block_exclusive_scan(c_eq, scan_sh);
+  uint32_t take = 0u;
+  int n_take = 0, eq_seen = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    bool t = false;
+    if (valid(j)) {
+      if (k >= n) {
+        t = true;
+      } else if (k > 0) {
+        const uint64_t km = (uint64_t)(key[j] - kmin) >> lo;
+        if (km > prefix) {
+          t = true;
+        } else if (km == prefix) {
+          t = (eq_before + eq_seen) < need;
+          ++eq_seen;
+        }
+      }
+    }
+    take |= (t ? 1u : 0u) << j;
+    n_take += t ? 1 : 0;
+  }
+  int pos = block_exclusive_scan(n_take, scan_sh);
+  int32_t* sel_row = selected + (int64_t)bh * g.k_max;
+  int32_t* m_row = mask + (int64_t)bh * g.k_max;
+  int32_t* ph_row = sel_phys ? sel_phys + (int64_t)bh * g.k_max : nullptr;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    if (take & (1u << j)) {
+      const int p = base + j;
+      sel_row[pos] = p;
+      m_row[pos] = a_old[j];
+      a_row[p] = step;
+      if (ph_row) ph_row[pos] = (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1;
+      ++pos;
+    }
+  }
+  for (int i = k + tid; i < g.k_max; i += THREADS) {
+    sel_row[i] = -1;
+    m_row[i] = -1;
+    if (ph_row) ph_row[i] = -1;
+  }
+  if (tid == 0) num_selected[bh] = k;
+}
+
+
+// ============================================================================
+// Attention role (see attend.hip for the design).
+// ============================================================================
+template <typename T, int D>
+struct Tiles {
+  static constexpr int VEC = 16 / sizeof(T);          // elements per 16 bytes
+  static constexpr int KROW = D + VEC;                // padded LDS key row (elements)
+  static constexpr int VROW = 16 + (sizeof(T) == 2 ? 8 : 4);  // padded V^T row
+  static constexpr int K_ELEMS = 32 * KROW;
+  static constexpr int V_ELEMS = 2 * D * VROW;
+  static constexpr int BUF_ELEMS = K_ELEMS + V_ELEMS;
+  static constexpr int KPR = D / VEC;                 // 16-byte pieces per key row
+  static constexpr int VPR = 16 / VEC;                // pieces per 16-token V^T row
+  static constexpr int TPP = VEC;                     // tokens per V piece
+  static constexpr int K_PIECES = 32 * KPR;
+  static constexpr int PIECES = K_PIECES + 2 * D * VPR;
+};
+
+struct AttendArgs {
+  Geometry g;
+  int step;
+  float scale_log2;
+  const void* q;
+  const void* kc;
+  const void* vc;
+  const int32_t* pt;
+  const int32_t* seq_lens;
+  const int32_t* sel;
+  const int32_t* msk;
+  const int32_t* nsel;
+  const int32_t* sel_phys;  // physical ids of the selected pages, or null (page-table lookup)
+  float* o_ws;
+  float* l_ws;
+};
+
+
+// The attention pass of one (sequence, KV head, row group, split).  Row-tile
+// state and the query operands are set up first; `wait()` is then called (the
+// fused step waits there for the page selection), and only then is the page
+// list read.  Uses `lds` (2 * Tiles<T, D>::BUF_ELEMS elements, 16-byte aligned)
+// and three int arrays of kMaxSplitPages entries.  The caller passes the
+// sequence length in effect.
+template <typename T, int D, int RTW, typename Wait>
+__device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
+                                            int seq_len, T* lds, int* s_phys, int* s_page,
+                                            int* s_mask, Wait&& wait) {
+  using TL = Tiles<T, D>;
+  const Geometry& g = a.g;
+  const int bh = b * g.hk + h;
+  const int nthreads = blockDim.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, nwaves = nthreads >> 6;
+  const int ln16 = lane & 15, g4 = lane >> 4;
+
+  // ---- per-row-tile state -------------------------------------------------
+  // Q^T operand: lane holds row (rt*16 + ln16), d elements [kk*32 + 8*g4, +8)
+  // (bf16) or [kq*16 + 4*g4, +4) (f32).
+  constexpr int QREGS = (sizeof(T) == 2) ? D / 32 : D / 16;
+  typedef typename std::conditional<sizeof(T) == 2, bf16x8, f32x4>::type qvec_t;
+  qvec_t qop[RTW][QREGS];
+  f32x4 acc[RTW][D / 16];
+  float m_run[RTW], l_run[RTW];
+  int row_r[RTW], row_tau[RTW];
+  bool row_live[RTW];
+  const int W = g.W;
+#pragma unroll
+  for (int j = 0; j < RTW; ++j) {
+    const int lt = wave + j * nwaves;
+    const int rt = rg * g.tiles_per_group + lt;
+    const int rho = rt * 16 + ln16;
+    const bool live = lt < g.tiles_per_group && rt < g.row_tiles && rho < g.R;
+    const int r = live ? rho / g.G : 0;
+    const int gq = live ? rho - r * g.G : 0;
+    const int tau = a.step - W + r;
+    row_r[j] = r;
+    row_tau[j] = tau;
+    row_live[j] = live && tau >= 0;
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) acc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const T* qrow = reinterpret_cast<const T*>(a.q) +
+                    (((int64_t)b * (W + 1) + r) * g.hq + (int64_t)h * g.G + gq) * D;
+#pragma unroll
+    for (int kk = 0; kk < QREGS; ++kk) {
+      if constexpr (sizeof(T) == 2) {
+        bf16x8 v;
+        if (live) {
+          v = *reinterpret_cast<const bf16x8*>(qrow + kk * 32 + 8 * g4);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = (__bf16)0.f;
+        }
+        qop[j][kk] = v;
+      } else {
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (live) v = *reinterpret_cast<const f32x4*>(qrow + kk * 16 + 4 * g4);
+        qop[j][kk] = v;
+      }
+    }
+  }
+  wait();
+  const int k_eff = a.nsel[bh];
+  const int first = split * g.pages_per_split;
+  const int np = min(g.pages_per_split, k_eff - first);
+  if (np <= 0) return;  // uniform: nothing selected in this split
+  const int nchunks = (np + g.chunk_pages - 1) / g.chunk_pages;
+  for (int i = tid; i < np; i += nthreads) {
+    const int lp = a.sel[(int64_t)bh * g.k_max + first + i];
+    int phys = -1;
+    if (a.sel_phys) {
+      phys = a.sel_phys[(int64_t)bh * g.k_max + first + i];
+    } else if (lp >= 0 && lp < g.max_pages) {
+      phys = a.pt[(int64_t)b * g.max_pages + lp];
+    }
+    if (lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
+    s_phys[i] = phys;
+    s_page[i] = lp;
+    s_mask[i] = a.msk[(int64_t)bh * g.k_max + first + i];
+  }
+
+  __syncthreads();  // page list ready
+
+  // ---- chunk staging: global -> registers -> LDS ----------------------------
+  const int pieces_per_thread = (TL::PIECES + nthreads - 1) / nthreads;
+  // Chunks whose loads are in flight ahead of the computation: two when a
+  // wavefront owns one row tile, one when it owns two (register budget).
+  constexpr int DEPTH = RTW == 1 ? 2 : 1;
+  uint4 stage[DEPTH][kMaxPieces];
+  const T* kc = reinterpret_cast<const T*>(a.kc);
+  const T* vc = reinterpret_cast<const T*>(a.vc);
+
+  auto tile_page = [&](int c, int tile, int* slot_off) -> int {
+    // split-local page index of a 16-token tile of chunk c, and its slot offset
+    if (g.chunk_pages == 2) {
+      *slot_off = 0;
+      return 2 * c + tile;
+    }
+    *slot_off = 16 * tile;
+    return c;
+  };
+
+  auto load_chunk = [&](int c, uint4* stage) {
+#pragma unroll
+    for (int i = 0; i < kMaxPieces; ++i) {
+      const int e = tid + i * nthreads;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (i < pieces_per_thread && e < TL::PIECES) {
+        if (e < TL::K_PIECES) {
+          const int tok = e / TL::KPR, q = e - tok * TL::KPR;
+          const int tile = tok >> 4;
+          int so;
+          const int pl = tile_page(c, tile, &so);
+          const int slot = so + (tok & 15);
+          if (pl < np && s_phys[pl] >= 0 && s_page[pl] * g.P + slot < seq_len) {
+            const T* src = kc + (((int64_t)s_phys[pl] * g.hk + h) * g.P + slot) * D + q * TL::VEC;
+            v = *reinterpret_cast<const uint4*>(src);
+          }
+        } else {
+          const int ev = e - TL::K_PIECES;
+          const int tile = ev / (D * TL::VPR);
+          const int rem = ev - tile * (D * TL::VPR);
+          const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
+          int so;
+          const int pl = tile_page(c, tile, &so);
+          if (pl < np && s_phys[pl] >= 0) {
+            const int slot0 = so + q * TL::TPP;
+            const int valid = seq_len - (s_page[pl] * g.P + slot0);  // stored tokens in piece
+            if (valid > 0) {
+              const T* src = vc + (((int64_t)s_phys[pl] * g.hk + h) * D + dr) * g.P + slot0;
+              v = *reinterpret_cast<const uint4*>(src);
+              if (valid < TL::TPP) {  // zero the unstored tail of the piece
+                uint32_t w[4] = {v.x, v.y, v.z, v.w};
+                if constexpr (sizeof(T) == 2) {
+#pragma unroll
+                  for (int t = 0; t < 8; ++t)
+                    if (t >= valid) w[t >> 1] &= (t & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+                } else {
+#pragma unroll
+                  for (int t = 0; t < 4; ++t)
+                    if (t >= valid) w[t] = 0u;
+                }
+                v = make_uint4(w[0], w[1], w[2], w[3]);
+              }
+            }
+          }
+        }
+      }
+      stage[i] = v;
+    }
+  };
+
+  auto store_chunk = [&](int buf, const uint4* stage) {
+    T* base = lds + buf * TL::BUF_ELEMS;
+#pragma unroll
+    for (int i = 0; i < kMaxPieces; ++i) {
+      const int e = tid + i * nthreads;
+      if (i < pieces_per_thread && e < TL::PIECES) {
+        T* dst;
+        if (e < TL::K_PIECES) {
+          const int tok = e / TL::KPR, q = e - tok * TL::KPR;
+          dst = base + tok * TL::KROW + q * TL::VEC;
+        } else {
+          const int ev = e - TL::K_PIECES;
+          const int tile = ev / (D * TL::VPR);
+          const int rem = ev - tile * (D * TL::VPR);
+          const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
+          dst = base + TL::K_ELEMS + (tile * D + dr) * TL::VROW + q * TL::TPP;
+        }
+        *reinterpret_cast<uint4*>(dst) = stage[i];
+      }
+    }
+  };
+
+  auto compute_chunk = [&](int c, int buf) {
+    const T* Ks = lds + buf * TL::BUF_ELEMS;
+    const T* Vs = Ks + TL::K_ELEMS;
+
+    // page facts for the two tiles of this chunk
+    bool tvalid[2];
+    int tmask[2], tbase[2];
+#pragma unroll
+    for (int tile = 0; tile < 2; ++tile) {
+      int so;
+      const int pl = tile_page(c, tile, &so);
+      tvalid[tile] = pl < np && s_phys[pl] >= 0;
+      tmask[tile] = tvalid[tile] ? s_mask[pl] : 0;
+      tbase[tile] = tvalid[tile] ? s_page[pl] * g.P + so : 0;  // position of tile slot 0
+    }
+
+#pragma unroll
+    for (int j = 0; j < RTW; ++j) {
+      const int lt = wave + j * nwaves;
+      if (lt >= g.tiles_per_group || rg * g.tiles_per_group + lt >= g.row_tiles) break;  // uniform
+
+      // ---- S^T = K . Q^T for both tiles
+      f32x4 s[2];
+#pragma unroll
+      for (int tile = 0; tile < 2; ++tile) {
+        f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+        const T* krow = Ks + (tile * 16 + ln16) * TL::KROW;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int kk = 0; kk < D / 32; ++kk) {
+            const bf16x8 kv = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 8 * g4);
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qop[j][kk], sacc, 0, 0, 0);
+          }
+        } else {
+#pragma unroll
+          for (int kq = 0; kq < D / 16; ++kq) {
+            const f32x4 kv = *reinterpret_cast<const f32x4*>(krow + kq * 16 + 4 * g4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[e], qop[j][kq][e], sacc, 0, 0, 0);
+          }
+        }
+        s[tile] = sacc;
+      }
+
+      // ---- mask, scale, online softmax (this lane: row ln16 of the tile)
+      float x[2][4];
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int tile = 0; tile < 2; ++tile) {
+        const bool use = row_live[j] && tvalid[tile] &&
+                         (row_r[j] == W || tmask[tile] < row_tau[j]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool ok = use && (tbase[tile] + 4 * g4 + i) < seq_len;
+          x[tile][i] = ok ? s[tile][i] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, x[tile][i]);
+        }
+      }
+      mloc = col_max4(mloc);
+      const float m_new = fmaxf(m_run[j], mloc);
+      const float mu = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = exp2f(m_run[j] - mu);
+      float p[2][4];
+      float psum = 0.f;
+#pragma unroll
+      for (int tile = 0; tile < 2; ++tile)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          p[tile][i] = exp2f(x[tile][i] - mu);
+          psum += p[tile][i];
+        }
+      l_run[j] = l_run[j] * alpha + psum;
+      m_run[j] = m_new;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[j][dt] *= alpha;
+
+      // ---- O^T += V^T . P^T
+      if constexpr (sizeof(T) == 2) {
+        bf16x8 ph, pl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = p[e >> 2][e & 3];
+          const __bf16 hi = (__bf16)pv;
+          ph[e] = hi;
+          pl[e] = (__bf16)(pv - (float)hi);
+        }
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) {
+          const int dr = dt * 16 + ln16;
+          const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(Vs + dr * TL::VROW + 4 * g4);
+          const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(Vs + (D + dr) * TL::VROW + 4 * g4);
+          const bf16x8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+          acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, acc[j][dt], 0, 0, 0);
+          acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, acc[j][dt], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) {
+          const int dr = dt * 16 + ln16;
+#pragma unroll
+          for (int tile = 0; tile < 2; ++tile) {
+            const f32x4 vv = *reinterpret_cast<const f32x4*>(Vs + (tile * D + dr) * TL::VROW + 4 * g4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[e], p[tile][e], acc[j][dt], 0, 0, 0);
+          }
+        }
+      }
+    }
+
+  };
+
+  // Chunk c goes through LDS buffer c & 1.  That buffer was last read while
+  // computing chunk c - 2, and every wavefront has since passed the barrier of
+  // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
+  // compile-time constants (two chunks per trip when DEPTH == 2).
+  if constexpr (DEPTH == 2) {
+    load_chunk(0, stage[0]);
+    if (nchunks > 1) load_chunk(1, stage[DEPTH - 1]);
+#pragma unroll 1
+    for (int c = 0; c < nchunks; c += 2) {
+      store_chunk(0, stage[0]);
+      if (c + 2 < nchunks) load_chunk(c + 2, stage[0]);
+      __syncthreads();
+      compute_chunk(c, 0);
+      if (c + 1 < nchunks) {
+        store_chunk(1, stage[DEPTH - 1]);
+        if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1]);
+        __syncthreads();
+        compute_chunk(c + 1, 1);
+      }
+    }
+  } else {
+    load_chunk(0, stage[0]);
+#pragma unroll 1
+    for (int c = 0; c < nchunks; ++c) {
+      store_chunk(c & 1, stage[0]);
+      if (c + 1 < nchunks) load_chunk(c + 1, stage[0]);
+      __syncthreads();
+      compute_chunk(c, c & 1);
+    }
+  }
+
+  // ---- normalise and write this split's partial (O, LSE) per row -------------
+  const int64_t part = ((int64_t)bh * g.n_splits + split) * g.R;
+#pragma unroll
+  for (int j = 0; j < RTW; ++j) {
+    const int lt = wave + j * nwaves;
+    const int rt = rg * g.tiles_per_group + lt;
+    if (lt >= g.tiles_per_group || rt >= g.row_tiles) break;
+    const float l = col_sum4(l_run[j]);
+    const int rho = rt * 16 + ln16;
+    if (rho < g.R) {
+      const float inv = l > 0.f ? 1.f / l : 0.f;
+      float* orow = a.o_ws + (part + rho) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const f32x4 o = acc[j][dt] * inv;
+        *reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4) = o;
+      }
+      if (g4 == 0) a.l_ws[part + rho] = l > 0.f ? (m_run[j] + __log2f(l)) * kLn2 : -INFINITY;
+    }
+  }
+}
+
+// ============================================================================
+// Combine + merge role (see merge.hip for the design).
+// ============================================================================
+struct MergeArgs {
+  Geometry g;
+  int step;
+  int mode;  // 0: splits -> part; 1: part -> cache; 2: splits -> cache
+  int xs;    // row slots per query head
+  const float* o_ws;
+  const float* l_ws;
+  const int32_t* nsel;
+  const float* o_part;
+  const float* l_part;
+  float* o_part_out;
+  float* l_part_out;
+  float* o_cache;
+  float* l_cache;
+  float* o_out;
+  float* l_out;
+};
+
+template <int D>
+struct Row {
+  static constexpr int E = D / 64;
+  float o[E];
+  float z;
+};
+
+// Combine the splits of row rho of (b, h): sum_s e^{Z_s} O_s / sum_s e^{Z_s}.
+template <int D>
+__device__ Row<D> combine_splits(const MergeArgs& a, int bh, int rho) {
+  const Geometry& g = a.g;
+  const int lane = threadIdx.x & 63;
+  const int e0 = lane * Row<D>::E;
+  const int nvs = min((a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split, g.n_splits);
+  const int64_t base = (int64_t)bh * g.n_splits * g.R + rho;
+  Row<D> res;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) res.o[e] = 0.f;
+  float zmax = -INFINITY;
+  for (int s0 = 0; s0 < nvs; s0 += 64) {
+    const float z = (s0 + lane < nvs) ? a.l_ws[base + (int64_t)(s0 + lane) * g.R] : -INFINITY;
+    zmax = fmaxf(zmax, z);
+  }
+  zmax = wave_max(zmax);
+  if (zmax == -INFINITY) {
+    res.z = -INFINITY;
+    return res;
+  }
+  float wsum = 0.f;
+  for (int s0 = 0; s0 < nvs; s0 += 64) {
+    const int s = s0 + lane;
+    const float w = (s < nvs) ? __expf(a.l_ws[base + (int64_t)s * g.R] - zmax) : 0.f;
+    wsum += w;
+    const int cnt = min(64, nvs - s0);
+    // 8 split rows in flight at a time
+    for (int j0 = 0; j0 < cnt; j0 += 8) {
+      float v[8][Row<D>::E];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int ss = s0 + min(j0 + j, cnt - 1);
+#pragma unroll
+        for (int e = 0; e < Row<D>::E; ++e)
+          v[j][e] = a.o_ws[(base + (int64_t)ss * g.R) * D + e0 + e];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j0 + j));
+        if (j0 + j < cnt) {
+#pragma unroll
+          for (int e = 0; e < Row<D>::E; ++e) res.o[e] += wj * v[j][e];
+        }
+      }
+    }
+  }
+  wsum = wave_sum(wsum);
+  const float inv = 1.f / wsum;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) res.o[e] *= inv;
+  res.z = zmax + __logf(wsum);
+  return res;
+}
+
+template <int D>
+__device__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
+  Row<D> r;
+  const float m = fmaxf(x.z, y.z);
+  if (m == -INFINITY) {
+#pragma unroll
+    for (int e = 0; e < Row<D>::E; ++e) r.o[e] = 0.f;
+    r.z = -INFINITY;
+    return r;
+  }
+  const float wa = __expf(x.z - m), wb = __expf(y.z - m);
+  const float inv = 1.f / (wa + wb);
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) r.o[e] = (wa * x.o[e] + wb * y.o[e]) * inv;
+  r.z = m + __logf(wa + wb);
+  return r;
+}
+
+template <int D>
+__device__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
+  const int e0 = (threadIdx.x & 63) * Row<D>::E;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) o[idx * D + e0 + e] = v.o[e];
+  if ((threadIdx.x & 63) == 0) z[idx] = v.z;
+}
+
+template <int D>
+__device__ Row<D> get(const float* o, const float* z, int64_t idx) {
+  Row<D> v;
+  const int e0 = (threadIdx.x & 63) * Row<D>::E;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) v.o[e] = o[idx * D + e0 + e];
+  v.z = z[idx];
+  return v;
+}
+
+template <int D>
+__device__ Row<D> partial(const MergeArgs& a, int b, int h, int gq, int r) {
+  const Geometry& g = a.g;
+  if (a.mode == 1) return get<D>(a.o_part, a.l_part, ((int64_t)b * (g.W + 1) + r) * g.hq + h * g.G + gq);
+  return combine_splits<D>(a, b * g.hk + h, r * g.G + gq);
+}
+
+// One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
+// executed by one wavefront; no barriers inside.
+template <int D>
+__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
+  const Geometry& g = a.g;
+  const int W = g.W;
+  int u = unit;
+  const int x = u % a.xs;
+  u /= a.xs;
+  const int gq = u % g.G;
+  u /= g.G;
+  const int h = u % g.hk, b = u / g.hk;
+  const int qh = h * g.G + gq;
+  const int64_t out_row = (int64_t)b * (W + 1);
+
+  if (a.mode == 0) {  // plain combine of the splits for row x
+    put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, partial<D>(a, b, h, gq, x));
+    return;
+  }
+
+  Row<D> zero;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) zero.o[e] = 0.f;
+  zero.z = -INFINITY;
+
+  const int r0 = x;
+  const int tau0 = a.step - W + r0;
+  if (r0 == W) {  // W == 0: the current row only
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, partial<D>(a, b, h, gq, r0));
+    return;
+  }
+  if (tau0 < 0) {
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, zero);
+  } else {
+    const int64_t ci = ((int64_t)b * W + (tau0 % W)) * g.hq + qh;
+    const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
+    const Row<D> merged = lse_merge<D>(cached, partial<D>(a, b, h, gq, r0));
+    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, merged);
+    if (r0 > 0) put<D>(a.o_cache, a.l_cache, ci, merged);
+  }
+  if (r0 == 0) {  // the current row: output, and push into slot t mod W
+    const Row<D> cur = partial<D>(a, b, h, gq, W);
+    put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, cur);
+    put<D>(a.o_cache, a.l_cache, ((int64_t)b * W + (a.step % W)) * g.hq + qh, cur);
+  }
+}
+
+// ============================================================================
+// Cross-workgroup hand-off for the fused step.
+// Producer: every wavefront waits until its own stores have completed (a bare
+// barrier does not wait for them), the workgroup meets at a barrier, and one
+// thread adds 1 to the counter with release semantics (which writes the L2 back
+// once).  Consumer: thread 0 polls the counter with relaxed device-coherent
+// loads (an acquire on every poll would invalidate the L2 each time), then
+// issues one acquire fence and releases the workgroup through a barrier.
+// Polling is bounded: past the limit the error word is set and the consumer
+// goes on, so no wait can hang.
+// ============================================================================
+constexpr int kSpinLimit = 1 << 20;  // polls of about 0.5 us each
+
+__device__ __forceinline__ void block_wait(const int32_t* ctr, int target, int32_t* err) {
+  if (threadIdx.x == 0) {
+    int it = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++it > kSpinLimit) {
+        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void block_signal(int32_t* ctr) {
+  __builtin_amdgcn_s_waitcnt(0);  // this wavefront's stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace retro
