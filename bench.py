@@ -33,7 +33,8 @@ if ROOT not in sys.path:
 
 METRIC = "retro_step µs/layer/decode-step + effective HBM GB/s (% peak), 32K ctx B=2048 W=16"
 PEAK_HBM_GBS = 8000.0
-ATTEND_SRC = os.path.join(ROOT, "paper_2508_09001_amd", "csrc", "attend.hip")
+ATTEND_SRC = [os.path.join(ROOT, "paper_2508_09001_amd", "csrc", f)
+              for f in ("attend.hip", "roles.h", "internal.h")]
 COUNTERS = os.path.join(ROOT, "profiles", "attend_kernel_llama3-8b-32k_counters.json")
 
 
@@ -53,9 +54,12 @@ def _args():
     return p.parse_args()
 
 
-def _sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def _sha(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def algorithmic_bytes(spec, seq_lens, num_selected):
@@ -77,12 +81,14 @@ def algorithmic_bytes(spec, seq_lens, num_selected):
 
 
 def _calib_copy():
+    """A plain elementwise kernel that reads n bytes and writes n bytes: the
+    reference for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
     import torch
     n = 512 << 20
-    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     for _ in range(3):
-        dst.copy_(src)
+        torch.neg(src, out=dst)
     torch.cuda.synchronize()
     print(json.dumps({"calib_copy_bytes": n, "launches": 3}))
 
@@ -196,7 +202,7 @@ def main():
     if os.path.exists(COUNTERS):
         with open(COUNTERS) as f:
             cnt = json.load(f)
-        if cnt.get("attend_source_sha256") == _sha(ATTEND_SRC):
+        if cnt.get("source_sha256") == _sha(ATTEND_SRC):
             traffic = cnt.get("hbm_bytes_per_launch")
 
     result = {

@@ -189,7 +189,8 @@ retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   float* scores = ws_at(workspace, g.ws_scores);
-  hipError_t e = retro::launch_score(g, q_cur, (int64_t)g.hq * g.D, *cache, scores, s);
+  hipError_t e = retro::launch_score(g, step, q_cur, (int64_t)g.hq * g.D, *cache, nullptr, nullptr,
+                                     scores, s);
   if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, nullptr, s);
   return from_hip(e);
 }
@@ -209,7 +210,7 @@ retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const voi
   hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, nullptr, o_ws, l_ws, s);
   if (e == hipSuccess)
     e = retro::launch_combine_merge(g, step, 0, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
-                                    o_part, lse_part, nullptr, nullptr, nullptr, s);
+                                    o_part, lse_part, nullptr, nullptr, nullptr, nullptr, s);
   return from_hip(e);
 }
 
@@ -237,7 +238,7 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
   if (g.W > 0 && (!ocache || !ocache->o_cache || !ocache->lse_cache)) return RETRO_EINVAL;
   return from_hip(retro::launch_combine_merge(g, step, 1, nullptr, nullptr, nullptr, o_part,
                                               lse_part, nullptr, nullptr, ocache, o_out, lse_out,
-                                              (hipStream_t)stream));
+                                              nullptr, (hipStream_t)stream));
 }
 
 }  // extern "C"
@@ -275,14 +276,17 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   const int64_t qbs = (int64_t)(g.W + 1) * g.hq * g.D;
   const char* q_cur = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
-  hipError_t e = retro::launch_append(g, step, *cache, k_new, v_new, s);
-  if (e == hipSuccess) e = retro::launch_score(g, q_cur, qbs, *cache, scores, s);
-  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, phys, s);
+  // score (+ the token's append) -> top-k + mask -> attention -> combine + merge
+  // (+ seq_lens advance)
+  Geometry gp = g;
+  gp.token_pending = 1;
+  hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores, s);
+  if (e == hipSuccess) e = retro::launch_topk_mask(gp, step, scores, *cache, *sel, phys, s);
   if (e == hipSuccess)
-    e = retro::launch_attend(g, step, q_window, *cache, *sel, phys, o_ws, l_ws, s);
+    e = retro::launch_attend(gp, step, q_window, *cache, *sel, phys, o_ws, l_ws, s);
   if (e == hipSuccess)
-    e = retro::launch_combine_merge(g, step, 2, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
-                                    nullptr, nullptr, ocache, o_out, lse_out, s);
+    e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
+                                    nullptr, nullptr, ocache, o_out, lse_out, cache, s);
   return from_hip(e);
 }
 

@@ -56,6 +56,10 @@ struct Geometry {
   bool fused;
   // workspace layout (bytes)
   size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_total;
+  // set for the launches of a step whose token is written by its score launch:
+  // seq_lens does not count the token yet (the merge launch advances it), and
+  // every launch uses the length with the token
+  int token_pending;
 };
 
 // Synchronisation words of the fused step in the workspace (int32 offsets):
@@ -79,8 +83,11 @@ hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, c
                          const void* v_new, hipStream_t s);
 hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
                           const void* k_src, const void* v_src, hipStream_t s);
-hipError_t launch_score(const Geometry& g, const void* q_cur, int64_t q_batch_stride,
-                        const retro_kv_cache& c, float* scores, hipStream_t s);
+// With g.token_pending, the score launch also appends the step's token
+// (k_new, v_new: [batch][h_k][d]) as AppendKV does, without advancing seq_lens.
+hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t q_batch_stride,
+                        const retro_kv_cache& c, const void* k_new, const void* v_new,
+                        float* scores, hipStream_t s);
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
                             const retro_kv_cache& c, const retro_selection& sel,
                             int32_t* sel_phys, hipStream_t s);
@@ -92,10 +99,12 @@ hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, 
                              const retro_selection& sel, const retro_output_cache* oc,
                              float* o_out, float* lse_out, void* workspace, hipStream_t s);
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
+// With g.token_pending and a cache, the launch also advances seq_lens past the
+// step's token (when its page is mapped).
 hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
                                 const float* l_ws, const int32_t* num_selected,
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
-                                float* lse_out, hipStream_t s);
+                                float* lse_out, const retro_kv_cache* cache, hipStream_t s);
 
 }  // namespace retro

@@ -26,6 +26,13 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   // units ordered (sequence, KV head, query head of the group, row slot), spread
   // so that a KV head's units share the XCD its attention splits ran on
   const Geometry& g = a.g;
+  if (blockIdx.x == 0 && g.token_pending && a.seq_lens) {
+    // no other workgroup of this launch reads seq_lens
+    for (int b = threadIdx.x; b < g.batch; b += blockDim.x) {
+      const int pos = a.seq_lens[b];
+      if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
+    }
+  }
   const int nunits = g.batch * g.hq * a.xs;
   const int u = xcd_remap(blockIdx.x, gridDim.x) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
@@ -54,6 +61,8 @@ MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_
   a.l_cache = oc ? oc->lse_cache : nullptr;
   a.o_out = o_out;
   a.l_out = lse_out;
+  a.seq_lens = nullptr;
+  a.pt = nullptr;
   return a;
 }
 
@@ -61,9 +70,13 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
                                 const float* l_ws, const int32_t* num_selected,
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
-                                float* lse_out, hipStream_t s) {
-  const MergeArgs a = make_merge_args(g, step, mode, o_ws, l_ws, num_selected, o_part, l_part,
-                                      o_part_out, l_part_out, oc, o_out, lse_out);
+                                float* lse_out, const retro_kv_cache* cache, hipStream_t s) {
+  MergeArgs a = make_merge_args(g, step, mode, o_ws, l_ws, num_selected, o_part, l_part,
+                                o_part_out, l_part_out, oc, o_out, lse_out);
+  if (cache) {
+    a.seq_lens = cache->seq_lens;
+    a.pt = cache->page_table;
+  }
   const int64_t units = (int64_t)g.batch * g.hq * a.xs;
   const unsigned blocks = (unsigned)((units + kWaves - 1) / kWaves);
   if (g.D == 128)

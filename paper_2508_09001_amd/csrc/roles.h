@@ -206,6 +206,45 @@ struct StepToken {
   int step;
 };
 
+// Physical page that receives the token at position pos of sequence b, or -1
+// when its logical page is out of range or unmapped (the token is then skipped).
+__device__ __forceinline__ int token_phys(const Geometry& g, const int32_t* pt, int b, int pos) {
+  const int lp = pos / g.P;
+  if (pos < 0 || lp >= g.max_pages) return -1;
+  const int phys = pt[(int64_t)b * g.max_pages + lp];
+  return (phys >= 0 && phys < g.num_phys) ? phys : -1;
+}
+
+// Length of sequence b during the step: seq_lens[b], plus the step's token
+// when it is still pending (see Geometry::token_pending) and will be stored.
+__device__ __forceinline__ int live_seq_len(const Geometry& g, const int32_t* seq_lens,
+                                            const int32_t* pt, int b) {
+  const int pos = seq_lens[b];
+  return (g.token_pending && token_phys(g, pt, b, pos) >= 0) ? pos + 1 : pos;
+}
+
+// The token of KV head h of sequence b at position pos, stored in physical page
+// phys (>= 0), as the score role appends it.
+template <typename T>
+__device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int step, int b, int h,
+                                                        int pos, int phys, const void* k_new,
+                                                        const void* v_new, void* kc, void* vc,
+                                                        int32_t* A) {
+  const int lp = pos / g.P, slot = pos - lp * g.P;
+  const int64_t bh = (int64_t)b * g.hk + h;
+  const int64_t ph = (int64_t)phys * g.hk + h;
+  StepToken<T> tk;
+  tk.lp = lp;
+  tk.slot = slot;
+  tk.k = reinterpret_cast<const T*>(k_new) + bh * g.D;
+  tk.v = reinterpret_cast<const T*>(v_new) + bh * g.D;
+  tk.k_row = reinterpret_cast<T*>(kc) + (ph * g.P + slot) * g.D;
+  tk.v_col = reinterpret_cast<T*>(vc) + ph * g.D * g.P + slot;
+  tk.a_entry = A + bh * g.max_pages + lp;
+  tk.step = step;
+  return tk;
+}
+
 // Scores pages [page0, page0 + blockDim/64 * PPW * ITERS) of one (sequence, KV
 // head).  A page is handled by one 16-lane row, lane c holding elements
 // [c*VEC, (c+1)*VEC): the first log2(VEC) levels of the pairwise tree are
@@ -316,57 +355,58 @@ struct TopkArgs {
   int32_t* sel_phys;  // physical ids of the kept pages, or null
 };
 
-constexpr int kTopkBins = 2048;  // bins of an 11-bit digit
-constexpr int kTopkSmall = 64;   // ints of small LDS scratch
+constexpr int kTopkBins = 2048;    // bins of an 11-bit digit
+constexpr int kTopkPasses = 3;     // 11 + 11 + 10 bits cover a 32-bit key
+constexpr int kTopkHistWords = kTopkPasses * kTopkBins;  // one histogram per pass
+constexpr int kTopkSmall = 32 + 256;  // ints: min/max exchange + per-(stripe, wave) counts
 
-// hist: kTopkBins uint32 of LDS; small: kTopkSmall ints of LDS.  n: pages of the
-// sequence.  Needs ceil(max_pages / blockDim.x) <= PER.
-template <int PER>
-__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, uint32_t* hist,
-                                          int* small) {
+__device__ __forceinline__ uint64_t wave_ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// number of set bits of m in lanes below this one
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
+// THREADS = blockDim.x threads (at most MAXW wavefronts); page i of the
+// sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
+// loads).  n: pages of the sequence, ceil(n / THREADS) <= PER.  tok_lp: logical page written by this step's token
+// (-1: none); its last_loaded entry is read as step - 1, the value the append
+// gives it.  hist: kTopkHistWords uint32 of LDS; small: kTopkSmall ints of LDS.
+// `wait()` is called after the page-table and last_loaded loads are issued and
+// before the scores are read.
+template <int PER, int MAXW, typename Wait>
+__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, int tok_lp,
+                                          uint32_t* hist, int* small, Wait&& wait) {
+  constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
+  static_assert(PER * MAXW <= kTopkSmall - 32 && MAXW <= 16 && PER <= 32, "top-k shape");
+  const int THREADS = blockDim.x, NW = THREADS >> 6;
   const Geometry& g = ta.g;
   const int step = ta.step;
-  const float* scores = ta.scores;
-  const int32_t* pt = ta.pt;
-  int32_t* A = ta.A;
-  int32_t* selected = ta.selected;
-  int32_t* mask = ta.mask;
-  int32_t* num_selected = ta.num_selected;
-  int32_t* sel_phys = ta.sel_phys;
-  const int THREADS = blockDim.x;
-  const int NW = THREADS >> 6;
-  constexpr int NB = kTopkBins;
-  const int BPT = (NB + THREADS - 1) / THREADS;  // bins per thread in the suffix scan
-  int* scan_sh = small;                                        // [16]
-  uint32_t* red_sh = reinterpret_cast<uint32_t*>(small + 16);  // [32]
-  uint32_t* s_sel = reinterpret_cast<uint32_t*>(small + 48);   // digit, above, count
-
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = bh / g.hk;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int per = (g.max_pages + THREADS - 1) / THREADS;
-  const int base = tid * per;
-  const float* srow = scores + (int64_t)bh * g.max_pages;
-  int32_t* a_row = A + (int64_t)bh * g.max_pages;
-  const int32_t* p_row = pt + (int64_t)b * g.max_pages;
+  const float* srow = ta.scores + (int64_t)bh * g.max_pages;
+  int32_t* a_row = ta.A + (int64_t)bh * g.max_pages;
+  const int32_t* p_row = ta.pt + (int64_t)b * g.max_pages;
+  int* red = small;        // [32]
+  int* cnt = small + 32;   // [PER * NW]
 
-  uint32_t key[PER];
+  auto valid = [&](int j) { return j * THREADS + tid < n; };
   int32_t a_old[PER], phys[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    const int idx = base + j;
-    if (j < per && idx < g.max_pages) {
-      key[j] = order_key(srow[idx]);
-      a_old[j] = a_row[idx];
+    const int idx = j * THREADS + tid;
+    a_old[j] = -1;
+    phys[j] = -1;
+    if (valid(j)) {
+      a_old[j] = idx == tok_lp ? step - 1 : a_row[idx];
       phys[j] = p_row[idx];
-    } else {
-      key[j] = 0u;
-      a_old[j] = -1;
-      phys[j] = -1;
     }
   }
-  const int k = min(g.budget / g.P, n);
-  auto valid = [&](int j) { return j < per && base + j < n; };
+  for (int i = tid; i < kTopkHistWords; i += THREADS) hist[i] = 0u;
+  wait();
+  uint32_t key[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) key[j] = valid(j) ? order_key(srow[j * THREADS + tid]) : 0u;
 
   // rel = key - kmin over the valid keys; T is searched among rel values.
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
@@ -379,96 +419,141 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, uin
   kmin = wave_umin(kmin);
   kmax = wave_umax(kmax);
   if (lane == 0) {
-    red_sh[wave] = kmin;
-    red_sh[16 + wave] = kmax;
+    red[wave] = (int)kmin;
+    red[16 + wave] = (int)kmax;
   }
-  __syncthreads();
+  __syncthreads();  // also orders the histogram clearing before the first pass
   for (int w = 0; w < NW; ++w) {
-    kmin = min(kmin, red_sh[w]);
-    kmax = max(kmax, red_sh[16 + w]);
+    kmin = min(kmin, (uint32_t)red[w]);
+    kmax = max(kmax, (uint32_t)red[16 + w]);
   }
   const uint32_t range = kmax - kmin;
   const int nbits = range ? 32 - __clz((int)range) : 1;
-  uint64_t prefix = 0u;  // chosen digits of T's rel, bits [lo, nbits)
+  const int k = min(g.budget / g.P, n);
+
+  // Radix select: pass p histograms the next digit of the keys that still match
+  // T's prefix into its own histogram; after one barrier every wavefront scans
+  // the histogram by itself (descending bins, lane l owning 32 of them), so the
+  // digit reaches all threads without a second barrier.
+  uint64_t prefix = 0u;  // digits of T's rel fixed so far, bits [lo, nbits)
   int lo = nbits;
-  int need = k;
+  uint32_t need = (uint32_t)k;  // keys still to take among those matching the prefix
   if (k > 0 && k < n) {
+    int pass = 0;
 #pragma unroll 1
-    for (int hi = nbits; hi > 0; hi = lo) {
+    for (int hi = nbits; hi > 0; hi = lo, ++pass) {
       lo = max(hi - 11, 0);
+      uint32_t* h = hist + pass * kTopkBins;
       const uint32_t dmask = (1u << (hi - lo)) - 1u;
-      for (int i = tid; i < NB; i += THREADS) hist[i] = 0u;
-      __syncthreads();
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const uint64_t rel = key[j] - kmin;
-        if (valid(j) && (rel >> hi) == prefix) atomicAdd(&hist[(rel >> lo) & dmask], 1u);
+        if (valid(j) && (rel >> hi) == prefix) atomicAdd(&h[(rel >> lo) & dmask], 1u);
       }
       __syncthreads();
-      // suffix scan: thread t owns bins [NB - BPT*(t+1), NB - BPT*t), descending
-      uint32_t local = 0u;
-      for (int i = 0; i < BPT; ++i) {
-        const int bin = NB - 1 - (tid * BPT + i);
-        if (bin >= 0) local += hist[bin];
+      const int base = kTopkBins - 32 * (lane + 1);
+      uint32_t gs[8];  // totals of this lane's eight 4-bin groups (ascending bins)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * i);
+        gs[i] = u.x + u.y + u.z + u.w;
       }
-      uint32_t cum = (uint32_t)block_exclusive_scan((int)local, scan_sh);
-      for (int i = 0; i < BPT; ++i) {
-        const int bin = NB - 1 - (tid * BPT + i);
-        if (bin < 0) break;
-        const uint32_t c = hist[bin];
-        if (cum < (uint32_t)need && cum + c >= (uint32_t)need) {
-          s_sel[0] = (uint32_t)bin;
-          s_sel[1] = cum;
-          s_sel[2] = c;
-        }
-        cum += c;
+      uint32_t own = 0u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) own += gs[i];
+      const uint32_t incl = (uint32_t)wave_inclusive_scan((int)own);
+      uint32_t acc = incl - own;  // keys in higher bins
+      const bool hit = acc < need && need <= incl;
+      // the group holding T's digit (highest group first), then the bin in it
+      int fgrp = 0;
+      uint32_t facc = 0u;
+      bool found = false;
+#pragma unroll
+      for (int i = 7; i >= 0; --i) {
+        const bool f = !found && acc + gs[i] >= need;
+        fgrp = f ? i : fgrp;
+        facc = f ? acc : facc;
+        found = found || f;
+        acc += gs[i];
       }
-      __syncthreads();
-      need -= (int)s_sel[1];
-      prefix = (prefix << (hi - lo)) | s_sel[0];
-      if ((int)s_sel[2] == need) break;  // the whole bin is kept: T's prefix suffices
+      const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * fgrp);
+      const uint32_t gv[4] = {u.x, u.y, u.z, u.w};
+      int fb = 0;
+      uint32_t fc = 0u, fa = 0u;
+      found = false;
+      acc = facc;
+#pragma unroll
+      for (int i = 3; i >= 0; --i) {
+        const bool f = !found && acc + gv[i] >= need;
+        fb = f ? base + 4 * fgrp + i : fb;
+        fc = f ? gv[i] : fc;
+        fa = f ? acc : fa;
+        found = found || f;
+        acc += gv[i];
+      }
+      const int src = __builtin_ctzll(wave_ballot(hit));
+      const int bin = __builtin_amdgcn_readlane(fb, src);
+      const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)fa, src);
+      const uint32_t inbin = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
+      need -= above;
+      prefix = (prefix << (hi - lo)) | (uint32_t)bin;
+      if (inbin == need) break;  // T's whole bin is kept: its prefix suffices
     }
   }
-  // compaction in page order
-  int c_eq = 0;
-#pragma unroll
-  for (int j = 0; j < PER; ++j)
-    if (valid(j) && ((uint64_t)(key[j] - kmin) >> lo) == prefix) ++c_eq;
-  const int eq_before = block_exclusive_scan(c_eq, scan_sh);
-  uint32_t take = 0u;
-  int n_take = 0, eq_seen = 0;
+
+  // Compaction in page order.  A kept page's output slot is the number of kept
+  // pages below it: pages above T's prefix all count, pages tying with it count
+  // up to `need` (lower page indices first).  Per stripe, ballots give the
+  // counts below a lane inside its wavefront; an exclusive scan over the
+  // (stripe, wavefront) count table, in page order, gives the rest.
+  const bool all = k >= n;
+  const bool some = k > 0 && k < n;
+  uint32_t gt_bits = 0u, eq_bits = 0u;  // per stripe: above T's prefix / tying with it
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    bool t = false;
-    if (valid(j)) {
-      if (k >= n) {
-        t = true;
-      } else if (k > 0) {
-        const uint64_t km = (uint64_t)(key[j] - kmin) >> lo;
-        if (km > prefix) {
-          t = true;
-        } else if (km == prefix) {
-          t = (eq_before + eq_seen) < need;
-          ++eq_seen;
-        }
-      }
-    }
-    take |= (t ? 1u : 0u) << j;
-    n_take += t ? 1 : 0;
+    const uint64_t km = (uint64_t)(key[j] - kmin) >> lo;
+    const bool v = valid(j);
+    const bool gt = v && (all || (some && km > prefix));
+    const bool eq = v && some && km == prefix;
+    gt_bits |= (gt ? 1u : 0u) << j;
+    eq_bits |= (eq ? 1u : 0u) << j;
+    const int cg = __popcll(wave_ballot(gt)), ce = __popcll(wave_ballot(eq));
+    if (lane == 0) cnt[j * NW + wave] = cg | (ce << 16);
   }
-  int pos = block_exclusive_scan(n_take, scan_sh);
-  int32_t* sel_row = selected + (int64_t)bh * g.k_max;
-  int32_t* m_row = mask + (int64_t)bh * g.k_max;
-  int32_t* ph_row = sel_phys ? sel_phys + (int64_t)bh * g.k_max : nullptr;
+  __syncthreads();
+  int sc[NCH];  // exclusive scan of the count table, entry c * 64 + lane
+  int carry = 0;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int e = c * 64 + lane;
+    const int val = e < PER * NW ? cnt[e] : 0;
+    const int incl = wave_inclusive_scan(val) + carry;
+    sc[c] = incl - val;
+    carry = __builtin_amdgcn_readlane(incl, 63);
+  }
+  int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
+  int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
+  int32_t* ph_row = ta.sel_phys ? ta.sel_phys + (int64_t)bh * g.k_max : nullptr;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    if (take & (1u << j)) {
-      const int p = base + j;
+    const int e = j * NW + wave;
+    int below = 0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      if (e / 64 == c) below = __builtin_amdgcn_readlane(sc[c], e % 64);
+    const bool is_gt = (gt_bits >> j) & 1u;
+    const bool is_eq = (eq_bits >> j) & 1u;
+    const int gb = (below & 0xFFFF) + lanes_below(wave_ballot(is_gt));
+    const int eb = (below >> 16) + lanes_below(wave_ballot(is_eq));
+    int pos = -1;
+    if (is_gt) pos = gb + min(eb, (int)need);
+    if (is_eq && eb < (int)need) pos = gb + eb;
+    if (pos >= 0 && pos < k) {  // always true for a kept page; guards the writes
+      const int p = j * THREADS + tid;
       sel_row[pos] = p;
       m_row[pos] = a_old[j];
       a_row[p] = step;
       if (ph_row) ph_row[pos] = (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1;
-      ++pos;
     }
   }
   for (int i = k + tid; i < g.k_max; i += THREADS) {
@@ -476,7 +561,7 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, uin
     m_row[i] = -1;
     if (ph_row) ph_row[i] = -1;
   }
-  if (tid == 0) num_selected[bh] = k;
+  if (tid == 0) ta.num_selected[bh] = k;
 }
 
 
@@ -879,6 +964,8 @@ struct MergeArgs {
   float* l_cache;
   float* o_out;
   float* l_out;
+  int32_t* seq_lens;    // advanced past a pending token (Geometry::token_pending), or null
+  const int32_t* pt;
 };
 
 template <int D>

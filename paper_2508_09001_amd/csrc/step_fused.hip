@@ -33,7 +33,7 @@ MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_
 namespace {
 
 constexpr int kLanes = 8;
-constexpr int kTopkPer = 24;
+constexpr int kTopkPer = 12;
 
 struct StepArgs {
   Geometry g;
@@ -58,7 +58,7 @@ struct StepArgs {
 template <typename T, int D>
 struct FusedLds {
   static constexpr size_t SCORE = sizeof(float) * 16 * D;
-  static constexpr size_t TOPK = sizeof(uint32_t) * kTopkBins;
+  static constexpr size_t TOPK = sizeof(uint32_t) * kTopkHistWords;
   static constexpr size_t ATTEND = sizeof(T) * 2 * Tiles<T, D>::BUF_ELEMS;
   static constexpr size_t BYTES = ATTEND > TOPK ? (ATTEND > SCORE ? ATTEND : SCORE)
                                                 : (TOPK > SCORE ? TOPK : SCORE);
@@ -105,26 +105,15 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     // the step's token goes to position seq_lens[b] if its logical page is mapped
     const int pos = a.seq_lens[b];
     const int lp = pos / g.P;
-    int phys_tok = -1;
-    if (pos >= 0 && lp < g.max_pages) phys_tok = a.pt[(int64_t)b * g.max_pages + lp];
-    const bool tok_ok = phys_tok >= 0 && phys_tok < g.num_phys;
+    const int phys_tok = token_phys(g, a.pt, b, pos);
+    const bool tok_ok = phys_tok >= 0;
     const int seq_len = pos + (tok_ok ? 1 : 0);
     const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
 
     if (role == 0) {
       StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
-      if (tok_ok) {
-        const int slot = pos - lp * g.P;
-        const int64_t ph = (int64_t)phys_tok * g.hk + h;
-        tk.lp = lp;
-        tk.slot = slot;
-        tk.k = reinterpret_cast<const T*>(a.k_new) + (int64_t)bh * D;
-        tk.v = reinterpret_cast<const T*>(a.v_new) + (int64_t)bh * D;
-        tk.k_row = reinterpret_cast<T*>(a.kc) + (ph * g.P + slot) * D;
-        tk.v_col = reinterpret_cast<T*>(a.vc) + ph * D * g.P + slot;
-        tk.a_entry = a.A + (int64_t)bh * g.max_pages + lp;
-        tk.step = a.step;
-      }
+      if (tok_ok)
+        tk = make_step_token<T>(g, a.step, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc, a.A);
       const int ppb = (blockDim.x >> 6) * ScoreShape<T, D>::PPW * kFusedScoreIters;
       score_role<T, D, kFusedScoreIters>(
           g, sub * ppb,
@@ -133,8 +122,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
           a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
       block_signal(cntA + bh);
     } else if (role == 1) {
-      block_wait(cntA + bh, g.fA, err);
-      topk_role<kTopkPer>(a.tk, bh, n_pages, reinterpret_cast<uint32_t*>(lds), small);
+      topk_role<kTopkPer, 8>(a.tk, bh, n_pages, tok_ok ? lp : -1,
+                                reinterpret_cast<uint32_t*>(lds), small,
+                                [&] { block_wait(cntA + bh, g.fA, err); });
       block_signal(cntB + bh);
     } else if (role == 2) {
       const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
@@ -163,10 +153,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     __threadfence();
     for (int b = tid; b < g.batch; b += blockDim.x) {
       const int pos = a.seq_lens[b];
-      const int lp = pos / g.P;
-      int phys = -1;
-      if (pos >= 0 && lp < g.max_pages) phys = a.pt[(int64_t)b * g.max_pages + lp];
-      if (phys >= 0 && phys < g.num_phys) a.seq_lens[b] = pos + 1;
+      if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
     }
     for (int l = tid; l < kLanes; l += blockDim.x) a.ctl[kCtlTicket + kCtlStride * l] = 0;
     for (int e = tid; e < 3 * BH; e += blockDim.x) a.ctl[kCtlCounts + e] = 0;
@@ -195,7 +182,7 @@ int fused_score_pages_per_block(int dtype, int D, int waves) {
 }
 
 bool fused_supported(const Geometry& g) {
-  return g.max_pages <= kTopkPer * 64 * g.waves && g.waves >= 4 && g.G <= 16;
+  return g.max_pages <= kTopkPer * 64 * g.waves && g.waves >= 4 && g.waves <= 8 && g.G <= 16;
 }
 
 hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
