@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   const int nunits = g.batch * g.hq * a.xs;
   const int u = xcd_remap(blockIdx.x, gridDim.x) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
-  merge_unit<D>(a, u);
+  merge_unit<D, 32>(a, u);
 }
 
 }  // namespace

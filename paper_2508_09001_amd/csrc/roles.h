@@ -273,13 +273,33 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
       for (int w = 0; w < S::WORDS; ++w) raw[it][0][w] = raw[it][1][w] = 0u;
     }
   }
-  for (int e = threadIdx.x; e < g.G * D; e += blockDim.x) sq[e] = to_f32(q[e]);
+  // the group's queries: 16-byte pieces, at most two per thread (G * d <= 2048
+  // elements for 256 threads), all requested before any is converted
+  constexpr int QV = 16 / sizeof(T);
+  uint4 qraw[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int e = (threadIdx.x + r * blockDim.x) * QV;
+    if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
+  }
   const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page0 + nw * S::PPW * ITERS;
   float kv[S::VEC];
   if (has_tok) {
     uint32_t kw[S::WORDS];
     load_words<S::WORDS>(tok.k + c * S::VEC, kw);
     words_to_f32<T, S::WORDS>(kw, kv);
+  }
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int e = (threadIdx.x + r * blockDim.x) * QV;
+    if (e < g.G * D) {
+      const uint32_t w[4] = {qraw[r].x, qraw[r].y, qraw[r].z, qraw[r].w};
+      float f[QV];
+      words_to_f32<T, 4>(w, f);
+#pragma unroll
+      for (int i = 0; i < QV; i += 4)
+        *reinterpret_cast<float4*>(sq + e + i) = make_float4(f[i], f[i + 1], f[i + 2], f[i + 3]);
+    }
   }
   __syncthreads();
 
@@ -368,13 +388,15 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 
 // THREADS = blockDim.x threads (at most MAXW wavefronts); page i of the
 // sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
-// loads).  n: pages of the sequence, ceil(n / THREADS) <= PER.  tok_lp: logical page written by this step's token
+// loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by this step's token
 // (-1: none); its last_loaded entry is read as step - 1, the value the append
-// gives it.  hist: kTopkHistWords uint32 of LDS; small: kTopkSmall ints of LDS.
+// gives it.  `pages_of()` gives n, the pages of the sequence; it is called once
+// the loads are issued.  hist: kTopkHistWords uint32 of LDS; small: kTopkSmall
+// ints of LDS.
 // `wait()` is called after the page-table and last_loaded loads are issued and
 // before the scores are read.
-template <int PER, int MAXW, typename Wait>
-__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, int tok_lp,
+template <int PER, int MAXW, typename PagesOf, typename Wait>
+__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
                                           uint32_t* hist, int* small, Wait&& wait) {
   constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
   static_assert(PER * MAXW <= kTopkSmall - 32 && MAXW <= 16 && PER <= 32, "top-k shape");
@@ -390,23 +412,30 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, int n, int
   int* red = small;        // [32]
   int* cnt = small + 32;   // [PER * NW]
 
-  auto valid = [&](int j) { return j * THREADS + tid < n; };
+  // Loads are issued for every stripe slot before the number of pages is known
+  // (an in-bounds index stands in for slots past the row; their values are
+  // not used), so none waits for another.
+  const int last = g.max_pages - 1;
   int32_t a_old[PER], phys[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    const int idx = j * THREADS + tid;
-    a_old[j] = -1;
-    phys[j] = -1;
-    if (valid(j)) {
-      a_old[j] = idx == tok_lp ? step - 1 : a_row[idx];
-      phys[j] = p_row[idx];
-    }
+    const int idx = min(j * THREADS + tid, last);
+    a_old[j] = a_row[idx];
+    phys[j] = p_row[idx];
   }
   for (int i = tid; i < kTopkHistWords; i += THREADS) hist[i] = 0u;
   wait();
+  float sv[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) sv[j] = srow[min(j * THREADS + tid, last)];
+  const int n = pages_of();
+  auto valid = [&](int j) { return j * THREADS + tid < n; };
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (j * THREADS + tid == tok_lp) a_old[j] = step - 1;
   uint32_t key[PER];
 #pragma unroll
-  for (int j = 0; j < PER; ++j) key[j] = valid(j) ? order_key(srow[j * THREADS + tid]) : 0u;
+  for (int j = 0; j < PER; ++j) key[j] = valid(j) ? order_key(sv[j]) : 0u;
 
   // rel = key - kmin over the valid keys; T is searched among rel values.
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
@@ -605,11 +634,11 @@ struct AttendArgs {
 // state and the query operands are set up first; `wait()` is then called (the
 // fused step waits there for the page selection), and only then is the page
 // list read.  Uses `lds` (2 * Tiles<T, D>::BUF_ELEMS elements, 16-byte aligned)
-// and three int arrays of kMaxSplitPages entries.  The caller passes the
-// sequence length in effect.
-template <typename T, int D, int RTW, typename Wait>
+// and three int arrays of kMaxSplitPages entries.  `seq_len_of()` gives the
+// sequence length in effect; it is called once the page-list loads are issued.
+template <typename T, int D, int RTW, typename SeqLen, typename Wait>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
-                                            int seq_len, T* lds, int* s_phys, int* s_page,
+                                            SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
                                             int* s_mask, Wait&& wait) {
   using TL = Tiles<T, D>;
   const Geometry& g = a.g;
@@ -667,23 +696,31 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     }
   }
   wait();
-  const int k_eff = a.nsel[bh];
+  // The split's rows of the selection are requested together with the number
+  // of selected pages (slots past it hold -1 and are dropped below); thread i
+  // handles slot i (kMaxSplitPages <= workgroup size).
   const int first = split * g.pages_per_split;
+  int lp = -1, m = 0, phys = -1;
+  if (tid < g.pages_per_split && first + tid < g.k_max) {
+    const int64_t o = (int64_t)bh * g.k_max + first + tid;
+    lp = a.sel[o];
+    m = a.msk[o];
+    if (a.sel_phys) phys = a.sel_phys[o];
+  }
+  const int k_eff = a.nsel[bh];
+  const int seq_len = seq_len_of();
   const int np = min(g.pages_per_split, k_eff - first);
   if (np <= 0) return;  // uniform: nothing selected in this split
   const int nchunks = (np + g.chunk_pages - 1) / g.chunk_pages;
-  for (int i = tid; i < np; i += nthreads) {
-    const int lp = a.sel[(int64_t)bh * g.k_max + first + i];
-    int phys = -1;
-    if (a.sel_phys) {
-      phys = a.sel_phys[(int64_t)bh * g.k_max + first + i];
-    } else if (lp >= 0 && lp < g.max_pages) {
+  // page list of the split: physical page (-1: skip), stored tokens (0 for a
+  // skipped page and past the list), mask value
+  if (tid < kMaxSplitPages) {
+    if (!a.sel_phys && tid < np && lp >= 0 && lp < g.max_pages)
       phys = a.pt[(int64_t)b * g.max_pages + lp];
-    }
-    if (lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
-    s_phys[i] = phys;
-    s_page[i] = lp;
-    s_mask[i] = a.msk[(int64_t)bh * g.k_max + first + i];
+    if (tid >= np || lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
+    s_phys[tid] = phys;
+    s_len[tid] = phys >= 0 ? max(0, min(g.P, seq_len - lp * g.P)) : 0;
+    s_mask[tid] = tid < np ? m : 0;
   }
 
   __syncthreads();  // page list ready
@@ -697,67 +734,62 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   const T* kc = reinterpret_cast<const T*>(a.kc);
   const T* vc = reinterpret_cast<const T*>(a.vc);
 
-  auto tile_page = [&](int c, int tile, int* slot_off) -> int {
-    // split-local page index of a 16-token tile of chunk c, and its slot offset
-    if (g.chunk_pages == 2) {
-      *slot_off = 0;
-      return 2 * c + tile;
+  // The part of each piece's address that does not depend on the chunk: its
+  // 16-token tile (page of the chunk), its slot in the page, its element offset
+  // in the page's (h_k) block and whether it is a V^T piece.  Page blocks of K
+  // and V^T have the same size, P * d elements.
+  int pc_tile[kMaxPieces], pc_slot[kMaxPieces], pc_off[kMaxPieces];
+  bool pc_v[kMaxPieces];
+#pragma unroll
+  for (int i = 0; i < kMaxPieces; ++i) {
+    const int e = min(tid + i * nthreads, TL::PIECES - 1);
+    int tile, slot, off;
+    const bool isv = e >= TL::K_PIECES;
+    if (!isv) {
+      const int tok = e / TL::KPR, q = e - tok * TL::KPR;
+      tile = tok >> 4;
+      slot = tok & 15;
+      off = q * TL::VEC;  // + slot * D below
+    } else {
+      const int ev = e - TL::K_PIECES;
+      tile = ev / (D * TL::VPR);
+      const int rem = ev - tile * (D * TL::VPR);
+      const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
+      slot = q * TL::TPP;
+      off = dr * g.P;  // + slot below
     }
-    *slot_off = 16 * tile;
-    return c;
-  };
+    if (g.chunk_pages == 1) slot += 16 * tile;  // both tiles lie in one page
+    pc_tile[i] = tile;
+    pc_slot[i] = slot;
+    pc_off[i] = isv ? off + slot : off + slot * D;
+    pc_v[i] = isv;
+  }
 
-  auto load_chunk = [&](int c, uint4* stage) {
+  // Every piece is loaded without a branch around the load (a piece that holds
+  // no stored data reads a stand-in address, the cache's first 16 bytes), so
+  // the loads of a chunk are all in flight together; `keep` records how many
+  // leading elements of each piece hold stored data (4 bits per piece), and
+  // the rest is zeroed when the piece is written to LDS.
+  const int64_t blk_elems = (int64_t)g.P * D;
+  auto load_chunk = [&](int c, uint4* stage, uint32_t& keep) {
+    uint32_t kp = 0u;
 #pragma unroll
     for (int i = 0; i < kMaxPieces; ++i) {
-      const int e = tid + i * nthreads;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (i < pieces_per_thread && e < TL::PIECES) {
-        if (e < TL::K_PIECES) {
-          const int tok = e / TL::KPR, q = e - tok * TL::KPR;
-          const int tile = tok >> 4;
-          int so;
-          const int pl = tile_page(c, tile, &so);
-          const int slot = so + (tok & 15);
-          if (pl < np && s_phys[pl] >= 0 && s_page[pl] * g.P + slot < seq_len) {
-            const T* src = kc + (((int64_t)s_phys[pl] * g.hk + h) * g.P + slot) * D + q * TL::VEC;
-            v = *reinterpret_cast<const uint4*>(src);
-          }
-        } else {
-          const int ev = e - TL::K_PIECES;
-          const int tile = ev / (D * TL::VPR);
-          const int rem = ev - tile * (D * TL::VPR);
-          const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
-          int so;
-          const int pl = tile_page(c, tile, &so);
-          if (pl < np && s_phys[pl] >= 0) {
-            const int slot0 = so + q * TL::TPP;
-            const int valid = seq_len - (s_page[pl] * g.P + slot0);  // stored tokens in piece
-            if (valid > 0) {
-              const T* src = vc + (((int64_t)s_phys[pl] * g.hk + h) * D + dr) * g.P + slot0;
-              v = *reinterpret_cast<const uint4*>(src);
-              if (valid < TL::TPP) {  // zero the unstored tail of the piece
-                uint32_t w[4] = {v.x, v.y, v.z, v.w};
-                if constexpr (sizeof(T) == 2) {
-#pragma unroll
-                  for (int t = 0; t < 8; ++t)
-                    if (t >= valid) w[t >> 1] &= (t & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-                } else {
-#pragma unroll
-                  for (int t = 0; t < 4; ++t)
-                    if (t >= valid) w[t] = 0u;
-                }
-                v = make_uint4(w[0], w[1], w[2], w[3]);
-              }
-            }
-          }
-        }
-      }
-      stage[i] = v;
+      const int pl = g.chunk_pages == 2 ? 2 * c + pc_tile[i] : c;
+      const int phys = s_phys[pl];
+      const int len = s_len[pl];
+      int n_el = pc_v[i] ? min(max(len - pc_slot[i], 0), TL::TPP) : (pc_slot[i] < len ? TL::VEC : 0);
+      if (i >= pieces_per_thread || tid + i * nthreads >= TL::PIECES) n_el = 0;
+      const T* src = kc;
+      if (n_el > 0)
+        src = (pc_v[i] ? vc : kc) + ((int64_t)phys * g.hk + h) * blk_elems + pc_off[i];
+      stage[i] = *reinterpret_cast<const uint4*>(src);
+      kp |= (uint32_t)n_el << (4 * i);
     }
+    keep = kp;
   };
 
-  auto store_chunk = [&](int buf, const uint4* stage) {
+  auto store_chunk = [&](int buf, const uint4* stage, uint32_t keep) {
     T* base = lds + buf * TL::BUF_ELEMS;
 #pragma unroll
     for (int i = 0; i < kMaxPieces; ++i) {
@@ -774,7 +806,18 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
           const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
           dst = base + TL::K_ELEMS + (tile * D + dr) * TL::VROW + q * TL::TPP;
         }
-        *reinterpret_cast<uint4*>(dst) = stage[i];
+        const int n_el = (keep >> (4 * i)) & 15;
+        uint32_t w[4] = {stage[i].x, stage[i].y, stage[i].z, stage[i].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if constexpr (sizeof(T) == 2) {
+            const uint32_t m = (2 * t < n_el ? 0x0000FFFFu : 0u) | (2 * t + 1 < n_el ? 0xFFFF0000u : 0u);
+            w[t] &= m;
+          } else {
+            w[t] = t < n_el ? w[t] : 0u;
+          }
+        }
+        *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
       }
     }
   };
@@ -783,16 +826,15 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     const T* Ks = lds + buf * TL::BUF_ELEMS;
     const T* Vs = Ks + TL::K_ELEMS;
 
-    // page facts for the two tiles of this chunk
-    bool tvalid[2];
-    int tmask[2], tbase[2];
+    // page facts for the two tiles of this chunk: stored tokens from the
+    // tile's first slot, mask value
+    int tlen[2], tmask[2];
 #pragma unroll
     for (int tile = 0; tile < 2; ++tile) {
-      int so;
-      const int pl = tile_page(c, tile, &so);
-      tvalid[tile] = pl < np && s_phys[pl] >= 0;
-      tmask[tile] = tvalid[tile] ? s_mask[pl] : 0;
-      tbase[tile] = tvalid[tile] ? s_page[pl] * g.P + so : 0;  // position of tile slot 0
+      const int pl = g.chunk_pages == 2 ? 2 * c + tile : c;
+      const int so = g.chunk_pages == 2 ? 0 : 16 * tile;
+      tlen[tile] = s_len[pl] - so;
+      tmask[tile] = s_mask[pl];
     }
 
 #pragma unroll
@@ -829,11 +871,11 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
       float mloc = -INFINITY;
 #pragma unroll
       for (int tile = 0; tile < 2; ++tile) {
-        const bool use = row_live[j] && tvalid[tile] &&
+        const bool use = row_live[j] && tlen[tile] > 0 &&
                          (row_r[j] == W || tmask[tile] < row_tau[j]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool ok = use && (tbase[tile] + 4 * g4 + i) < seq_len;
+          const bool ok = use && (4 * g4 + i) < tlen[tile];
           x[tile][i] = ok ? s[tile][i] * a.scale_log2 : -INFINITY;
           mloc = fmaxf(mloc, x[tile][i]);
         }
@@ -896,28 +938,29 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   // computing chunk c - 2, and every wavefront has since passed the barrier of
   // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
   // compile-time constants (two chunks per trip when DEPTH == 2).
+  uint32_t keep[DEPTH];
   if constexpr (DEPTH == 2) {
-    load_chunk(0, stage[0]);
-    if (nchunks > 1) load_chunk(1, stage[DEPTH - 1]);
+    load_chunk(0, stage[0], keep[0]);
+    if (nchunks > 1) load_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
 #pragma unroll 1
     for (int c = 0; c < nchunks; c += 2) {
-      store_chunk(0, stage[0]);
-      if (c + 2 < nchunks) load_chunk(c + 2, stage[0]);
+      store_chunk(0, stage[0], keep[0]);
+      if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
       __syncthreads();
       compute_chunk(c, 0);
       if (c + 1 < nchunks) {
-        store_chunk(1, stage[DEPTH - 1]);
-        if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1]);
+        store_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
+        if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1], keep[DEPTH - 1]);
         __syncthreads();
         compute_chunk(c + 1, 1);
       }
     }
   } else {
-    load_chunk(0, stage[0]);
+    load_chunk(0, stage[0], keep[0]);
 #pragma unroll 1
     for (int c = 0; c < nchunks; ++c) {
-      store_chunk(c & 1, stage[0]);
-      if (c + 1 < nchunks) load_chunk(c + 1, stage[0]);
+      store_chunk(c & 1, stage[0], keep[0]);
+      if (c + 1 < nchunks) load_chunk(c + 1, stage[0], keep[0]);
       __syncthreads();
       compute_chunk(c, c & 1);
     }
@@ -975,59 +1018,74 @@ struct Row {
   float z;
 };
 
-// Combine the splits of row rho of (b, h): sum_s e^{Z_s} O_s / sum_s e^{Z_s}.
-template <int D>
-__device__ Row<D> combine_splits(const MergeArgs& a, int bh, int rho) {
+// Combine the splits of NR rows rho[] of (b, h): sum_s e^{Z_s} O_s / sum_s e^{Z_s},
+// Z = ln sum_s e^{Z_s}.  Splits are taken GS at a time with every load of the
+// group (log-normalisers one per lane, output rows E floats per lane) in
+// flight together; groups after the first are folded in relative to the
+// running maximum.
+template <int D, int NR, int GS>
+__device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const int (&rho)[NR],
+                                               Row<D> (&res)[NR]) {
+  constexpr int E = Row<D>::E;
   const Geometry& g = a.g;
   const int lane = threadIdx.x & 63;
-  const int e0 = lane * Row<D>::E;
+  const int e0 = lane * E;
   const int nvs = min((a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split, g.n_splits);
-  const int64_t base = (int64_t)bh * g.n_splits * g.R + rho;
-  Row<D> res;
+  float m[NR], wl[NR], acc[NR][E];
 #pragma unroll
-  for (int e = 0; e < Row<D>::E; ++e) res.o[e] = 0.f;
-  float zmax = -INFINITY;
-  for (int s0 = 0; s0 < nvs; s0 += 64) {
-    const float z = (s0 + lane < nvs) ? a.l_ws[base + (int64_t)(s0 + lane) * g.R] : -INFINITY;
-    zmax = fmaxf(zmax, z);
+  for (int r = 0; r < NR; ++r) {
+    m[r] = -INFINITY;
+    wl[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[r][e] = 0.f;
   }
-  zmax = wave_max(zmax);
-  if (zmax == -INFINITY) {
-    res.z = -INFINITY;
-    return res;
-  }
-  float wsum = 0.f;
-  for (int s0 = 0; s0 < nvs; s0 += 64) {
-    const int s = s0 + lane;
-    const float w = (s < nvs) ? __expf(a.l_ws[base + (int64_t)s * g.R] - zmax) : 0.f;
-    wsum += w;
-    const int cnt = min(64, nvs - s0);
-    // 8 split rows in flight at a time
-    for (int j0 = 0; j0 < cnt; j0 += 8) {
-      float v[8][Row<D>::E];
+  for (int s0 = 0; s0 < nvs; s0 += GS) {
+    const int cnt = min(GS, nvs - s0);
+    float z[NR], v[NR][GS][E];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int ss = s0 + min(j0 + j, cnt - 1);
+    for (int r = 0; r < NR; ++r) {
+      const int64_t base = (int64_t)bh * g.n_splits * g.R + rho[r];
+      z[r] = lane < cnt ? a.l_ws[base + (int64_t)(s0 + lane) * g.R] : -INFINITY;
 #pragma unroll
-        for (int e = 0; e < Row<D>::E; ++e)
-          v[j][e] = a.o_ws[(base + (int64_t)ss * g.R) * D + e0 + e];
-      }
+      for (int j = 0; j < GS; ++j) {
+        const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j0 + j));
-        if (j0 + j < cnt) {
-#pragma unroll
-          for (int e = 0; e < Row<D>::E; ++e) res.o[e] += wj * v[j][e];
-        }
+        for (int e = 0; e < E; ++e) v[r][j][e] = a.o_ws[row * D + e0 + e];
       }
     }
-  }
-  wsum = wave_sum(wsum);
-  const float inv = 1.f / wsum;
 #pragma unroll
-  for (int e = 0; e < Row<D>::E; ++e) res.o[e] *= inv;
-  res.z = zmax + __logf(wsum);
-  return res;
+    for (int r = 0; r < NR; ++r) {
+      const float m_new = fmaxf(m[r], wave_max(z[r]));
+      if (m_new == -INFINITY) continue;  // uniform: no split holds a selected entry yet
+      const float scale = __expf(m[r] - m_new);  // 0 while m is -inf
+      wl[r] *= scale;
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[r][e] *= scale;
+      const float w = lane < cnt ? __expf(z[r] - m_new) : 0.f;
+      wl[r] += w;
+#pragma unroll
+      for (int j = 0; j < GS; ++j) {
+        const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j));
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[r][e] += wj * v[r][j][e];  // wj = 0 past cnt
+      }
+      m[r] = m_new;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    if (m[r] == -INFINITY) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) res[r].o[e] = 0.f;
+      res[r].z = -INFINITY;
+      continue;
+    }
+    const float wsum = wave_sum(wl[r]);
+    const float inv = 1.f / wsum;
+#pragma unroll
+    for (int e = 0; e < E; ++e) res[r].o[e] = acc[r][e] * inv;
+    res[r].z = m[r] + __logf(wsum);
+  }
 }
 
 template <int D>
@@ -1066,16 +1124,29 @@ __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
   return v;
 }
 
-template <int D>
-__device__ Row<D> partial(const MergeArgs& a, int b, int h, int gq, int r) {
+// The partial (O, Z) of window rows r[] of query head gq of (b, h): from the
+// split partials, or (mode 1) from the caller's o_part / lse_part.
+template <int D, int NR, int GS>
+__device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int gq, const int (&r)[NR],
+                                         Row<D> (&res)[NR]) {
   const Geometry& g = a.g;
-  if (a.mode == 1) return get<D>(a.o_part, a.l_part, ((int64_t)b * (g.W + 1) + r) * g.hq + h * g.G + gq);
-  return combine_splits<D>(a, b * g.hk + h, r * g.G + gq);
+  if (a.mode == 1) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i)
+      res[i] = get<D>(a.o_part, a.l_part, ((int64_t)b * (g.W + 1) + r[i]) * g.hq + h * g.G + gq);
+    return;
+  }
+  int rho[NR];
+#pragma unroll
+  for (int i = 0; i < NR; ++i) rho[i] = r[i] * g.G + gq;
+  combine_splits<D, NR, GS>(a, b * g.hk + h, rho, res);
 }
 
 // One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
-// executed by one wavefront; no barriers inside.
-template <int D>
+// executed by one wavefront; no barriers inside.  The unit of row 0 also
+// handles the current row W, whose cache slot is the one row 0 leaves.  GS:
+// splits whose loads are in flight together (at most 64).
+template <int D, int GS>
 __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   const Geometry& g = a.g;
   const int W = g.W;
@@ -1088,36 +1159,49 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   const int qh = h * g.G + gq;
   const int64_t out_row = (int64_t)b * (W + 1);
 
-  if (a.mode == 0) {  // plain combine of the splits for row x
-    put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, partial<D>(a, b, h, gq, x));
+  if (a.mode == 0 || x == W) {  // plain combine of row x (W == 0: the current row only)
+    Row<D> p[1];
+    partials<D, 1, GS>(a, b, h, gq, {x}, p);
+    if (a.mode == 0)
+      put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, p[0]);
+    else
+      put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, p[0]);
     return;
   }
 
+  const int tau0 = a.step - W + x;
   Row<D> zero;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) zero.o[e] = 0.f;
   zero.z = -INFINITY;
-
-  const int r0 = x;
-  const int tau0 = a.step - W + r0;
-  if (r0 == W) {  // W == 0: the current row only
-    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, partial<D>(a, b, h, gq, r0));
+  if (x > 0) {
+    if (tau0 < 0) {  // the row's query does not exist yet
+      put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, zero);
+      return;
+    }
+    const int64_t ci = ((int64_t)b * W + tau0 % W) * g.hq + qh;
+    const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
+    Row<D> p[1];
+    partials<D, 1, GS>(a, b, h, gq, {x}, p);
+    const Row<D> merged = lse_merge<D>(cached, p[0]);
+    put<D>(a.o_cache, a.l_cache, ci, merged);
+    put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, merged);
     return;
   }
-  if (tau0 < 0) {
-    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, zero);
-  } else {
-    const int64_t ci = ((int64_t)b * W + (tau0 % W)) * g.hq + qh;
-    const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
-    const Row<D> merged = lse_merge<D>(cached, partial<D>(a, b, h, gq, r0));
-    put<D>(a.o_out, a.l_out, (out_row + r0) * g.hq + qh, merged);
-    if (r0 > 0) put<D>(a.o_cache, a.l_cache, ci, merged);
-  }
-  if (r0 == 0) {  // the current row: output, and push into slot t mod W
-    const Row<D> cur = partial<D>(a, b, h, gq, W);
-    put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, cur);
-    put<D>(a.o_cache, a.l_cache, ((int64_t)b * W + (a.step % W)) * g.hq + qh, cur);
-  }
+  // Row 0 leaves the window (final); the current row then takes its slot,
+  // (t - W) mod W == t mod W.
+  const int64_t slot = ((int64_t)b * W + a.step % W) * g.hq + qh;
+  Row<D> cached = zero;
+  if (tau0 >= 0) cached = get<D>(a.o_cache, a.l_cache, slot);
+  Row<D> p[2];
+  partials<D, 2, GS>(a, b, h, gq, {0, W}, p);
+  const Row<D> merged = tau0 >= 0 ? lse_merge<D>(cached, p[0]) : zero;
+  put<D>(a.o_out, a.l_out, out_row * g.hq + qh, merged);
+  put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, p[1]);
+  // the slot's old contents are in registers (merged depends on them) before
+  // it is overwritten
+  asm volatile("" : : "v"(merged.z) : "memory");
+  put<D>(a.o_cache, a.l_cache, slot, p[1]);
 }
 
 // ============================================================================

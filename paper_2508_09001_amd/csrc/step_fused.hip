@@ -122,20 +122,20 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
           a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
       block_signal(cntA + bh);
     } else if (role == 1) {
-      topk_role<kTopkPer, 8>(a.tk, bh, n_pages, tok_ok ? lp : -1,
+      topk_role<kTopkPer, 8>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
                                 reinterpret_cast<uint32_t*>(lds), small,
                                 [&] { block_wait(cntA + bh, g.fA, err); });
       block_signal(cntB + bh);
     } else if (role == 2) {
       const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
-      attend_role<T, D, RTW>(a.at, b, h, rg, split, seq_len, reinterpret_cast<T*>(lds), s_phys,
+      attend_role<T, D, RTW>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
                              s_page, s_mask, [&] { block_wait(cntB + bh, 1, err); });
       block_signal(cntC + bh);
     } else {
       block_wait(cntC + bh, g.fC, err);
       const int per_bh = g.G * a.mg.xs;
       const int local = sub * (blockDim.x >> 6) + (tid >> 6);
-      if (local < per_bh) merge_unit<D>(a.mg, bh * per_bh + local);
+      if (local < per_bh) merge_unit<D, 16>(a.mg, bh * per_bh + local);
     }
   }
 

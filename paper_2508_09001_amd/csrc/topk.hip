@@ -32,8 +32,10 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
   __shared__ int small[kTopkSmall];
   const int bh = blockIdx.x;
   const int b = bh / ta.g.hk;
-  const int n = min((live_seq_len(ta.g, seq_lens, ta.pt, b) + ta.g.P - 1) / ta.g.P, ta.g.max_pages);
-  topk_role<PER, THREADS / 64>(ta, bh, n, -1, hist, small, [] {});
+  topk_role<PER, THREADS / 64>(
+      ta, bh,
+      [&] { return min((live_seq_len(ta.g, seq_lens, ta.pt, b) + ta.g.P - 1) / ta.g.P, ta.g.max_pages); },
+      -1, hist, small, [] {});
 }
 
 }  // namespace
