@@ -222,7 +222,9 @@ def main():
                    "q_heads": spec.num_q_heads, "head_dim": spec.head_dim,
                    "context": int(spec.prefill[0]), "page_size": spec.page_size,
                    "budget_tokens": spec.budget, "window": spec.window, "layers_rotated": L,
-                   "launch": "hip-graph per step"},
+                   "launch": "hip-graph per step",
+                   "step_path": ("single launch" if os.environ.get("RETRO_STEP_FUSED") == "1"
+                                 else "four launches")},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),

@@ -70,10 +70,12 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.waves = std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D));
   if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
 
-  x.fA = (x.max_pages + fused_score_pages_per_block(x.dtype, x.D, x.waves) - 1) /
-         fused_score_pages_per_block(x.dtype, x.D, x.waves);
-  x.fC = x.n_rgroups * x.n_splits;
-  x.fD = (x.G * (x.W > 0 ? x.W : 1) + x.waves - 1) / x.waves;
+  x.f_rgroups = (x.row_tiles + kFusedWaves - 1) / kFusedWaves;
+  x.f_tpg = (x.row_tiles + x.f_rgroups - 1) / x.f_rgroups;
+  const int f_ppb = fused_score_pages_per_block(x.dtype, x.D);
+  x.fA = (x.max_pages + f_ppb - 1) / f_ppb;
+  x.fC = x.f_rgroups * x.n_splits;
+  x.fD = (x.G * (x.W > 0 ? x.W : 1) + kFusedWaves - 1) / kFusedWaves;
   x.f_grid = (int64_t)8 * ((bh + 7) / 8) * (x.fA + 1 + x.fC + x.fD);
   x.fused = fused_supported(x) && x.f_grid < (1LL << 31);
 

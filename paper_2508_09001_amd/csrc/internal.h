@@ -50,7 +50,10 @@ struct Geometry {
   int tiles_per_group;
   int rtw;            // row tiles per wave
   int waves;          // waves per attention workgroup
-  // fused step plan: tasks per KV head of each role, grid size, availability
+  // fused step plan (workgroups of kFusedWaves wavefronts, one attention row
+  // tile per wavefront): row groups and tiles per group of its attention
+  // tasks, tasks per KV head of each role, grid size, availability
+  int f_rgroups, f_tpg;
   int fA, fC, fD;
   int64_t f_grid;
   bool fused;
@@ -72,10 +75,11 @@ constexpr int kCtlExit = 256;
 constexpr int kCtlError = 257;
 constexpr int kCtlCounts = 512;
 constexpr int kFusedScoreIters = 4;
+constexpr int kFusedWaves = 8;
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
 int attend_min_waves(int dtype, int D);
-int fused_score_pages_per_block(int dtype, int D, int waves);
+int fused_score_pages_per_block(int dtype, int D);
 bool fused_supported(const Geometry& g);
 
 // ---- launchers (return hipSuccess or the launch error) ----

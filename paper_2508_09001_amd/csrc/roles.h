@@ -10,9 +10,19 @@ namespace retro {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kMaxPieces = 4;       // 16-byte staging registers per thread per chunk
+constexpr int kMaxPieces = 4;       // 16-byte staging registers per thread per chunk (attention kernel)
 constexpr int kMaxSplitPages = 64;  // selected pages per attention split
 
+
+// The thread's index in the workgroup, as a value the compiler cannot move:
+// roles run inside the fused kernel's task loop, and values computed from the
+// index alone would otherwise be hoisted out of it and kept live (in registers
+// every role then lacks) across all roles.
+__device__ __forceinline__ int thread_index() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
 
 // Order-preserving map of a float to 32 bits: larger float -> larger key; -0 == +0.
 __device__ __forceinline__ uint32_t order_key(float s) {
@@ -256,7 +266,8 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
                                            const StepToken<T> tok) {
 #pragma clang fp contract(off)
   using S = ScoreShape<T, D>;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int tid = thread_index();
+  const int lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int c = lane % S::LPP;
   // every load before any wait: digest rows (in bounds of the [max_pages] row
   // whatever the sequence length), the queries, the token's key
@@ -279,7 +290,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
   uint4 qraw[2];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    const int e = (threadIdx.x + r * blockDim.x) * QV;
+    const int e = (tid + r * blockDim.x) * QV;
     if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
   const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page0 + nw * S::PPW * ITERS;
@@ -291,7 +302,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
   }
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    const int e = (threadIdx.x + r * blockDim.x) * QV;
+    const int e = (tid + r * blockDim.x) * QV;
     if (e < g.G * D) {
       const uint32_t w[4] = {qraw[r].x, qraw[r].y, qraw[r].z, qraw[r].w};
       float f[QV];
@@ -351,11 +362,11 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
     if (page < n_pages && c == 0) srow[page] = Ssum + 0.0f;
   }
   if (has_tok) {
-    for (int i = threadIdx.x; i < D; i += blockDim.x) {
+    for (int i = tid; i < D; i += blockDim.x) {
       tok.k_row[i] = tok.k[i];
       tok.v_col[(int64_t)i * g.P] = tok.v[i];
     }
-    if (threadIdx.x == 0) *tok.a_entry = tok.step - 1;
+    if (tid == 0) *tok.a_entry = tok.step - 1;
   }
 }
 
@@ -403,7 +414,7 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
   const int THREADS = blockDim.x, NW = THREADS >> 6;
   const Geometry& g = ta.g;
   const int step = ta.step;
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = thread_index(), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = bh / g.hk;
   const float* srow = ta.scores + (int64_t)bh * g.max_pages;
@@ -634,9 +645,10 @@ struct AttendArgs {
 // state and the query operands are set up first; `wait()` is then called (the
 // fused step waits there for the page selection), and only then is the page
 // list read.  Uses `lds` (2 * Tiles<T, D>::BUF_ELEMS elements, 16-byte aligned)
-// and three int arrays of kMaxSplitPages entries.  `seq_len_of()` gives the
+// and three int arrays of kMaxSplitPages entries; MAXP bounds the 16-byte pieces
+// of a chunk per thread (ceil(Tiles::PIECES / threads)).  `seq_len_of()` gives the
 // sequence length in effect; it is called once the page-list loads are issued.
-template <typename T, int D, int RTW, typename SeqLen, typename Wait>
+template <typename T, int D, int RTW, int MAXP, typename SeqLen, typename Wait>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
                                             SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
                                             int* s_mask, Wait&& wait) {
@@ -644,7 +656,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   const Geometry& g = a.g;
   const int bh = b * g.hk + h;
   const int nthreads = blockDim.x;
-  const int tid = threadIdx.x;
+  const int tid = thread_index();
   const int lane = tid & 63, wave = tid >> 6, nwaves = nthreads >> 6;
   const int ln16 = lane & 15, g4 = lane >> 4;
 
@@ -730,7 +742,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   // Chunks whose loads are in flight ahead of the computation: two when a
   // wavefront owns one row tile, one when it owns two (register budget).
   constexpr int DEPTH = RTW == 1 ? 2 : 1;
-  uint4 stage[DEPTH][kMaxPieces];
+  uint4 stage[DEPTH][MAXP];
   const T* kc = reinterpret_cast<const T*>(a.kc);
   const T* vc = reinterpret_cast<const T*>(a.vc);
 
@@ -738,10 +750,10 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   // 16-token tile (page of the chunk), its slot in the page, its element offset
   // in the page's (h_k) block and whether it is a V^T piece.  Page blocks of K
   // and V^T have the same size, P * d elements.
-  int pc_tile[kMaxPieces], pc_slot[kMaxPieces], pc_off[kMaxPieces];
-  bool pc_v[kMaxPieces];
+  int pc_tile[MAXP], pc_slot[MAXP], pc_off[MAXP];
+  bool pc_v[MAXP];
 #pragma unroll
-  for (int i = 0; i < kMaxPieces; ++i) {
+  for (int i = 0; i < MAXP; ++i) {
     const int e = min(tid + i * nthreads, TL::PIECES - 1);
     int tile, slot, off;
     const bool isv = e >= TL::K_PIECES;
@@ -774,7 +786,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   auto load_chunk = [&](int c, uint4* stage, uint32_t& keep) {
     uint32_t kp = 0u;
 #pragma unroll
-    for (int i = 0; i < kMaxPieces; ++i) {
+    for (int i = 0; i < MAXP; ++i) {
       const int pl = g.chunk_pages == 2 ? 2 * c + pc_tile[i] : c;
       const int phys = s_phys[pl];
       const int len = s_len[pl];
@@ -792,7 +804,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   auto store_chunk = [&](int buf, const uint4* stage, uint32_t keep) {
     T* base = lds + buf * TL::BUF_ELEMS;
 #pragma unroll
-    for (int i = 0; i < kMaxPieces; ++i) {
+    for (int i = 0; i < MAXP; ++i) {
       const int e = tid + i * nthreads;
       if (i < pieces_per_thread && e < TL::PIECES) {
         T* dst;
@@ -1028,7 +1040,7 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
                                                Row<D> (&res)[NR]) {
   constexpr int E = Row<D>::E;
   const Geometry& g = a.g;
-  const int lane = threadIdx.x & 63;
+  const int lane = thread_index() & 63;
   const int e0 = lane * E;
   const int nvs = min((a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split, g.n_splits);
   float m[NR], wl[NR], acc[NR][E];
@@ -1108,16 +1120,16 @@ __device__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
 
 template <int D>
 __device__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
-  const int e0 = (threadIdx.x & 63) * Row<D>::E;
+  const int e0 = (thread_index() & 63) * Row<D>::E;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) o[idx * D + e0 + e] = v.o[e];
-  if ((threadIdx.x & 63) == 0) z[idx] = v.z;
+  if ((thread_index() & 63) == 0) z[idx] = v.z;
 }
 
 template <int D>
 __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
   Row<D> v;
-  const int e0 = (threadIdx.x & 63) * Row<D>::E;
+  const int e0 = (thread_index() & 63) * Row<D>::E;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) v.o[e] = o[idx * D + e0 + e];
   v.z = z[idx];
@@ -1210,7 +1222,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
 // barrier does not wait for them), the workgroup meets at a barrier, and one
 // thread adds 1 to the counter with release semantics (which writes the L2 back
 // once).  Consumer: thread 0 polls the counter with relaxed device-coherent
-// loads (an acquire on every poll would invalidate the L2 each time), then
+// loads (an acquire on every poll would invalidate the caches each time), then
 // issues one acquire fence and releases the workgroup through a barrier.
 // Polling is bounded: past the limit the error word is set and the consumer
 // goes on, so no wait can hang.

@@ -14,6 +14,11 @@
 // L2.  Hand-offs use per-head counters (roles.h: block_signal / block_wait,
 // bounded waits).
 //
+// Workgroups have kFusedWaves (8) wavefronts and at most 128 VGPRs per lane, so
+// two fit on a CU: at the workloads' sizes every task of an XCD is resident
+// from the start, and consumers issue the loads that do not depend on their
+// producer (queries, page table, last_loaded) before they wait.
+//
 // The step's own token is appended by the score block whose pages include it,
 // before that block scores them.  Sequence lengths are advanced by the last
 // workgroup to finish, which also zeroes every synchronisation word, so the
@@ -32,7 +37,7 @@ MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_
 
 namespace {
 
-constexpr int kLanes = 8;
+constexpr int kMaxLanes = 8;  // lanes: workgroups with blockIdx mod 8 == lane share an XCD
 constexpr int kTopkPer = 12;
 
 struct StepArgs {
@@ -64,8 +69,13 @@ struct FusedLds {
                                                 : (TOPK > SCORE ? TOPK : SCORE);
 };
 
-template <typename T, int D, int RTW>
-__global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
+constexpr int kThreads = 64 * kFusedWaves;
+
+template <typename T, int D>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
+step_kernel(StepArgs a) {
+  // chunk pieces per thread of the attention role
+  constexpr int MAXP = (Tiles<T, D>::PIECES + kThreads - 1) / kThreads;
   __shared__ __attribute__((aligned(16))) char lds[FusedLds<T, D>::BYTES];
   __shared__ int s_phys[kMaxSplitPages];
   __shared__ int s_page[kMaxSplitPages];
@@ -81,61 +91,63 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   int32_t* cntC = cntB + BH;
   int32_t* err = a.ctl + kCtlError;
 
-  const int lane8 = blockIdx.x % kLanes;
+  const int lane = blockIdx.x % kMaxLanes;
   if (tid == 0)
-    s_ticket = __hip_atomic_fetch_add(a.ctl + kCtlTicket + kCtlStride * lane8, 1,
+    s_ticket = __hip_atomic_fetch_add(a.ctl + kCtlTicket + kCtlStride * lane, 1,
                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
-  int t = s_ticket;
-  const int nbh = (BH - lane8 + kLanes - 1) / kLanes;  // heads in this lane
-  int role = -1, i = 0, sub = 0;
-  if (t < nbh * g.fA) {
-    role = 0, i = t / g.fA, sub = t % g.fA;
-  } else if ((t -= nbh * g.fA) < nbh) {
-    role = 1, i = t;
-  } else if ((t -= nbh) < nbh * g.fC) {
-    role = 2, i = t / g.fC, sub = t % g.fC;
-  } else if ((t -= nbh * g.fC) < nbh * g.fD) {
-    role = 3, i = t / g.fD, sub = t % g.fD;
-  }
+  {
+    int t = s_ticket;
+    const int nbh = (BH - lane + kMaxLanes - 1) / kMaxLanes;  // heads in this lane
+    int role = -1, i = 0, sub = 0;
+    if (t < nbh * g.fA) {
+      role = 0, i = t / g.fA, sub = t % g.fA;
+    } else if ((t -= nbh * g.fA) < nbh) {
+      role = 1, i = t;
+    } else if ((t -= nbh) < nbh * g.fC) {
+      role = 2, i = t / g.fC, sub = t % g.fC;
+    } else if ((t -= nbh * g.fC) < nbh * g.fD) {
+      role = 3, i = t / g.fD, sub = t % g.fD;
+    }
 
-  if (role >= 0) {
-    const int bh = lane8 + kLanes * i;
-    const int b = bh / g.hk, h = bh - b * g.hk;
-    // the step's token goes to position seq_lens[b] if its logical page is mapped
-    const int pos = a.seq_lens[b];
-    const int lp = pos / g.P;
-    const int phys_tok = token_phys(g, a.pt, b, pos);
-    const bool tok_ok = phys_tok >= 0;
-    const int seq_len = pos + (tok_ok ? 1 : 0);
-    const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
+    if (role >= 0) {
+      const int bh = lane + kMaxLanes * i;
+      const int b = bh / g.hk, h = bh - b * g.hk;
+      // the step's token goes to position seq_lens[b] if its logical page is mapped
+      const int pos = a.seq_lens[b];
+      const int lp = pos / g.P;
+      const int phys_tok = token_phys(g, a.pt, b, pos);
+      const bool tok_ok = phys_tok >= 0;
+      const int seq_len = pos + (tok_ok ? 1 : 0);
+      const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
 
-    if (role == 0) {
-      StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
-      if (tok_ok)
-        tk = make_step_token<T>(g, a.step, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc, a.A);
-      const int ppb = (blockDim.x >> 6) * ScoreShape<T, D>::PPW * kFusedScoreIters;
-      score_role<T, D, kFusedScoreIters>(
-          g, sub * ppb,
-          reinterpret_cast<const T*>(a.q_cur) + b * a.q_bstride + (int64_t)h * g.G * D,
-          reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D, n_pages,
-          a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
-      block_signal(cntA + bh);
-    } else if (role == 1) {
-      topk_role<kTopkPer, 8>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
-                                reinterpret_cast<uint32_t*>(lds), small,
-                                [&] { block_wait(cntA + bh, g.fA, err); });
-      block_signal(cntB + bh);
-    } else if (role == 2) {
-      const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
-      attend_role<T, D, RTW>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
-                             s_page, s_mask, [&] { block_wait(cntB + bh, 1, err); });
-      block_signal(cntC + bh);
-    } else {
-      block_wait(cntC + bh, g.fC, err);
-      const int per_bh = g.G * a.mg.xs;
-      const int local = sub * (blockDim.x >> 6) + (tid >> 6);
-      if (local < per_bh) merge_unit<D, 16>(a.mg, bh * per_bh + local);
+      if (role == 0) {
+        StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
+        if (tok_ok)
+          tk = make_step_token<T>(g, a.step, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc, a.A);
+        const int ppb = kFusedWaves * ScoreShape<T, D>::PPW * kFusedScoreIters;
+        score_role<T, D, kFusedScoreIters>(
+            g, sub * ppb,
+            reinterpret_cast<const T*>(a.q_cur) + b * a.q_bstride + (int64_t)h * g.G * D,
+            reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D, n_pages,
+            a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
+        block_signal(cntA + bh);
+      } else if (role == 1) {
+        topk_role<kTopkPer, kFusedWaves>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
+                                  reinterpret_cast<uint32_t*>(lds), small,
+                                  [&] { block_wait(cntA + bh, g.fA, err); });
+        block_signal(cntB + bh);
+      } else if (role == 2) {
+        const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
+        attend_role<T, D, 1, MAXP>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
+                               s_page, s_mask, [&] { block_wait(cntB + bh, 1, err); });
+        block_signal(cntC + bh);
+      } else {
+        block_wait(cntC + bh, g.fC, err);
+        const int per_bh = g.G * a.mg.xs;
+        const int local = sub * (blockDim.x >> 6) + (tid >> 6);
+        if (local < per_bh) merge_unit<D, 8>(a.mg, bh * per_bh + local);
+      }
     }
   }
 
@@ -155,34 +167,28 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       const int pos = a.seq_lens[b];
       if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
     }
-    for (int l = tid; l < kLanes; l += blockDim.x) a.ctl[kCtlTicket + kCtlStride * l] = 0;
+    for (int l = tid; l < kMaxLanes; l += blockDim.x) a.ctl[kCtlTicket + kCtlStride * l] = 0;
     for (int e = tid; e < 3 * BH; e += blockDim.x) a.ctl[kCtlCounts + e] = 0;
     if (tid == 0) a.ctl[kCtlExit] = 0;
   }
 }
 
-template <typename T, int D, int RTW>
-hipError_t step_t(const StepArgs& a, hipStream_t s) {
-  const Geometry& g = a.g;
-  step_kernel<T, D, RTW><<<(unsigned)g.f_grid, 64 * g.waves, 0, s>>>(a);
-  return hipGetLastError();
-}
-
 template <typename T, int D>
-hipError_t step_d(const StepArgs& a, hipStream_t s) {
-  return a.g.rtw == 1 ? step_t<T, D, 1>(a, s) : step_t<T, D, 2>(a, s);
+hipError_t step_t(const StepArgs& a, hipStream_t s) {
+  step_kernel<T, D><<<(unsigned)a.g.f_grid, kThreads, 0, s>>>(a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-int fused_score_pages_per_block(int dtype, int D, int waves) {
+int fused_score_pages_per_block(int dtype, int D) {
   const int ppw = dtype == RETRO_BF16 ? (D == 128 ? ScoreShape<bf16_t, 128>::PPW : ScoreShape<bf16_t, 64>::PPW)
                                       : (D == 128 ? ScoreShape<float, 128>::PPW : ScoreShape<float, 64>::PPW);
-  return waves * ppw * kFusedScoreIters;
+  return kFusedWaves * ppw * kFusedScoreIters;
 }
 
 bool fused_supported(const Geometry& g) {
-  return g.max_pages <= kTopkPer * 64 * g.waves && g.waves >= 4 && g.waves <= 8 && g.G <= 16;
+  return g.max_pages <= kTopkPer * kThreads && g.G <= 16;
 }
 
 hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
@@ -196,7 +202,13 @@ hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, 
   StepArgs a;
   a.g = g;
   a.step = step;
-  a.at = make_attend_args(g, step, q_window, c, sel, phys, o_ws, l_ws);
+  // the attention tasks: one row tile per wavefront
+  Geometry ga = g;
+  ga.rtw = 1;
+  ga.waves = kFusedWaves;
+  ga.n_rgroups = g.f_rgroups;
+  ga.tiles_per_group = g.f_tpg;
+  a.at = make_attend_args(ga, step, q_window, c, sel, phys, o_ws, l_ws);
   a.tk = TopkArgs{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
                   sel.num_selected, phys};
   a.mg = make_merge_args(g, step, 2, o_ws, l_ws, sel.num_selected, nullptr, nullptr, nullptr,
@@ -213,8 +225,8 @@ hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, 
   a.A = c.last_loaded;
   a.scores = scores;
   a.ctl = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl);
-  if (g.dtype == RETRO_BF16) return g.D == 128 ? step_d<bf16_t, 128>(a, s) : step_d<bf16_t, 64>(a, s);
-  return g.D == 128 ? step_d<float, 128>(a, s) : step_d<float, 64>(a, s);
+  if (g.dtype == RETRO_BF16) return g.D == 128 ? step_t<bf16_t, 128>(a, s) : step_t<bf16_t, 64>(a, s);
+  return g.D == 128 ? step_t<float, 128>(a, s) : step_t<float, 64>(a, s);
 }
 
 }  // namespace retro
