@@ -4,6 +4,8 @@
 // threads unless stated) and takes its LDS from the caller.
 #pragma once
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace retro {
@@ -646,9 +648,10 @@ struct AttendArgs {
 // fused step waits there for the page selection), and only then is the page
 // list read.  Uses `lds` (2 * Tiles<T, D>::BUF_ELEMS elements, 16-byte aligned)
 // and three int arrays of kMaxSplitPages entries; MAXP bounds the 16-byte pieces
-// of a chunk per thread (ceil(Tiles::PIECES / threads)).  `seq_len_of()` gives the
+// of a chunk per thread (ceil(Tiles::PIECES / threads)); PAIR computes chunks
+// two at a time (more registers).  `seq_len_of()` gives the
 // sequence length in effect; it is called once the page-list loads are issued.
-template <typename T, int D, int RTW, int MAXP, typename SeqLen, typename Wait>
+template <typename T, int D, int RTW, int MAXP, bool PAIR, typename SeqLen, typename Wait>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
                                             SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
                                             int* s_mask, Wait&& wait) {
@@ -834,19 +837,33 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     }
   };
 
-  auto compute_chunk = [&](int c, int buf) {
-    const T* Ks = lds + buf * TL::BUF_ELEMS;
-    const T* Vs = Ks + TL::K_ELEMS;
-
-    // page facts for the two tiles of this chunk: stored tokens from the
-    // tile's first slot, mask value
-    int tlen[2], tmask[2];
+  // Attention over a group of NC chunks held in LDS (chunk c + i in buffer
+  // (buf0 + i) & 1; only the first nv hold data): S for all of the group's
+  // 16-token tiles, one online-softmax update over them, then O += P V per
+  // chunk.  Grouping two chunks gives each wavefront twice the independent
+  // matrix products per softmax step.
+  auto compute_group = [&](auto nc_tag, int c, int buf0, int nv) {
+    constexpr int NC = decltype(nc_tag)::value;
+    constexpr int NT = 2 * NC;  // tiles of the group
+    const T* Ks[NC];
+    const T* Vs[NC];
 #pragma unroll
-    for (int tile = 0; tile < 2; ++tile) {
-      const int pl = g.chunk_pages == 2 ? 2 * c + tile : c;
+    for (int i = 0; i < NC; ++i) {
+      Ks[i] = lds + ((buf0 + i) & 1) * TL::BUF_ELEMS;
+      Vs[i] = Ks[i] + TL::K_ELEMS;
+    }
+
+    // page facts of the group's tiles: stored tokens from the tile's first
+    // slot (0 past the group's valid chunks), mask value
+    int tlen[NT], tmask[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+      const int cc = c + tt / 2, tile = tt & 1;
+      const int pl = g.chunk_pages == 2 ? 2 * cc + tile : cc;
       const int so = g.chunk_pages == 2 ? 0 : 16 * tile;
-      tlen[tile] = s_len[pl] - so;
-      tmask[tile] = s_mask[pl];
+      const bool in = tt / 2 < nv;
+      tlen[tt] = in ? s_len[pl] - so : 0;
+      tmask[tt] = in ? s_mask[pl] : 0;
     }
 
 #pragma unroll
@@ -854,96 +871,106 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
       const int lt = wave + j * nwaves;
       if (lt >= g.tiles_per_group || rg * g.tiles_per_group + lt >= g.row_tiles) break;  // uniform
 
-      // ---- S^T = K . Q^T for both tiles
-      f32x4 s[2];
+      // ---- S^T = K . Q^T for every tile of the group
+      f32x4 s[NT];
 #pragma unroll
-      for (int tile = 0; tile < 2; ++tile) {
+      for (int tt = 0; tt < NT; ++tt) {
         f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
-        const T* krow = Ks + (tile * 16 + ln16) * TL::KROW;
-        if constexpr (sizeof(T) == 2) {
+        if (tt / 2 < nv) {  // uniform
+          const T* krow = Ks[tt / 2] + ((tt & 1) * 16 + ln16) * TL::KROW;
+          if constexpr (sizeof(T) == 2) {
 #pragma unroll
-          for (int kk = 0; kk < D / 32; ++kk) {
-            const bf16x8 kv = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 8 * g4);
-            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qop[j][kk], sacc, 0, 0, 0);
-          }
-        } else {
+            for (int kk = 0; kk < D / 32; ++kk) {
+              const bf16x8 kv = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 8 * g4);
+              sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qop[j][kk], sacc, 0, 0, 0);
+            }
+          } else {
 #pragma unroll
-          for (int kq = 0; kq < D / 16; ++kq) {
-            const f32x4 kv = *reinterpret_cast<const f32x4*>(krow + kq * 16 + 4 * g4);
+            for (int kq = 0; kq < D / 16; ++kq) {
+              const f32x4 kv = *reinterpret_cast<const f32x4*>(krow + kq * 16 + 4 * g4);
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[e], qop[j][kq][e], sacc, 0, 0, 0);
+              for (int e = 0; e < 4; ++e)
+                sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[e], qop[j][kq][e], sacc, 0, 0, 0);
+            }
           }
         }
-        s[tile] = sacc;
+        s[tt] = sacc;
       }
 
       // ---- mask, scale, online softmax (this lane: row ln16 of the tile)
-      float x[2][4];
+      float x[NT][4];
       float mloc = -INFINITY;
 #pragma unroll
-      for (int tile = 0; tile < 2; ++tile) {
-        const bool use = row_live[j] && tlen[tile] > 0 &&
-                         (row_r[j] == W || tmask[tile] < row_tau[j]);
+      for (int tt = 0; tt < NT; ++tt) {
+        const bool use = row_live[j] && tlen[tt] > 0 &&
+                         (row_r[j] == W || tmask[tt] < row_tau[j]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool ok = use && (4 * g4 + i) < tlen[tile];
-          x[tile][i] = ok ? s[tile][i] * a.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, x[tile][i]);
+          const bool ok = use && (4 * g4 + i) < tlen[tt];
+          x[tt][i] = ok ? s[tt][i] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, x[tt][i]);
         }
       }
       mloc = col_max4(mloc);
       const float m_new = fmaxf(m_run[j], mloc);
       const float mu = (m_new == -INFINITY) ? 0.f : m_new;
       const float alpha = exp2f(m_run[j] - mu);
-      float p[2][4];
+      float p[NT][4];
       float psum = 0.f;
 #pragma unroll
-      for (int tile = 0; tile < 2; ++tile)
+      for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          p[tile][i] = exp2f(x[tile][i] - mu);
-          psum += p[tile][i];
+          p[tt][i] = exp2f(x[tt][i] - mu);
+          psum += p[tt][i];
         }
       l_run[j] = l_run[j] * alpha + psum;
       m_run[j] = m_new;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) acc[j][dt] *= alpha;
 
-      // ---- O^T += V^T . P^T
-      if constexpr (sizeof(T) == 2) {
-        bf16x8 ph, pl;
+      // ---- O^T += V^T . P^T, chunk by chunk
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = p[e >> 2][e & 3];
-          const __bf16 hi = (__bf16)pv;
-          ph[e] = hi;
-          pl[e] = (__bf16)(pv - (float)hi);
-        }
+      for (int i = 0; i < NC; ++i) {
+        if (i >= nv) break;  // uniform
+        if constexpr (sizeof(T) == 2) {
+          bf16x8 ph, pl;
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          const int dr = dt * 16 + ln16;
-          const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(Vs + dr * TL::VROW + 4 * g4);
-          const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(Vs + (D + dr) * TL::VROW + 4 * g4);
-          const bf16x8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, acc[j][dt], 0, 0, 0);
-          acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, acc[j][dt], 0, 0, 0);
-        }
-      } else {
+          for (int e = 0; e < 8; ++e) {
+            const float pv = p[2 * i + (e >> 2)][e & 3];
+            const __bf16 hi = (__bf16)pv;
+            ph[e] = hi;
+            pl[e] = (__bf16)(pv - (float)hi);
+          }
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          const int dr = dt * 16 + ln16;
+          for (int dt = 0; dt < D / 16; ++dt) {
+            const int dr = dt * 16 + ln16;
+            const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(Vs[i] + dr * TL::VROW + 4 * g4);
+            const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(Vs[i] + (D + dr) * TL::VROW + 4 * g4);
+            const bf16x8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+            acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, acc[j][dt], 0, 0, 0);
+            acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, acc[j][dt], 0, 0, 0);
+          }
+        } else {
 #pragma unroll
-          for (int tile = 0; tile < 2; ++tile) {
-            const f32x4 vv = *reinterpret_cast<const f32x4*>(Vs + (tile * D + dr) * TL::VROW + 4 * g4);
+          for (int dt = 0; dt < D / 16; ++dt) {
+            const int dr = dt * 16 + ln16;
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[e], p[tile][e], acc[j][dt], 0, 0, 0);
+            for (int tile = 0; tile < 2; ++tile) {
+              const f32x4 vv =
+                  *reinterpret_cast<const f32x4*>(Vs[i] + (tile * D + dr) * TL::VROW + 4 * g4);
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[e], p[2 * i + tile][e],
+                                                                 acc[j][dt], 0, 0, 0);
+            }
           }
         }
       }
     }
-
+  };
+  auto compute_chunk = [&](int c, int buf) {
+    compute_group(std::integral_constant<int, 1>{}, c, buf, 1);
   };
 
   // Chunk c goes through LDS buffer c & 1.  That buffer was last read while
@@ -951,7 +978,23 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
   // compile-time constants (two chunks per trip when DEPTH == 2).
   uint32_t keep[DEPTH];
-  if constexpr (DEPTH == 2) {
+  if constexpr (PAIR && DEPTH == 2) {
+    // chunks in pairs: both of a pair in LDS and computed together while the
+    // next pair's loads are in flight
+    load_chunk(0, stage[0], keep[0]);
+    if (nchunks > 1) load_chunk(1, stage[1], keep[1]);
+#pragma unroll 1
+    for (int c = 0; c < nchunks; c += 2) {
+      const int nv = min(2, nchunks - c);
+      store_chunk(0, stage[0], keep[0]);
+      if (nv > 1) store_chunk(1, stage[1], keep[1]);
+      if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
+      if (c + 3 < nchunks) load_chunk(c + 3, stage[1], keep[1]);
+      __syncthreads();
+      compute_group(std::integral_constant<int, 2>{}, c, 0, nv);
+      if (c + 2 < nchunks) __syncthreads();  // the buffers are rewritten next trip
+    }
+  } else if constexpr (DEPTH == 2) {
     load_chunk(0, stage[0], keep[0]);
     if (nchunks > 1) load_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
 #pragma unroll 1

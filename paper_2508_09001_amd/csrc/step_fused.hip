@@ -139,7 +139,7 @@ step_kernel(StepArgs a) {
         block_signal(cntB + bh);
       } else if (role == 2) {
         const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
-        attend_role<T, D, 1, MAXP>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
+        attend_role<T, D, 1, MAXP, false>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
                                s_page, s_mask, [&] { block_wait(cntB + bh, 1, err); });
         block_signal(cntC + bh);
       } else {
