@@ -38,12 +38,19 @@ def sources_sha256(paths) -> str:
 
 
 def _short(name: str) -> str:
-    for marker in ("(anonymous namespace)::", "retro::"):
-        i = name.find(marker)
-        if i >= 0:
-            name = name[i + len(marker):]
-    j = name.find("(")
-    return name[:j] if j > 0 else name
+    """Kernel name without return type, namespaces and parameter list."""
+    if name.startswith("void "):
+        name = name[5:]
+    name = name.replace("retro::(anonymous namespace)::", "").replace("retro::", "")
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
 
 
 def kernel_durations(out_dir: str) -> dict:
