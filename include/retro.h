@@ -136,7 +136,11 @@ const char* retro_status_string(int32_t status);
 /* Validate dims; on success write k_max = min(budget_tokens / page_size, max_pages). */
 retro_status retro_k_max(const retro_dims* dims, int32_t* k_max);
 
-/* Bytes of scratch the select / attend / step calls need for these dims. */
+/* Bytes of scratch the select / attend / step calls need for these dims.  The
+ * workspace holds, besides scratch, counters that let one launch hand work from
+ * its workgroups to a last one: zero-fill it once before its first use (every
+ * call leaves those counters at zero again when it completes), and let one call
+ * at a time use it (calls sharing a workspace are ordered on one stream). */
 retro_status retro_workspace_size(const retro_dims* dims, size_t* bytes);
 
 /* Bulk-store n_tokens tokens of sequence `seq` at positions start_pos ..
@@ -214,11 +218,9 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
  * semantics, without materialising o_part / lse_part.
  * With RETRO_STEP_FUSED=1 in the environment (read on every call) the step runs
  * as one launch whose workgroups hand work to each other through counters kept
- * in `workspace`: the workspace must then be zero-filled once before its first
- * use, and every such call leaves those counters at zero again on completion.
- * A workspace is used by one call at a time (calls sharing it are ordered on
- * one stream).  If a hand-off wait ever exceeds its bound the launch completes
- * with unspecified outputs instead of hanging. */
+ * in `workspace` (zero-filled once, as for every call).  If a hand-off wait
+ * there ever exceeds its bound the launch completes with unspecified outputs
+ * instead of hanging. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,

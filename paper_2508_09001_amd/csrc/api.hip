@@ -90,6 +90,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * x.n_splits * x.R * sizeof(float));
   x.ws_ctl = off;
   off += align256((kCtlCounts + 3 * bhs) * sizeof(int32_t));
+  x.ws_sel = off;  // per-head counters of the score + selection launch
+  off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -191,9 +193,11 @@ retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   float* scores = ws_at(workspace, g.ws_scores);
+  int32_t* counters = reinterpret_cast<int32_t*>((char*)workspace + g.ws_sel);
   hipError_t e = retro::launch_score(g, step, q_cur, (int64_t)g.hq * g.D, *cache, nullptr, nullptr,
-                                     scores, s);
-  if (e == hipSuccess) e = retro::launch_topk_mask(g, step, scores, *cache, *sel, nullptr, s);
+                                     scores, sel, nullptr, counters, s);
+  if (e == hipSuccess && !retro::score_selects(g))
+    e = retro::launch_topk_mask(g, step, scores, *cache, *sel, nullptr, s);
   return from_hip(e);
 }
 
@@ -278,12 +282,15 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   const int64_t qbs = (int64_t)(g.W + 1) * g.hq * g.D;
   const char* q_cur = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
-  // score (+ the token's append) -> top-k + mask -> attention -> combine + merge
+  // score (+ the token's append, + top-k + mask) -> attention -> combine + merge
   // (+ seq_lens advance)
   Geometry gp = g;
   gp.token_pending = 1;
-  hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores, s);
-  if (e == hipSuccess) e = retro::launch_topk_mask(gp, step, scores, *cache, *sel, phys, s);
+  int32_t* counters = reinterpret_cast<int32_t*>((char*)workspace + g.ws_sel);
+  hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores, sel, phys,
+                                     counters, s);
+  if (e == hipSuccess && !retro::score_selects(gp))
+    e = retro::launch_topk_mask(gp, step, scores, *cache, *sel, phys, s);
   if (e == hipSuccess)
     e = retro::launch_attend(gp, step, q_window, *cache, *sel, phys, o_ws, l_ws, s);
   if (e == hipSuccess)

@@ -58,7 +58,7 @@ struct Geometry {
   int64_t f_grid;
   bool fused;
   // workspace layout (bytes)
-  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_total;
+  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_sel, ws_total;
   // set for the launches of a step whose token is written by its score launch:
   // seq_lens does not count the token yet (the merge launch advances it), and
   // every launch uses the length with the token
@@ -75,6 +75,10 @@ constexpr int kCtlExit = 256;
 constexpr int kCtlError = 257;
 constexpr int kCtlCounts = 512;
 constexpr int kFusedScoreIters = 4;
+// counters of the score + selection launch: per KV head 1 + kSelMaxGroups
+// counters, each kSelCounterInts apart (one 128-byte line)
+constexpr int kSelCounterInts = 32;
+constexpr int kSelMaxGroups = 8;
 constexpr int kFusedWaves = 8;
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
@@ -89,9 +93,14 @@ hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, i
                           const void* k_src, const void* v_src, hipStream_t s);
 // With g.token_pending, the score launch also appends the step's token
 // (k_new, v_new: [batch][h_k][d]) as AppendKV does, without advancing seq_lens.
+// With a selection, counters ([batch * h_k] ints of the workspace, zero
+// between launches) and score_selects(g), it also runs top-k + mask (the last
+// workgroup of each KV head); otherwise launch_topk_mask must follow.
+bool score_selects(const Geometry& g);
 hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t q_batch_stride,
                         const retro_kv_cache& c, const void* k_new, const void* v_new,
-                        float* scores, hipStream_t s);
+                        float* scores, const retro_selection* sel, int32_t* sel_phys,
+                        int32_t* counters, hipStream_t s);
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
                             const retro_kv_cache& c, const retro_selection& sel,
                             int32_t* sel_phys, hipStream_t s);

@@ -204,8 +204,10 @@ __device__ __forceinline__ void f32_to_words(const float* in, uint32_t* w) {
   }
 }
 
-// The step's own token, appended by the score block whose pages include it
-// (fused step): AppendKV, the digest update and Alg. 2's first line.
+// The step's own token, appended by the score block whose pages include it:
+// AppendKV and the digest update.  Alg. 2's first line (last_loaded of the
+// token's page = step - 1) is applied by the selection (topk_role), which owns
+// every last_loaded write of the step.
 template <typename T>
 struct StepToken {
   int lp;            // logical page of the token (-1: none)
@@ -214,8 +216,6 @@ struct StepToken {
   const T* v;        // [d] value of this KV head
   T* k_row;          // the slot's key row (token-major page)
   T* v_col;          // the slot's value column (d-major page): element i at v_col[i * P]
-  int32_t* a_entry;  // last_loaded entry of the page
-  int step;
 };
 
 // Physical page that receives the token at position pos of sequence b, or -1
@@ -238,10 +238,9 @@ __device__ __forceinline__ int live_seq_len(const Geometry& g, const int32_t* se
 // The token of KV head h of sequence b at position pos, stored in physical page
 // phys (>= 0), as the score role appends it.
 template <typename T>
-__device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int step, int b, int h,
-                                                        int pos, int phys, const void* k_new,
-                                                        const void* v_new, void* kc, void* vc,
-                                                        int32_t* A) {
+__device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b, int h, int pos,
+                                                        int phys, const void* k_new,
+                                                        const void* v_new, void* kc, void* vc) {
   const int lp = pos / g.P, slot = pos - lp * g.P;
   const int64_t bh = (int64_t)b * g.hk + h;
   const int64_t ph = (int64_t)phys * g.hk + h;
@@ -252,8 +251,6 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int s
   tk.v = reinterpret_cast<const T*>(v_new) + bh * g.D;
   tk.k_row = reinterpret_cast<T*>(kc) + (ph * g.P + slot) * g.D;
   tk.v_col = reinterpret_cast<T*>(vc) + ph * g.D * g.P + slot;
-  tk.a_entry = A + bh * g.max_pages + lp;
-  tk.step = step;
   return tk;
 }
 
@@ -361,14 +358,16 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
       s = s + dpp_f<kDppShl8>(s);
       Ssum = (gq == 0) ? s : Ssum + s;
     }
-    if (page < n_pages && c == 0) srow[page] = Ssum + 0.0f;
+    // device-coherent store: a later reader of the same launch (the selection)
+    // may run on another XCD
+    if (page < n_pages && c == 0)
+      __hip_atomic_store(srow + page, Ssum + 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (has_tok) {
     for (int i = tid; i < D; i += blockDim.x) {
       tok.k_row[i] = tok.k[i];
       tok.v_col[(int64_t)i * g.P] = tok.v[i];
     }
-    if (tid == 0) *tok.a_entry = tok.step - 1;
   }
 }
 
@@ -401,9 +400,10 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 
 // THREADS = blockDim.x threads (at most MAXW wavefronts); page i of the
 // sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
-// loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by this step's token
-// (-1: none); its last_loaded entry is read as step - 1, the value the append
-// gives it.  `pages_of()` gives n, the pages of the sequence; it is called once
+// loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by
+// this step's token (-1: none): Alg. 2's first line applies to it, so its
+// last_loaded entry is taken as step - 1, and set to step - 1 if the page is
+// not kept.  `pages_of()` gives n, the pages of the sequence; it is called once
 // the loads are issued.  hist: kTopkHistWords uint32 of LDS; small: kTopkSmall
 // ints of LDS.
 // `wait()` is called after the page-table and last_loaded loads are issued and
@@ -438,9 +438,11 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
   }
   for (int i = tid; i < kTopkHistWords; i += THREADS) hist[i] = 0u;
   wait();
-  float sv[PER];
+  float sv[PER];  // device-coherent loads: the scores may come from other XCDs of this launch
 #pragma unroll
-  for (int j = 0; j < PER; ++j) sv[j] = srow[min(j * THREADS + tid, last)];
+  for (int j = 0; j < PER; ++j)
+    sv[j] = __hip_atomic_load(srow + min(j * THREADS + tid, last), __ATOMIC_RELAXED,
+                              __HIP_MEMORY_SCOPE_AGENT);
   const int n = pages_of();
   auto valid = [&](int j) { return j * THREADS + tid < n; };
 #pragma unroll
@@ -540,6 +542,31 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
       need -= above;
       prefix = (prefix << (hi - lo)) | (uint32_t)bin;
       if (inbin == need) break;  // T's whole bin is kept: its prefix suffices
+      if (lo > 0 && inbin <= 64) {
+        // T is one of the bin's few keys: list them (in the next pass's
+        // histogram, still zero) and rank them exactly, every wavefront on its
+        // own, instead of histogramming further digits.
+        uint32_t* cand = hist + (pass + 1) * kTopkBins;  // [0]: count, [1..]: rel values
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          const uint64_t rel = key[j] - kmin;
+          if (valid(j) && (rel >> lo) == prefix) cand[1 + atomicAdd(&cand[0], 1u)] = (uint32_t)rel;
+        }
+        __syncthreads();
+        const uint32_t v = lane < (int)inbin ? cand[1 + lane] : 0u;
+        uint32_t gt = 0u, eq = 0u;  // candidates above / equal to this lane's
+        for (int j2 = 0; j2 < (int)inbin; ++j2) {
+          const uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)v, j2);
+          gt += w > v ? 1u : 0u;
+          eq += w == v ? 1u : 0u;
+        }
+        const bool is_t = lane < (int)inbin && gt < need && need <= gt + eq;
+        const int st = __builtin_ctzll(wave_ballot(is_t));
+        prefix = (uint32_t)__builtin_amdgcn_readlane((int)v, st);  // T's whole rel
+        need -= (uint32_t)__builtin_amdgcn_readlane((int)gt, st);   // keys equal to T to take
+        lo = 0;
+        break;
+      }
     }
   }
 
@@ -590,12 +617,14 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
     int pos = -1;
     if (is_gt) pos = gb + min(eb, (int)need);
     if (is_eq && eb < (int)need) pos = gb + eb;
+    const int p = j * THREADS + tid;
     if (pos >= 0 && pos < k) {  // always true for a kept page; guards the writes
-      const int p = j * THREADS + tid;
       sel_row[pos] = p;
       m_row[pos] = a_old[j];
       a_row[p] = step;
       if (ph_row) ph_row[pos] = (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1;
+    } else if (p == tok_lp) {
+      a_row[p] = step - 1;  // the token's page, not kept
     }
   }
   for (int i = k + tid; i < g.k_max; i += THREADS) {

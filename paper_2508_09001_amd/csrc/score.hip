@@ -2,6 +2,18 @@
 // the fixed fp32 order described in roles.h (score_role).  Digests are stored
 // per logical page, so a KV head's digests form one contiguous stream; a
 // workgroup of four wavefronts scores a block of consecutive pages.
+//
+// With a selection epilogue (PER > 0) the kernel also runs PageSelect and
+// UpdateAndBuildMask: the last workgroup of each KV head runs the top-k + mask
+// role on the head's scores (see topk.hip for the algorithm), then clears the
+// head's counter for the next launch.  Scores are written and read with
+// device-coherent (agent-scope) atomic stores and loads, which bypass the
+// per-XCD L2s; a workgroup counts itself out only after its score stores have
+// completed, so the last one reads them all without any L2 write-back or
+// invalidation (fences at device scope would write back and invalidate whole
+// L2s, once per workgroup).
+#include <algorithm>
+
 #include "roles.h"
 
 namespace retro {
@@ -12,63 +24,134 @@ namespace {
 constexpr int kScoreIters = 1;
 
 struct TokenArgs {
-  int step;
   const void* k_new;
   const void* v_new;
   void* kc;
   void* vc;
   const int32_t* pt;
-  int32_t* A;
 };
 
-template <typename T, int D>
+struct SelectArgs {
+  TopkArgs tk;
+  // per KV head: a head counter, then one counter per group of `group`
+  // workgroups, each in a 128-byte line of its own (kSelCounterInts apart);
+  // zero between launches
+  int32_t* count;
+  int group;
+};
+
+template <typename T, int D, int PER>
 __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restrict__ q,
                                                    int64_t q_bstride, T* __restrict__ dg,
                                                    const int32_t* __restrict__ seq_lens,
-                                                   float* __restrict__ scores, TokenArgs ta) {
-  extern __shared__ float sq[];  // [G][D] the group's current queries, as fp32
+                                                   float* __restrict__ scores, TokenArgs ta,
+                                                   SelectArgs sa) {
+  // [G][D] fp32 queries while scoring; the top-k histograms and scratch after
+  extern __shared__ __attribute__((aligned(16))) float dyn_lds[];
   constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
   const int pos = seq_lens[b];
-  StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
+  StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
   int seq_len = pos;
   if (g.token_pending) {
     const int phys = token_phys(g, ta.pt, b, pos);
     if (phys >= 0) {
       seq_len = pos + 1;
-      tk = make_step_token<T>(g, ta.step, b, h, pos, phys, ta.k_new, ta.v_new, ta.kc, ta.vc, ta.A);
+      tk = make_step_token<T>(g, b, h, pos, phys, ta.k_new, ta.v_new, ta.kc, ta.vc);
     }
   }
   const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
+  int32_t warm_a = 0, warm_p = 0;
+  if constexpr (PER > 0) {
+    // Fetch this workgroup's last_loaded and page-table entries along with its
+    // digests, so that the selection finds them in the caches.
+    const int p = blockIdx.x * PPB + (threadIdx.x & (PPB - 1));
+    if (threadIdx.x < PPB && p < g.max_pages) {
+      warm_a = sa.tk.A[bh * g.max_pages + p];
+      warm_p = sa.tk.pt[(int64_t)b * g.max_pages + p];
+    }
+  }
   score_role<T, D, kScoreIters>(g, blockIdx.x * PPB, q + b * q_bstride + (int64_t)h * g.G * D,
                                 dg + bh * g.max_pages * 2 * D, n_pages, scores + bh * g.max_pages,
-                                sq, tk);
+                                dyn_lds, tk);
+  if constexpr (PER > 0) {
+    asm volatile("" : : "v"(warm_a), "v"(warm_p));  // keeps the two loads
+    __shared__ int s_last;
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's score stores have completed
+    __syncthreads();
+    // Count out in two levels (a group of workgroups, then the head), so that
+    // no counter takes more than max(group, number of groups) updates.
+    if (threadIdx.x == 0) {
+      const int ngroups = (gridDim.x + sa.group - 1) / sa.group;
+      int32_t* head = sa.count + bh * (int64_t)kSelCounterInts * (1 + kSelMaxGroups);
+      const int grp = blockIdx.x / sa.group;
+      const int in_grp = min(sa.group, (int)gridDim.x - grp * sa.group);
+      int32_t* gc = head + kSelCounterInts * (1 + grp);
+      bool last = false;
+      if (__hip_atomic_fetch_add(gc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == in_grp - 1) {
+        __hip_atomic_store(gc, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = __hip_atomic_fetch_add(head, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               ngroups - 1;
+        if (last) __hip_atomic_store(head, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      s_last = last;
+    }
+    __syncthreads();
+    if (s_last) {
+      uint32_t* hist = reinterpret_cast<uint32_t*>(dyn_lds);
+      int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
+      topk_role<PER, 4>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
+    }
+  }
+}
+
+template <typename T, int D, int PER>
+hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
+                   const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
+                   const SelectArgs& sa, hipStream_t s) {
+  constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
+  static_assert(PPB == 16, "the selection counters assume 16 pages per workgroup");
+  dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
+  size_t lds = sizeof(float) * g.G * D;
+  if (PER > 0) lds = std::max(lds, sizeof(int32_t) * (kTopkHistWords + kTopkSmall));
+  const TokenArgs ta{k_new, v_new, c.k_cache, c.v_cache, c.page_table};
+  score_kernel<T, D, PER><<<grid, 256, lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens,
+                                                 scores, ta, sa);
+  return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
+hipError_t score_d(const Geometry& g, int step, const void* q, int64_t qbs,
                    const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
-                   hipStream_t s) {
-  constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
-  dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
-  const size_t lds = sizeof(float) * g.G * D;
-  const TokenArgs ta{step, k_new, v_new, c.k_cache, c.v_cache, c.page_table, c.last_loaded};
-  score_kernel<T, D><<<grid, 256, lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens, scores,
-                                            ta);
-  return hipGetLastError();
+                   const SelectArgs& sa, hipStream_t s) {
+  if (!sa.count) return score_t<T, D, 0>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  if (g.max_pages <= 256 * 4) return score_t<T, D, 4>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  if (g.max_pages <= 256 * 12) return score_t<T, D, 12>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  return score_t<T, D, 24>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
 }
 
 }  // namespace
 
+bool score_selects(const Geometry& g) { return g.max_pages <= 256 * 24; }
+
 hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t q_batch_stride,
                         const retro_kv_cache& c, const void* k_new, const void* v_new,
-                        float* scores, hipStream_t s) {
+                        float* scores, const retro_selection* sel, int32_t* sel_phys,
+                        int32_t* counters, hipStream_t s) {
+  SelectArgs sa{};
+  if (sel && counters && score_selects(g)) {
+    sa.tk = TopkArgs{g, step, scores, c.page_table, c.last_loaded, sel->selected, sel->mask,
+                     sel->num_selected, sel_phys};
+    sa.count = counters;
+    const int blocks = (g.max_pages + 15) / 16;  // workgroups per KV head (16 pages each)
+    sa.group = std::max(16, (blocks + kSelMaxGroups - 1) / kSelMaxGroups);
+  }
   if (g.dtype == RETRO_BF16)
-    return g.D == 128 ? score_t<bf16_t, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, s)
-                      : score_t<bf16_t, 64>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, s);
-  return g.D == 128 ? score_t<float, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, s)
-                    : score_t<float, 64>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, s);
+    return g.D == 128 ? score_d<bf16_t, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s)
+                      : score_d<bf16_t, 64>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s);
+  return g.D == 128 ? score_d<float, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s)
+                    : score_d<float, 64>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s);
 }
 
 }  // namespace retro

@@ -122,9 +122,9 @@ step_kernel(StepArgs a) {
       const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
 
       if (role == 0) {
-        StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
+        StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
         if (tok_ok)
-          tk = make_step_token<T>(g, a.step, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc, a.A);
+          tk = make_step_token<T>(g, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc);
         const int ppb = kFusedWaves * ScoreShape<T, D>::PPW * kFusedScoreIters;
         score_role<T, D, kFusedScoreIters>(
             g, sub * ppb,

@@ -32,10 +32,16 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
   __shared__ int small[kTopkSmall];
   const int bh = blockIdx.x;
   const int b = bh / ta.g.hk;
+  // a pending token (Geometry::token_pending) gets Alg. 2's first line here
+  int tok_lp = -1;
+  if (ta.g.token_pending) {
+    const int pos = seq_lens[b];
+    if (token_phys(ta.g, ta.pt, b, pos) >= 0) tok_lp = pos / ta.g.P;
+  }
   topk_role<PER, THREADS / 64>(
       ta, bh,
       [&] { return min((live_seq_len(ta.g, seq_lens, ta.pt, b) + ta.g.P - 1) / ta.g.P, ta.g.max_pages); },
-      -1, hist, small, [] {});
+      tok_lp, hist, small, [] {});
 }
 
 }  // namespace
