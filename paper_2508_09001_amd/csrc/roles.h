@@ -1065,9 +1065,12 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
         const f32x4 o = acc[j][dt] * inv;
-        *reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4) = o;
+        // streamed out: read once by the combine, not worth keeping in L2
+        __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4));
       }
-      if (g4 == 0) a.l_ws[part + rho] = l > 0.f ? (m_run[j] + __log2f(l)) * kLn2 : -INFINITY;
+      if (g4 == 0)
+        __builtin_nontemporal_store(l > 0.f ? (m_run[j] + __log2f(l)) * kLn2 : -INFINITY,
+                                    a.l_ws + part + rho);
     }
   }
 }

@@ -20,7 +20,8 @@ namespace retro {
 namespace {
 
 // One pass of four pages per wavefront: many small workgroups keep several
-// wavefronts per SIMD busy, which hides the dependent add chains of the tree.
+// wavefronts per SIMD busy, which hides the dependent add chains of the tree
+// (two passes per workgroup measured slower).
 constexpr int kScoreIters = 1;
 
 struct TokenArgs {
@@ -111,7 +112,7 @@ hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
                    const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
                    const SelectArgs& sa, hipStream_t s) {
   constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
-  static_assert(PPB == 16, "the selection counters assume 16 pages per workgroup");
+  static_assert(PPB == 4 * 4 * kScoreIters, "pages per workgroup as the selection counters assume");
   dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
   size_t lds = sizeof(float) * g.G * D;
   if (PER > 0) lds = std::max(lds, sizeof(int32_t) * (kTopkHistWords + kTopkSmall));
@@ -144,7 +145,8 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
     sa.tk = TopkArgs{g, step, scores, c.page_table, c.last_loaded, sel->selected, sel->mask,
                      sel->num_selected, sel_phys};
     sa.count = counters;
-    const int blocks = (g.max_pages + 15) / 16;  // workgroups per KV head (16 pages each)
+    constexpr int PPB = 4 * 4 * kScoreIters;  // pages per workgroup (four pages per wavefront pass)
+    const int blocks = (g.max_pages + PPB - 1) / PPB;  // workgroups per KV head
     sa.group = std::max(16, (blocks + kSelMaxGroups - 1) / kSelMaxGroups);
   }
   if (g.dtype == RETRO_BF16)
