@@ -224,7 +224,7 @@ def main():
                    "budget_tokens": spec.budget, "window": spec.window, "layers_rotated": L,
                    "launch": "hip-graph per step",
                    "step_path": ("single launch" if os.environ.get("RETRO_STEP_FUSED") == "1"
-                                 else "four launches")},
+                                 else "three launches")},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
