@@ -293,6 +293,15 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
     if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
   const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page0 + nw * S::PPW * ITERS;
+  // the token's key and value, element tid, for the append at the end: read
+  // now so that the append does not wait for a round trip of its own (every
+  // workgroup running this role has at least 256 threads)
+  static_assert(D <= 256, "one element per thread");
+  T tok_k = T{}, tok_v = T{};
+  if (has_tok) {  // uniform
+    tok_k = tok.k[min(tid, D - 1)];
+    tok_v = tok.v[min(tid, D - 1)];
+  }
   float kv[S::VEC];
   if (has_tok) {
     uint32_t kw[S::WORDS];
@@ -363,11 +372,9 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
     if (page < n_pages && c == 0)
       __hip_atomic_store(srow + page, Ssum + 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (has_tok) {
-    for (int i = tid; i < D; i += blockDim.x) {
-      tok.k_row[i] = tok.k[i];
-      tok.v_col[(int64_t)i * g.P] = tok.v[i];
-    }
+  if (has_tok && tid < D) {
+    tok.k_row[tid] = tok_k;
+    tok.v_col[(int64_t)tid * g.P] = tok_v;
   }
 }
 
@@ -390,7 +397,7 @@ struct TopkArgs {
 constexpr int kTopkBins = 2048;    // bins of an 11-bit digit
 constexpr int kTopkPasses = 3;     // 11 + 11 + 10 bits cover a 32-bit key
 constexpr int kTopkHistWords = kTopkPasses * kTopkBins;  // one histogram per pass
-constexpr int kTopkSmall = 32 + 256;  // ints: min/max exchange + per-(stripe, wave) counts
+constexpr int kTopkSmall = 32 + 4 + 256;  // ints: min/max exchange, pass result, per-(stripe, wave) counts
 
 __device__ __forceinline__ uint64_t wave_ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 // number of set bits of m in lanes below this one
@@ -412,7 +419,7 @@ template <int PER, int MAXW, typename PagesOf, typename Wait>
 __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
                                           uint32_t* hist, int* small, Wait&& wait) {
   constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
-  static_assert(PER * MAXW <= kTopkSmall - 32 && MAXW <= 16 && PER <= 32, "top-k shape");
+  static_assert(PER * MAXW <= kTopkSmall - 36 && MAXW <= 16 && PER <= 32, "top-k shape");
   const int THREADS = blockDim.x, NW = THREADS >> 6;
   const Geometry& g = ta.g;
   const int step = ta.step;
@@ -423,7 +430,8 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
   int32_t* a_row = ta.A + (int64_t)bh * g.max_pages;
   const int32_t* p_row = ta.pt + (int64_t)b * g.max_pages;
   int* red = small;        // [32]
-  int* cnt = small + 32;   // [PER * NW]
+  int* res = small + 32;   // [4]: T's digit, keys above its bin, keys in it
+  int* cnt = small + 36;   // [PER * NW]
 
   // Loads are issued for every stripe slot before the number of pages is known
   // (an in-bounds index stands in for slots past the row; their values are
@@ -467,18 +475,18 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
     red[16 + wave] = (int)kmax;
   }
   __syncthreads();  // also orders the histogram clearing before the first pass
-  for (int w = 0; w < NW; ++w) {
-    kmin = min(kmin, (uint32_t)red[w]);
-    kmax = max(kmax, (uint32_t)red[16 + w]);
-  }
+  kmin = wave_umin(lane < NW ? (uint32_t)red[lane] : 0xFFFFFFFFu);
+  kmax = wave_umax(lane < NW ? (uint32_t)red[16 + lane] : 0u);
   const uint32_t range = kmax - kmin;
   const int nbits = range ? 32 - __clz((int)range) : 1;
   const int k = min(g.budget / g.P, n);
 
   // Radix select: pass p histograms the next digit of the keys that still match
-  // T's prefix into its own histogram; after one barrier every wavefront scans
-  // the histogram by itself (descending bins, lane l owning 32 of them), so the
-  // digit reaches all threads without a second barrier.
+  // T's prefix into its own histogram.  After a barrier, wavefront 0 alone
+  // scans it (descending bins, lane l owning 32 of them) and publishes T's
+  // digit, the keys above its bin and the keys in it; the other wavefronts
+  // wait at the next barrier (a scan by every wavefront would share the four
+  // SIMDs between sixteen copies of the same work).
   uint64_t prefix = 0u;  // digits of T's rel fixed so far, bits [lo, nbits)
   int lo = nbits;
   uint32_t need = (uint32_t)k;  // keys still to take among those matching the prefix
@@ -495,78 +503,59 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
         if (valid(j) && (rel >> hi) == prefix) atomicAdd(&h[(rel >> lo) & dmask], 1u);
       }
       __syncthreads();
-      const int base = kTopkBins - 32 * (lane + 1);
-      uint32_t gs[8];  // totals of this lane's eight 4-bin groups (ascending bins)
+      if (wave == 0) {
+        const int base = kTopkBins - 32 * (lane + 1);
+        uint32_t gs[8];  // totals of this lane's eight 4-bin groups (ascending bins)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * i);
-        gs[i] = u.x + u.y + u.z + u.w;
+        for (int i = 0; i < 8; ++i) {
+          const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * i);
+          gs[i] = u.x + u.y + u.z + u.w;
+        }
+        uint32_t own = 0u;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) own += gs[i];
+        const uint32_t incl = (uint32_t)wave_inclusive_scan((int)own);
+        uint32_t acc = incl - own;  // keys in higher bins
+        const bool hit = acc < need && need <= incl;
+        // the group holding T's digit (highest group first), then the bin in it
+        int fgrp = 0;
+        uint32_t facc = 0u;
+        bool found = false;
+#pragma unroll
+        for (int i = 7; i >= 0; --i) {
+          const bool f = !found && acc + gs[i] >= need;
+          fgrp = f ? i : fgrp;
+          facc = f ? acc : facc;
+          found = found || f;
+          acc += gs[i];
+        }
+        const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * fgrp);
+        const uint32_t gv[4] = {u.x, u.y, u.z, u.w};
+        int fb = 0;
+        uint32_t fc = 0u, fa = 0u;
+        found = false;
+        acc = facc;
+#pragma unroll
+        for (int i = 3; i >= 0; --i) {
+          const bool f = !found && acc + gv[i] >= need;
+          fb = f ? base + 4 * fgrp + i : fb;
+          fc = f ? gv[i] : fc;
+          fa = f ? acc : fa;
+          found = found || f;
+          acc += gv[i];
+        }
+        if (hit) {  // exactly one lane: need lies in its range of the running total
+          res[0] = fb;
+          res[1] = (int)fa;
+          res[2] = (int)fc;
+        }
       }
-      uint32_t own = 0u;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) own += gs[i];
-      const uint32_t incl = (uint32_t)wave_inclusive_scan((int)own);
-      uint32_t acc = incl - own;  // keys in higher bins
-      const bool hit = acc < need && need <= incl;
-      // the group holding T's digit (highest group first), then the bin in it
-      int fgrp = 0;
-      uint32_t facc = 0u;
-      bool found = false;
-#pragma unroll
-      for (int i = 7; i >= 0; --i) {
-        const bool f = !found && acc + gs[i] >= need;
-        fgrp = f ? i : fgrp;
-        facc = f ? acc : facc;
-        found = found || f;
-        acc += gs[i];
-      }
-      const uint4 u = *reinterpret_cast<const uint4*>(h + base + 4 * fgrp);
-      const uint32_t gv[4] = {u.x, u.y, u.z, u.w};
-      int fb = 0;
-      uint32_t fc = 0u, fa = 0u;
-      found = false;
-      acc = facc;
-#pragma unroll
-      for (int i = 3; i >= 0; --i) {
-        const bool f = !found && acc + gv[i] >= need;
-        fb = f ? base + 4 * fgrp + i : fb;
-        fc = f ? gv[i] : fc;
-        fa = f ? acc : fa;
-        found = found || f;
-        acc += gv[i];
-      }
-      const int src = __builtin_ctzll(wave_ballot(hit));
-      const int bin = __builtin_amdgcn_readlane(fb, src);
-      const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)fa, src);
-      const uint32_t inbin = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
+      __syncthreads();
+      const int bin = res[0];
+      const uint32_t above = (uint32_t)res[1], inbin = (uint32_t)res[2];
       need -= above;
       prefix = (prefix << (hi - lo)) | (uint32_t)bin;
       if (inbin == need) break;  // T's whole bin is kept: its prefix suffices
-      if (lo > 0 && inbin <= 64) {
-        // T is one of the bin's few keys: list them (in the next pass's
-        // histogram, still zero) and rank them exactly, every wavefront on its
-        // own, instead of histogramming further digits.
-        uint32_t* cand = hist + (pass + 1) * kTopkBins;  // [0]: count, [1..]: rel values
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-          const uint64_t rel = key[j] - kmin;
-          if (valid(j) && (rel >> lo) == prefix) cand[1 + atomicAdd(&cand[0], 1u)] = (uint32_t)rel;
-        }
-        __syncthreads();
-        const uint32_t v = lane < (int)inbin ? cand[1 + lane] : 0u;
-        uint32_t gt = 0u, eq = 0u;  // candidates above / equal to this lane's
-        for (int j2 = 0; j2 < (int)inbin; ++j2) {
-          const uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)v, j2);
-          gt += w > v ? 1u : 0u;
-          eq += w == v ? 1u : 0u;
-        }
-        const bool is_t = lane < (int)inbin && gt < need && need <= gt + eq;
-        const int st = __builtin_ctzll(wave_ballot(is_t));
-        prefix = (uint32_t)__builtin_amdgcn_readlane((int)v, st);  // T's whole rel
-        need -= (uint32_t)__builtin_amdgcn_readlane((int)gt, st);   // keys equal to T to take
-        lo = 0;
-        break;
-      }
     }
   }
 

@@ -1,12 +1,14 @@
 // Page criticality score, eq. (quest_score), per (sequence, KV head, page), in
 // the fixed fp32 order described in roles.h (score_role).  Digests are stored
 // per logical page, so a KV head's digests form one contiguous stream; a
-// workgroup of four wavefronts scores a block of consecutive pages.
+// workgroup scores a block of consecutive pages, four per wavefront.
 //
 // With a selection epilogue (PER > 0) the kernel also runs PageSelect and
 // UpdateAndBuildMask: the last workgroup of each KV head runs the top-k + mask
 // role on the head's scores (see topk.hip for the algorithm), then clears the
-// head's counter for the next launch.  Scores are written and read with
+// head's counter for the next launch.  That role runs in one workgroup per
+// head, so its time is the instruction count of one wavefront: workgroups of
+// sixteen wavefronts give each thread at most PER = 1..6 pages of the head.  Scores are written and read with
 // device-coherent (agent-scope) atomic stores and loads, which bypass the
 // per-XCD L2s; a workgroup counts itself out only after its score stores have
 // completed, so the last one reads them all without any L2 write-back or
@@ -19,10 +21,16 @@
 namespace retro {
 namespace {
 
-// One pass of four pages per wavefront: many small workgroups keep several
-// wavefronts per SIMD busy, which hides the dependent add chains of the tree
-// (two passes per workgroup measured slower).
-constexpr int kScoreIters = 1;
+// Workgroup shape: one pass of four pages per wavefront (many small passes in
+// parallel hide the dependent add chains of the tree); four wavefronts without
+// the selection epilogue, sixteen with it, so that the selection's per-thread
+// share of the head's pages is small.  (Two passes per wavefront, which lets
+// all workgroups of a 32K-token context start at once instead of a few waiting
+// for a free compute unit, measured 0.8 us slower per step.)
+constexpr int score_threads(int per) { return per > 0 ? 1024 : 256; }
+constexpr int score_iters(int) { return 1; }
+// pages a workgroup scores (four per wavefront and pass)
+constexpr int score_pages_per_block(int per) { return score_threads(per) / 64 * 4 * score_iters(per); }
 
 struct TokenArgs {
   const void* k_new;
@@ -42,14 +50,14 @@ struct SelectArgs {
 };
 
 template <typename T, int D, int PER>
-__global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restrict__ q,
+__global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, const T* __restrict__ q,
                                                    int64_t q_bstride, T* __restrict__ dg,
                                                    const int32_t* __restrict__ seq_lens,
                                                    float* __restrict__ scores, TokenArgs ta,
                                                    SelectArgs sa) {
   // [G][D] fp32 queries while scoring; the top-k histograms and scratch after
   extern __shared__ __attribute__((aligned(16))) float dyn_lds[];
-  constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
+  constexpr int PPB = score_threads(PER) / 64 * ScoreShape<T, D>::PPW * score_iters(PER);
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
   const int pos = seq_lens[b];
@@ -73,7 +81,7 @@ __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restr
       warm_p = sa.tk.pt[(int64_t)b * g.max_pages + p];
     }
   }
-  score_role<T, D, kScoreIters>(g, blockIdx.x * PPB, q + b * q_bstride + (int64_t)h * g.G * D,
+  score_role<T, D, score_iters(PER)>(g, blockIdx.x * PPB, q + b * q_bstride + (int64_t)h * g.G * D,
                                 dg + bh * g.max_pages * 2 * D, n_pages, scores + bh * g.max_pages,
                                 dyn_lds, tk);
   if constexpr (PER > 0) {
@@ -102,7 +110,7 @@ __global__ void __launch_bounds__(256) score_kernel(Geometry g, const T* __restr
     if (s_last) {
       uint32_t* hist = reinterpret_cast<uint32_t*>(dyn_lds);
       int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-      topk_role<PER, 4>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
+      topk_role<PER, score_threads(PER) / 64>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
     }
   }
 }
@@ -111,13 +119,13 @@ template <typename T, int D, int PER>
 hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
                    const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
                    const SelectArgs& sa, hipStream_t s) {
-  constexpr int PPB = 4 * ScoreShape<T, D>::PPW * kScoreIters;
-  static_assert(PPB == 4 * 4 * kScoreIters, "pages per workgroup as the selection counters assume");
+  constexpr int PPB = score_threads(PER) / 64 * ScoreShape<T, D>::PPW * score_iters(PER);
+  static_assert(PPB == score_pages_per_block(PER), "pages per workgroup as the selection counters assume");
   dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
   size_t lds = sizeof(float) * g.G * D;
   if (PER > 0) lds = std::max(lds, sizeof(int32_t) * (kTopkHistWords + kTopkSmall));
   const TokenArgs ta{k_new, v_new, c.k_cache, c.v_cache, c.page_table};
-  score_kernel<T, D, PER><<<grid, 256, lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens,
+  score_kernel<T, D, PER><<<grid, score_threads(PER), lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens,
                                                  scores, ta, sa);
   return hipGetLastError();
 }
@@ -127,14 +135,16 @@ hipError_t score_d(const Geometry& g, int step, const void* q, int64_t qbs,
                    const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
                    const SelectArgs& sa, hipStream_t s) {
   if (!sa.count) return score_t<T, D, 0>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
-  if (g.max_pages <= 256 * 4) return score_t<T, D, 4>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
-  if (g.max_pages <= 256 * 12) return score_t<T, D, 12>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
-  return score_t<T, D, 24>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  constexpr int TH = score_threads(1);
+  if (g.max_pages <= TH * 1) return score_t<T, D, 1>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  if (g.max_pages <= TH * 2) return score_t<T, D, 2>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  if (g.max_pages <= TH * 3) return score_t<T, D, 3>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
+  return score_t<T, D, 6>(g, step, q, qbs, c, k_new, v_new, scores, sa, s);
 }
 
 }  // namespace
 
-bool score_selects(const Geometry& g) { return g.max_pages <= 256 * 24; }
+bool score_selects(const Geometry& g) { return g.max_pages <= score_threads(1) * 6; }
 
 hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t q_batch_stride,
                         const retro_kv_cache& c, const void* k_new, const void* v_new,
@@ -145,7 +155,7 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
     sa.tk = TopkArgs{g, step, scores, c.page_table, c.last_loaded, sel->selected, sel->mask,
                      sel->num_selected, sel_phys};
     sa.count = counters;
-    constexpr int PPB = 4 * 4 * kScoreIters;  // pages per workgroup (four pages per wavefront pass)
+    const int PPB = score_pages_per_block(1);
     const int blocks = (g.max_pages + PPB - 1) / PPB;  // workgroups per KV head
     sa.group = std::max(16, (blocks + kSelMaxGroups - 1) / kSelMaxGroups);
   }

@@ -8,10 +8,10 @@
 // 2. Radix select over rel = key - min_key with 11-bit digits taken from the
 //    top of rel's actual bit length.  Each pass histograms the digit of the
 //    keys still in the running into a histogram of its own (so none is cleared
-//    between passes), and after one barrier every wavefront scans it by itself:
-//    a prefix sum over its lanes' bin totals locates T, the k-th largest key,
-//    and `need` becomes the number of keys to take from T's bin.  The search
-//    stops as soon as that bin is taken whole or all bits are fixed.
+//    between passes); one wavefront scans it (a prefix sum over its lanes' bin
+//    totals locates T, the k-th largest key) and publishes T's digit through
+//    LDS, and `need` becomes the number of keys to take from T's bin.  The
+//    search stops as soon as that bin is taken whole or all bits are fixed.
 // 3. Compaction in page order: a page is kept if its rel is above T's prefix,
 //    or ties with it and is among the first `need` such pages (ties go to the
 //    lower page index).  Ballots count kept pages below a lane within its
@@ -52,12 +52,12 @@ hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
   TopkArgs ta{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
               sel.num_selected, sel_phys};
   const unsigned grid = (unsigned)(g.batch * g.hk);
-  if (g.max_pages <= 256 * 4)
-    topk_mask_kernel<256, 4><<<grid, 256, 0, s>>>(ta, c.seq_lens);
-  else if (g.max_pages <= 256 * 12)
-    topk_mask_kernel<256, 12><<<grid, 256, 0, s>>>(ta, c.seq_lens);
-  else if (g.max_pages <= 256 * 24)
-    topk_mask_kernel<256, 24><<<grid, 256, 0, s>>>(ta, c.seq_lens);
+  // one workgroup per head: its time is one wavefront's instruction count,
+  // so sixteen wavefronts share the pages
+  if (g.max_pages <= 1024 * 3)
+    topk_mask_kernel<1024, 3><<<grid, 1024, 0, s>>>(ta, c.seq_lens);
+  else if (g.max_pages <= 1024 * 6)
+    topk_mask_kernel<1024, 6><<<grid, 1024, 0, s>>>(ta, c.seq_lens);
   else
     topk_mask_kernel<1024, 16><<<grid, 1024, 0, s>>>(ta, c.seq_lens);
   return hipGetLastError();
