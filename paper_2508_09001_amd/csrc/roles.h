@@ -259,8 +259,10 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b
 // [c*VEC, (c+1)*VEC): the first log2(VEC) levels of the pairwise tree are
 // in-lane, the last four pair lane c with c+1, c+2, c+4, c+8 through DPP (the
 // left operand is always the lower index).  tok.lp < 0: no token to append.
+// The workgroup scores pages [page0, page_end) (at most ITERS passes of four
+// pages per wavefront; pass it covers the workgroup's pages it*nw*4 onwards).
 template <typename T, int D, int ITERS>
-__device__ __forceinline__ void score_role(const Geometry& g, int page0, const T* q,
+__device__ __forceinline__ void score_role(const Geometry& g, int page0, int page_end, const T* q,
                                            T* drow, int n_pages, float* srow, float* sq,
                                            const StepToken<T> tok) {
 #pragma clang fp contract(off)
@@ -273,8 +275,8 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
   uint32_t raw[ITERS][2][S::WORDS];
 #pragma unroll
   for (int it = 0; it < ITERS; ++it) {
-    const int page = page0 + (wave * ITERS + it) * S::PPW + lane / S::LPP;
-    if (page < g.max_pages) {
+    const int page = page0 + (it * nw + wave) * S::PPW + lane / S::LPP;
+    if (page < page_end) {
       const T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
       load_words<S::WORDS>(row, raw[it][0]);
       load_words<S::WORDS>(row + D, raw[it][1]);
@@ -292,7 +294,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
     const int e = (tid + r * blockDim.x) * QV;
     if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
-  const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page0 + nw * S::PPW * ITERS;
+  const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page_end;
   // the token's key and value, element tid, for the append at the end: read
   // now so that the append does not wait for a round trip of its own (every
   // workgroup running this role has at least 256 threads)
@@ -324,7 +326,9 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
 
 #pragma unroll
   for (int it = 0; it < ITERS; ++it) {
-    const int page = page0 + (wave * ITERS + it) * S::PPW + lane / S::LPP;
+    const int wpage0 = page0 + (it * nw + wave) * S::PPW;
+    if (it > 0 && wpage0 >= page_end) break;  // uniform: no page of this pass
+    const int page = wpage0 + lane / S::LPP;
     float lo[S::VEC], hi[S::VEC];
     words_to_f32<T, S::WORDS>(raw[it][0], lo);
     words_to_f32<T, S::WORDS>(raw[it][1], hi);
@@ -369,7 +373,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, const T
     }
     // device-coherent store: a later reader of the same launch (the selection)
     // may run on another XCD
-    if (page < n_pages && c == 0)
+    if (page < n_pages && page < page_end && c == 0)
       __hip_atomic_store(srow + page, Ssum + 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (has_tok && tid < D) {

@@ -21,16 +21,43 @@
 namespace retro {
 namespace {
 
-// Workgroup shape: one pass of four pages per wavefront (many small passes in
-// parallel hide the dependent add chains of the tree); four wavefronts without
-// the selection epilogue, sixteen with it, so that the selection's per-thread
-// share of the head's pages is small.  (Two passes per wavefront, which lets
-// all workgroups of a 32K-token context start at once instead of a few waiting
-// for a free compute unit, measured 0.8 us slower per step.)
+// Workgroup shape.  Four pages per wavefront and pass.  Without the selection
+// epilogue: four wavefronts, one pass (many small workgroups hide the dependent
+// add chains of the tree).  With it: sixteen wavefronts, so that the
+// selection's per-thread share of the head's pages is small, and up to two
+// passes: a KV head's pages are spread over as many workgroups as fit on the
+// chip at once (one sixteen-wavefront workgroup per compute unit), since a
+// workgroup that waits for a free unit starts about 1.3 us after one ends and
+// holds up its head's selection; a wavefront with no page in the second pass
+// skips it.
 constexpr int score_threads(int per) { return per > 0 ? 1024 : 256; }
-constexpr int score_iters(int) { return 1; }
-// pages a workgroup scores (four per wavefront and pass)
+constexpr int score_iters(int per) { return per > 0 ? 2 : 1; }
+// most pages a workgroup scores
 constexpr int score_pages_per_block(int per) { return score_threads(per) / 64 * 4 * score_iters(per); }
+
+int compute_units() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+// Workgroups per KV head and pages per workgroup of the selecting launch.
+void select_split(const Geometry& g, int* nbh, int* ppb) {
+  const int one_pass = score_threads(1) / 64 * 4;
+  const int fit = std::max(1, compute_units() / std::max(1, g.hk * g.batch));
+  int n = (g.max_pages + one_pass - 1) / one_pass;
+  if (n > fit) n = std::max(fit, (g.max_pages + score_pages_per_block(1) - 1) / score_pages_per_block(1));
+  const int per = (g.max_pages + n - 1) / n;
+  *ppb = per;
+  *nbh = (g.max_pages + per - 1) / per;
+}
 
 struct TokenArgs {
   const void* k_new;
@@ -47,6 +74,7 @@ struct SelectArgs {
   // zero between launches
   int32_t* count;
   int group;
+  int nbh, ppb;  // workgroups per KV head, pages per workgroup (at most score_pages_per_block)
 };
 
 template <typename T, int D, int PER>
@@ -54,10 +82,11 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
                                                    int64_t q_bstride, T* __restrict__ dg,
                                                    const int32_t* __restrict__ seq_lens,
                                                    float* __restrict__ scores, TokenArgs ta,
-                                                   SelectArgs sa) {
+                                                   SelectArgs sa, int ppb) {
   // [G][D] fp32 queries while scoring; the top-k histograms and scratch after
   extern __shared__ __attribute__((aligned(16))) float dyn_lds[];
-  constexpr int PPB = score_threads(PER) / 64 * ScoreShape<T, D>::PPW * score_iters(PER);
+  static_assert(ScoreShape<T, D>::PPW == 4, "four pages per wavefront and pass");
+  const int page0 = blockIdx.x * ppb, page_end = min(page0 + ppb, g.max_pages);
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
   const int pos = seq_lens[b];
@@ -75,13 +104,13 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
   if constexpr (PER > 0) {
     // Fetch this workgroup's last_loaded and page-table entries along with its
     // digests, so that the selection finds them in the caches.
-    const int p = blockIdx.x * PPB + (threadIdx.x & (PPB - 1));
-    if (threadIdx.x < PPB && p < g.max_pages) {
+    const int p = page0 + (int)threadIdx.x;
+    if (p < page_end) {
       warm_a = sa.tk.A[bh * g.max_pages + p];
       warm_p = sa.tk.pt[(int64_t)b * g.max_pages + p];
     }
   }
-  score_role<T, D, score_iters(PER)>(g, blockIdx.x * PPB, q + b * q_bstride + (int64_t)h * g.G * D,
+  score_role<T, D, score_iters(PER)>(g, page0, page_end, q + b * q_bstride + (int64_t)h * g.G * D,
                                 dg + bh * g.max_pages * 2 * D, n_pages, scores + bh * g.max_pages,
                                 dyn_lds, tk);
   if constexpr (PER > 0) {
@@ -119,14 +148,13 @@ template <typename T, int D, int PER>
 hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
                    const retro_kv_cache& c, const void* k_new, const void* v_new, float* scores,
                    const SelectArgs& sa, hipStream_t s) {
-  constexpr int PPB = score_threads(PER) / 64 * ScoreShape<T, D>::PPW * score_iters(PER);
-  static_assert(PPB == score_pages_per_block(PER), "pages per workgroup as the selection counters assume");
-  dim3 grid((g.max_pages + PPB - 1) / PPB, g.hk, g.batch);
+  if (sa.ppb < 1 || sa.ppb > score_pages_per_block(PER) || sa.nbh < 1) return hipErrorInvalidValue;
+  dim3 grid(sa.nbh, g.hk, g.batch);
   size_t lds = sizeof(float) * g.G * D;
   if (PER > 0) lds = std::max(lds, sizeof(int32_t) * (kTopkHistWords + kTopkSmall));
   const TokenArgs ta{k_new, v_new, c.k_cache, c.v_cache, c.page_table};
   score_kernel<T, D, PER><<<grid, score_threads(PER), lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens,
-                                                 scores, ta, sa);
+                                                 scores, ta, sa, sa.ppb);
   return hipGetLastError();
 }
 
@@ -155,9 +183,11 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
     sa.tk = TopkArgs{g, step, scores, c.page_table, c.last_loaded, sel->selected, sel->mask,
                      sel->num_selected, sel_phys};
     sa.count = counters;
-    const int PPB = score_pages_per_block(1);
-    const int blocks = (g.max_pages + PPB - 1) / PPB;  // workgroups per KV head
-    sa.group = std::max(16, (blocks + kSelMaxGroups - 1) / kSelMaxGroups);
+    select_split(g, &sa.nbh, &sa.ppb);
+    sa.group = std::max(16, (sa.nbh + kSelMaxGroups - 1) / kSelMaxGroups);
+  } else {
+    sa.ppb = score_pages_per_block(0);
+    sa.nbh = (g.max_pages + sa.ppb - 1) / sa.ppb;
   }
   if (g.dtype == RETRO_BF16)
     return g.D == 128 ? score_d<bf16_t, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s)

@@ -127,7 +127,7 @@ step_kernel(StepArgs a) {
           tk = make_step_token<T>(g, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc);
         const int ppb = kFusedWaves * ScoreShape<T, D>::PPW * kFusedScoreIters;
         score_role<T, D, kFusedScoreIters>(
-            g, sub * ppb,
+            g, sub * ppb, min(sub * ppb + ppb, g.max_pages),
             reinterpret_cast<const T*>(a.q_cur) + b * a.q_bstride + (int64_t)h * g.G * D,
             reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D, n_pages,
             a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
