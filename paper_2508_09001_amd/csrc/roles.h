@@ -355,10 +355,13 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
       float t[S::VEC];
 #pragma unroll
       for (int v = 0; v < S::VEC; ++v) {
+        // max(q*lo, q*hi) is the product with hi for q >= 0 and with lo for
+        // q < 0 (lo <= hi, and rounding is monotone): one product instead of
+        // two.  Only a zero term's sign can differ (q < 0, lo = -0, hi = +0),
+        // which changes no sum with a nonzero term and is cleared by the
+        // final + 0.0f otherwise, so the score is the same bit for bit.
         const float qv = sq[gq * D + c * S::VEC + v];
-        const float a0 = qv * lo[v];
-        const float a1 = qv * hi[v];
-        t[v] = a0 > a1 ? a0 : a1;
+        t[v] = qv * (qv >= 0.f ? hi[v] : lo[v]);
       }
 #pragma unroll
       for (int w = 1; w < S::VEC; w *= 2)

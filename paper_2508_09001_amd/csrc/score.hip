@@ -119,7 +119,8 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
     __builtin_amdgcn_s_waitcnt(0);  // this wavefront's score stores have completed
     __syncthreads();
     // Count out in two levels (a group of workgroups, then the head), so that
-    // no counter takes more than max(group, number of groups) updates.
+    // no counter takes more than max(group, number of groups) updates; with a
+    // single group its counter is the head's.
     if (threadIdx.x == 0) {
       const int ngroups = (gridDim.x + sa.group - 1) / sa.group;
       int32_t* head = sa.count + bh * (int64_t)kSelCounterInts * (1 + kSelMaxGroups);
@@ -129,9 +130,10 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
       bool last = false;
       if (__hip_atomic_fetch_add(gc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == in_grp - 1) {
         __hip_atomic_store(gc, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        last = __hip_atomic_fetch_add(head, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-               ngroups - 1;
-        if (last) __hip_atomic_store(head, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = ngroups == 1 ||
+               __hip_atomic_fetch_add(head, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                   ngroups - 1;
+        if (last && ngroups > 1) __hip_atomic_store(head, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       s_last = last;
     }
@@ -184,7 +186,8 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
                      sel->num_selected, sel_phys};
     sa.count = counters;
     select_split(g, &sa.nbh, &sa.ppb);
-    sa.group = std::max(16, (sa.nbh + kSelMaxGroups - 1) / kSelMaxGroups);
+    // one counter per head up to 32 workgroups, else groups of at least 16
+    sa.group = sa.nbh <= 32 ? sa.nbh : std::max(16, (sa.nbh + kSelMaxGroups - 1) / kSelMaxGroups);
   } else {
     sa.ppb = score_pages_per_block(0);
     sa.nbh = (g.max_pages + sa.ppb - 1) / sa.ppb;
