@@ -87,3 +87,17 @@ def test_fp32_head_dim_128_many_rows():
     spec = W.Spec("edge-f32-d128", batch=1, num_kv_heads=2, group=8, head_dim=128, page_size=16,
                   budget=512, window=20, steps=24, dtype="f32", prefill=(3000,), seed=12)
     run_parity(spec, 24, label="edge f32 d128 R=168")
+
+
+def test_six_row_tiles_bf16_d64():
+    # R = 23 * 4 = 92 rows: six 16-row tiles, more than the four SIMDs of a CU
+    spec = W.Spec("edge-6tiles", batch=2, num_kv_heads=2, group=4, head_dim=64, page_size=16,
+                  budget=640, window=22, steps=28, dtype="bf16", prefill=(2100, 1337), seed=13)
+    run_parity(spec, 28, page_perm_seed=4, label="edge 6 row tiles bf16 d64")
+
+
+def test_five_row_tiles_fp32():
+    # R = 35 * 2 = 70 rows: five tiles, fp32 inputs
+    spec = W.Spec("edge-5tiles-f32", batch=1, num_kv_heads=2, group=2, head_dim=128, page_size=16,
+                  budget=384, window=34, steps=40, dtype="f32", prefill=(1500,), seed=14)
+    run_parity(spec, 40, label="edge 5 row tiles f32")
