@@ -89,7 +89,7 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.ws_lpart = off;
   off += align256(bhs * x.n_splits * x.R * sizeof(float));
   x.ws_ctl = off;
-  off += align256((kCtlCounts + 3 * bhs) * sizeof(int32_t));
+  off += align256((kCtlCounts + 3 * bhs * kCtlStride) * sizeof(int32_t));
   x.ws_sel = off;  // per-head counters of the score + selection launch
   off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
   x.ws_total = off;

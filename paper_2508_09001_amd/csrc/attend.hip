@@ -53,7 +53,7 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
   const int rg = u % g.n_rgroups;
   u /= g.n_rgroups;
   const int h = u % g.hk, b = u / g.hk;
-  attend_role<T, D, RTW, kMaxPieces, RTW == 1>(a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); },
+  attend_role<T, D, RTW, kMaxPieces, RTW == 1, false>(a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); },
                          lds, s_phys, s_page, s_mask, [] {});
 }
 

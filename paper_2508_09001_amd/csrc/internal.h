@@ -68,7 +68,9 @@ struct Geometry {
 // Synchronisation words of the fused step in the workspace (int32 offsets):
 // 8 lane ticket counters kCtlStride apart, the exit counter, a sticky error
 // word (a bounded wait ran out), then per-head counters of the score, top-k and
-// attention roles.  All zero between launches.
+// attention roles, each in a 128-byte line of its own (kCtlStride apart) so
+// that the polls of different heads do not meet on one line.  All zero
+// between launches.
 constexpr int kCtlTicket = 0;
 constexpr int kCtlStride = 32;
 constexpr int kCtlExit = 256;

@@ -20,6 +20,27 @@ constexpr int kMaxSplitPages = 64;  // selected pages per attention split
 // roles run inside the fused kernel's task loop, and values computed from the
 // index alone would otherwise be hoisted out of it and kept live (in registers
 // every role then lacks) across all roles.
+// Device-coherent accesses (sc1: written through / read past the per-XCD L2s)
+// for data handed between workgroups of one launch without fences.  Vector
+// forms go through a buffer resource over [base, base + 2 GiB) (byte offsets;
+// the host keeps such buffers below that size).
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+constexpr int kCpolSc1 = 16;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+}
+template <bool COH, typename V>
+__device__ __forceinline__ void put_c(V* p, V v) {
+  if constexpr (COH) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else *p = v;
+}
+template <bool COH, typename V>
+__device__ __forceinline__ V get_c(const V* p) {
+  if constexpr (COH) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else return *p;
+}
+
 __device__ __forceinline__ int thread_index() {
   int t = threadIdx.x;
   asm volatile("" : "+v"(t));
@@ -261,7 +282,9 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b
 // left operand is always the lower index).  tok.lp < 0: no token to append.
 // The workgroup scores pages [page0, page_end) (at most ITERS passes of four
 // pages per wavefront; pass it covers the workgroup's pages it*nw*4 onwards).
-template <typename T, int D, int ITERS>
+// COH: the token's key and value are read by other workgroups of the same
+// launch, so they are stored device-coherently.
+template <typename T, int D, int ITERS, bool COH = false>
 __device__ __forceinline__ void score_role(const Geometry& g, int page0, int page_end, const T* q,
                                            T* drow, int n_pages, float* srow, float* sq,
                                            const StepToken<T> tok) {
@@ -380,8 +403,14 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
       __hip_atomic_store(srow + page, Ssum + 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (has_tok && tid < D) {
-    tok.k_row[tid] = tok_k;
-    tok.v_col[(int64_t)tid * g.P] = tok_v;
+    if constexpr (COH) {
+      using U = typename std::conditional<sizeof(T) == 2, uint16_t, uint32_t>::type;
+      put_c<true>(reinterpret_cast<U*>(tok.k_row + tid), __builtin_bit_cast(U, tok_k));
+      put_c<true>(reinterpret_cast<U*>(tok.v_col + (int64_t)tid * g.P), __builtin_bit_cast(U, tok_v));
+    } else {
+      tok.k_row[tid] = tok_k;
+      tok.v_col[(int64_t)tid * g.P] = tok_v;
+    }
   }
 }
 
@@ -422,7 +451,9 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 // ints of LDS.
 // `wait()` is called after the page-table and last_loaded loads are issued and
 // before the scores are read.
-template <int PER, int MAXW, typename PagesOf, typename Wait>
+// COH: the selection is read by other workgroups of the same launch, so it is
+// stored device-coherently.
+template <int PER, int MAXW, bool COH, typename PagesOf, typename Wait>
 __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
                                           uint32_t* hist, int* small, Wait&& wait) {
   constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
@@ -615,20 +646,20 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
     if (is_eq && eb < (int)need) pos = gb + eb;
     const int p = j * THREADS + tid;
     if (pos >= 0 && pos < k) {  // always true for a kept page; guards the writes
-      sel_row[pos] = p;
-      m_row[pos] = a_old[j];
+      put_c<COH>(sel_row + pos, p);
+      put_c<COH>(m_row + pos, a_old[j]);
       a_row[p] = step;
-      if (ph_row) ph_row[pos] = (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1;
+      if (ph_row) put_c<COH>(ph_row + pos, (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1);
     } else if (p == tok_lp) {
       a_row[p] = step - 1;  // the token's page, not kept
     }
   }
   for (int i = k + tid; i < g.k_max; i += THREADS) {
-    sel_row[i] = -1;
-    m_row[i] = -1;
-    if (ph_row) ph_row[i] = -1;
+    put_c<COH>(sel_row + i, -1);
+    put_c<COH>(m_row + i, -1);
+    if (ph_row) put_c<COH>(ph_row + i, -1);
   }
-  if (tid == 0) ta.num_selected[bh] = k;
+  if (tid == 0) put_c<COH>(ta.num_selected + bh, k);
 }
 
 
@@ -676,7 +707,9 @@ struct AttendArgs {
 // of a chunk per thread (ceil(Tiles::PIECES / threads)); PAIR computes chunks
 // two at a time (more registers).  `seq_len_of()` gives the
 // sequence length in effect; it is called once the page-list loads are issued.
-template <typename T, int D, int RTW, int MAXP, bool PAIR, typename SeqLen, typename Wait>
+// COH: the selection comes from, and the partials go to, other workgroups of
+// the same launch: device-coherent loads and stores.
+template <typename T, int D, int RTW, int MAXP, bool PAIR, bool COH, typename SeqLen, typename Wait>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
                                             SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
                                             int* s_mask, Wait&& wait) {
@@ -743,11 +776,11 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   int lp = -1, m = 0, phys = -1;
   if (tid < g.pages_per_split && first + tid < g.k_max) {
     const int64_t o = (int64_t)bh * g.k_max + first + tid;
-    lp = a.sel[o];
-    m = a.msk[o];
-    if (a.sel_phys) phys = a.sel_phys[o];
+    lp = get_c<COH>(a.sel + o);
+    m = get_c<COH>(a.msk + o);
+    if (a.sel_phys) phys = get_c<COH>(a.sel_phys + o);
   }
-  const int k_eff = a.nsel[bh];
+  const int k_eff = get_c<COH>(a.nsel + bh);
   const int seq_len = seq_len_of();
   const int np = min(g.pages_per_split, k_eff - first);
   if (np <= 0) return;  // uniform: nothing selected in this split
@@ -1058,15 +1091,23 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     if (rho < g.R) {
       const float inv = l > 0.f ? 1.f / l : 0.f;
       float* orow = a.o_ws + (part + rho) * D;
+      const float lse = l > 0.f ? (m_run[j] + __log2f(l)) * kLn2 : -INFINITY;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
         const f32x4 o = acc[j][dt] * inv;
-        // streamed out: read once by the combine, not worth keeping in L2
-        __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4));
+        if constexpr (COH) {
+          const uint32_t off = (uint32_t)(((part + rho) * D + dt * 16 + 4 * g4) * sizeof(float));
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4v, o),
+                                                 coherent_rsrc(a.o_ws), off, 0, kCpolSc1);
+        } else {
+          // streamed out: read once by the combine, not worth keeping in L2
+          __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4));
+        }
       }
-      if (g4 == 0)
-        __builtin_nontemporal_store(l > 0.f ? (m_run[j] + __log2f(l)) * kLn2 : -INFINITY,
-                                    a.l_ws + part + rho);
+      if (g4 == 0) {
+        if constexpr (COH) put_c<true>(a.l_ws + part + rho, lse);
+        else __builtin_nontemporal_store(lse, a.l_ws + part + rho);
+      }
     }
   }
 }
@@ -1106,14 +1147,17 @@ struct Row {
 // group (log-normalisers one per lane, output rows E floats per lane) in
 // flight together; groups after the first are folded in relative to the
 // running maximum.
-template <int D, int NR, int GS>
+// COH: the partials and the selection count come from other workgroups of the
+// same launch: device-coherent loads.
+template <int D, int NR, int GS, bool COH>
 __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const int (&rho)[NR],
                                                Row<D> (&res)[NR]) {
   constexpr int E = Row<D>::E;
   const Geometry& g = a.g;
   const int lane = thread_index() & 63;
   const int e0 = lane * E;
-  const int nvs = min((a.nsel[bh] + g.pages_per_split - 1) / g.pages_per_split, g.n_splits);
+  const int nvs = min((get_c<COH>(a.nsel + bh) + g.pages_per_split - 1) / g.pages_per_split,
+                      g.n_splits);
   float m[NR], wl[NR], acc[NR][E];
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
@@ -1128,12 +1172,19 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
       const int64_t base = (int64_t)bh * g.n_splits * g.R + rho[r];
-      z[r] = lane < cnt ? a.l_ws[base + (int64_t)(s0 + lane) * g.R] : -INFINITY;
+      z[r] = lane < cnt ? get_c<COH>(a.l_ws + base + (int64_t)(s0 + lane) * g.R) : -INFINITY;
 #pragma unroll
       for (int j = 0; j < GS; ++j) {
         const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
+        if constexpr (COH && E == 2) {
+          const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(
+              coherent_rsrc(a.o_ws), (uint32_t)((row * D + e0) * sizeof(float)), 0, kCpolSc1);
+          v[r][j][0] = __uint_as_float(w[0]);
+          v[r][j][1] = __uint_as_float(w[1]);
+        } else {
 #pragma unroll
-        for (int e = 0; e < E; ++e) v[r][j][e] = a.o_ws[row * D + e0 + e];
+          for (int e = 0; e < E; ++e) v[r][j][e] = get_c<COH>(a.o_ws + row * D + e0 + e);
+        }
       }
     }
 #pragma unroll
@@ -1209,7 +1260,7 @@ __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
 
 // The partial (O, Z) of window rows r[] of query head gq of (b, h): from the
 // split partials, or (mode 1) from the caller's o_part / lse_part.
-template <int D, int NR, int GS>
+template <int D, int NR, int GS, bool COH>
 __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int gq, const int (&r)[NR],
                                          Row<D> (&res)[NR]) {
   const Geometry& g = a.g;
@@ -1222,14 +1273,14 @@ __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int g
   int rho[NR];
 #pragma unroll
   for (int i = 0; i < NR; ++i) rho[i] = r[i] * g.G + gq;
-  combine_splits<D, NR, GS>(a, b * g.hk + h, rho, res);
+  combine_splits<D, NR, GS, COH>(a, b * g.hk + h, rho, res);
 }
 
 // One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
 // executed by one wavefront; no barriers inside.  The unit of row 0 also
 // handles the current row W, whose cache slot is the one row 0 leaves.  GS:
 // splits whose loads are in flight together (at most 64).
-template <int D, int GS>
+template <int D, int GS, bool COH = false>
 __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   const Geometry& g = a.g;
   const int W = g.W;
@@ -1244,7 +1295,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
 
   if (a.mode == 0 || x == W) {  // plain combine of row x (W == 0: the current row only)
     Row<D> p[1];
-    partials<D, 1, GS>(a, b, h, gq, {x}, p);
+    partials<D, 1, GS, COH>(a, b, h, gq, {x}, p);
     if (a.mode == 0)
       put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, p[0]);
     else
@@ -1265,7 +1316,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
     const int64_t ci = ((int64_t)b * W + tau0 % W) * g.hq + qh;
     const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
     Row<D> p[1];
-    partials<D, 1, GS>(a, b, h, gq, {x}, p);
+    partials<D, 1, GS, COH>(a, b, h, gq, {x}, p);
     const Row<D> merged = lse_merge<D>(cached, p[0]);
     put<D>(a.o_cache, a.l_cache, ci, merged);
     put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, merged);
@@ -1277,7 +1328,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   Row<D> cached = zero;
   if (tau0 >= 0) cached = get<D>(a.o_cache, a.l_cache, slot);
   Row<D> p[2];
-  partials<D, 2, GS>(a, b, h, gq, {0, W}, p);
+  partials<D, 2, GS, COH>(a, b, h, gq, {0, W}, p);
   const Row<D> merged = tau0 >= 0 ? lse_merge<D>(cached, p[0]) : zero;
   put<D>(a.o_out, a.l_out, out_row * g.hq + qh, merged);
   put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, p[1]);
@@ -1288,17 +1339,18 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
 }
 
 // ============================================================================
-// Cross-workgroup hand-off for the fused step.
+// Cross-workgroup hand-off for the fused step, without fences.  Everything a
+// consumer reads from its producers is written and read device-coherently (sc1
+// accesses, which go through / past the per-XCD L2s; the roles' COH forms).
 // Producer: every wavefront waits until its own stores have completed (a bare
 // barrier does not wait for them), the workgroup meets at a barrier, and one
-// thread adds 1 to the counter with release semantics (which writes the L2 back
-// once).  Consumer: thread 0 polls the counter with relaxed device-coherent
-// loads (an acquire on every poll would invalidate the caches each time), then
-// issues one acquire fence and releases the workgroup through a barrier.
-// Polling is bounded: past the limit the error word is set and the consumer
-// goes on, so no wait can hang.
+// thread adds 1 to the counter (relaxed, device scope).  Consumer: thread 0
+// polls the counter with relaxed device-coherent loads, then releases the
+// workgroup through a barrier.  (Release / acquire fences here write back or
+// invalidate a whole L2 each time.)  Polling is bounded: past the limit the
+// error word is set and the consumer goes on, so no wait can hang.
 // ============================================================================
-constexpr int kSpinLimit = 1 << 20;  // polls of about 0.5 us each
+constexpr int kSpinLimit = 1 << 18;  // polls of about 0.5 us each
 
 __device__ __forceinline__ void block_wait(const int32_t* ctr, int target, int32_t* err) {
   if (threadIdx.x == 0) {
@@ -1308,10 +1360,8 @@ __device__ __forceinline__ void block_wait(const int32_t* ctr, int target, int32
         __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
-      __builtin_amdgcn_s_sleep(1);
+      __builtin_amdgcn_s_sleep(8);  // ~0.2 us between polls: less traffic on the counter's line
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    __builtin_amdgcn_s_waitcnt(0);
   }
   __syncthreads();
 }
@@ -1319,7 +1369,7 @@ __device__ __forceinline__ void block_wait(const int32_t* ctr, int target, int32
 __device__ __forceinline__ void block_signal(int32_t* ctr) {
   __builtin_amdgcn_s_waitcnt(0);  // this wavefront's stores have completed
   __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace retro

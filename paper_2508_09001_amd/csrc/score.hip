@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
     if (s_last) {
       uint32_t* hist = reinterpret_cast<uint32_t*>(dyn_lds);
       int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-      topk_role<PER, score_threads(PER) / 64>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
+      topk_role<PER, score_threads(PER) / 64, false>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
     }
   }
 }

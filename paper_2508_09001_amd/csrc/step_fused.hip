@@ -71,7 +71,8 @@ struct FusedLds {
 
 constexpr int kThreads = 64 * kFusedWaves;
 
-template <typename T, int D>
+// PER: stripes of the head's pages per thread in the top-k role (max_pages <= PER * kThreads)
+template <typename T, int D, int PER>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 8)))
 step_kernel(StepArgs a) {
   // chunk pieces per thread of the attention role
@@ -86,9 +87,10 @@ step_kernel(StepArgs a) {
   const Geometry& g = a.g;
   const int tid = threadIdx.x;
   const int BH = g.batch * g.hk;
+  // per-head counters, kCtlStride ints apart: cntX + kCtlStride * bh
   int32_t* cntA = a.ctl + kCtlCounts;
-  int32_t* cntB = cntA + BH;
-  int32_t* cntC = cntB + BH;
+  int32_t* cntB = cntA + BH * kCtlStride;
+  int32_t* cntC = cntB + BH * kCtlStride;
   int32_t* err = a.ctl + kCtlError;
 
   const int lane = blockIdx.x % kMaxLanes;
@@ -126,56 +128,59 @@ step_kernel(StepArgs a) {
         if (tok_ok)
           tk = make_step_token<T>(g, b, h, pos, phys_tok, a.k_new, a.v_new, a.kc, a.vc);
         const int ppb = kFusedWaves * ScoreShape<T, D>::PPW * kFusedScoreIters;
-        score_role<T, D, kFusedScoreIters>(
+        score_role<T, D, kFusedScoreIters, true>(
             g, sub * ppb, min(sub * ppb + ppb, g.max_pages),
             reinterpret_cast<const T*>(a.q_cur) + b * a.q_bstride + (int64_t)h * g.G * D,
             reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D, n_pages,
             a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
-        block_signal(cntA + bh);
+        block_signal(cntA + kCtlStride * bh);
       } else if (role == 1) {
-        topk_role<kTopkPer, kFusedWaves>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
+        topk_role<PER, kFusedWaves, true>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
                                   reinterpret_cast<uint32_t*>(lds), small,
-                                  [&] { block_wait(cntA + bh, g.fA, err); });
-        block_signal(cntB + bh);
+                                  [&] { block_wait(cntA + kCtlStride * bh, g.fA, err); });
+        block_signal(cntB + kCtlStride * bh);
       } else if (role == 2) {
         const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
-        attend_role<T, D, 1, MAXP, false>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
-                               s_page, s_mask, [&] { block_wait(cntB + bh, 1, err); });
-        block_signal(cntC + bh);
+        attend_role<T, D, 1, MAXP, false, true>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
+                               s_page, s_mask, [&] { block_wait(cntB + kCtlStride * bh, 1, err); });
+        block_signal(cntC + kCtlStride * bh);
       } else {
-        block_wait(cntC + bh, g.fC, err);
+        block_wait(cntC + kCtlStride * bh, g.fC, err);
         const int per_bh = g.G * a.mg.xs;
         const int local = sub * (blockDim.x >> 6) + (tid >> 6);
-        if (local < per_bh) merge_unit<D, 8>(a.mg, bh * per_bh + local);
+        if (local < per_bh) merge_unit<D, 8, true>(a.mg, bh * per_bh + local);
       }
     }
   }
 
-  // exit: the last workgroup advances the sequence lengths and clears the
-  // synchronisation words for the next launch
+  // exit: the last workgroup advances the sequence lengths (no other
+  // workgroup reads them any more) and clears the synchronisation words for
+  // the next launch (every other workgroup is past its waits)
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (tid == 0) {
-    __threadfence();
-    const int old = __hip_atomic_fetch_add(a.ctl + kCtlExit, 1, __ATOMIC_ACQ_REL,
+    const int old = __hip_atomic_fetch_add(a.ctl + kCtlExit, 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
     s_last = (old == (int)gridDim.x - 1);
   }
   __syncthreads();
   if (s_last) {
-    __threadfence();
     for (int b = tid; b < g.batch; b += blockDim.x) {
       const int pos = a.seq_lens[b];
       if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
     }
-    for (int l = tid; l < kMaxLanes; l += blockDim.x) a.ctl[kCtlTicket + kCtlStride * l] = 0;
-    for (int e = tid; e < 3 * BH; e += blockDim.x) a.ctl[kCtlCounts + e] = 0;
-    if (tid == 0) a.ctl[kCtlExit] = 0;
+    for (int l = tid; l < kMaxLanes; l += blockDim.x) put_c<true>(a.ctl + kCtlTicket + kCtlStride * l, 0);
+    for (int e = tid; e < 3 * BH; e += blockDim.x) put_c<true>(a.ctl + kCtlCounts + kCtlStride * e, 0);
+    if (tid == 0) put_c<true>(a.ctl + kCtlExit, 0);
   }
 }
 
 template <typename T, int D>
 hipError_t step_t(const StepArgs& a, hipStream_t s) {
-  step_kernel<T, D><<<(unsigned)a.g.f_grid, kThreads, 0, s>>>(a);
+  if (a.g.max_pages <= kThreads * 6)
+    step_kernel<T, D, 6><<<(unsigned)a.g.f_grid, kThreads, 0, s>>>(a);
+  else
+    step_kernel<T, D, kTopkPer><<<(unsigned)a.g.f_grid, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -188,7 +193,10 @@ int fused_score_pages_per_block(int dtype, int D) {
 }
 
 bool fused_supported(const Geometry& g) {
-  return g.max_pages <= kTopkPer * kThreads && g.G <= 16;
+  // partial outputs are addressed with 32-bit byte offsets (device-coherent
+  // buffer accesses)
+  const double part_bytes = (double)g.batch * g.hk * g.n_splits * g.R * g.D * sizeof(float);
+  return g.max_pages <= kTopkPer * kThreads && g.G <= 16 && part_bytes < 2147483648.0;
 }
 
 hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,

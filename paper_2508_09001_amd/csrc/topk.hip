@@ -38,7 +38,7 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
     const int pos = seq_lens[b];
     if (token_phys(ta.g, ta.pt, b, pos) >= 0) tok_lp = pos / ta.g.P;
   }
-  topk_role<PER, THREADS / 64>(
+  topk_role<PER, THREADS / 64, false>(
       ta, bh,
       [&] { return min((live_seq_len(ta.g, seq_lens, ta.pt, b) + ta.g.P - 1) / ta.g.P, ta.g.max_pages); },
       tok_lp, hist, small, [] {});
