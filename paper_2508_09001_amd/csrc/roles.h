@@ -594,6 +594,38 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
       need -= above;
       prefix = (prefix << (hi - lo)) | (uint32_t)bin;
       if (inbin == need) break;  // T's whole bin is kept: its prefix suffices
+      if (lo > 0 && inbin <= 64) {
+        // T is one of its bin's few keys: list them (in the next pass's
+        // histogram, still zero) and let wavefront 0 rank them exactly (lane i
+        // holds candidate i and counts the larger and equal ones through LDS
+        // broadcast reads) instead of histogramming further digits.
+        uint32_t* cand = hist + (pass + 1) * kTopkBins;  // [0]: count, [1..]: rel values
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          const uint64_t rel = key[j] - kmin;
+          if (valid(j) && (rel >> lo) == prefix) cand[1 + atomicAdd(&cand[0], 1u)] = (uint32_t)rel;
+        }
+        __syncthreads();
+        if (wave == 0) {
+          const uint32_t v = lane < (int)inbin ? cand[1 + lane] : 0u;
+          uint32_t gt = 0u, eq = 0u;
+          for (int j2 = 0; j2 < (int)inbin; ++j2) {
+            const uint32_t w = cand[1 + j2];
+            gt += w > v ? 1u : 0u;
+            eq += w == v ? 1u : 0u;
+          }
+          const bool is_t = lane < (int)inbin && gt < need && need <= gt + eq;
+          if (lane == __builtin_ctzll(wave_ballot(is_t))) {
+            res[0] = (int)v;   // T's whole rel
+            res[1] = (int)gt;  // candidates above T
+          }
+        }
+        __syncthreads();
+        prefix = (uint32_t)res[0];
+        need -= (uint32_t)res[1];  // keys equal to T still to take
+        lo = 0;
+        break;
+      }
     }
   }
 

@@ -11,7 +11,9 @@
 //    between passes); one wavefront scans it (a prefix sum over its lanes' bin
 //    totals locates T, the k-th largest key) and publishes T's digit through
 //    LDS, and `need` becomes the number of keys to take from T's bin.  The
-//    search stops as soon as that bin is taken whole or all bits are fixed.
+//    search stops as soon as that bin is taken whole or all bits are fixed;
+//    a bin of at most 64 keys is instead listed in LDS and ranked exactly by
+//    one wavefront.
 // 3. Compaction in page order: a page is kept if its rel is above T's prefix,
 //    or ties with it and is among the first `need` such pages (ties go to the
 //    lower page index).  Ballots count kept pages below a lane within its
