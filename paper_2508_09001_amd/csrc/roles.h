@@ -815,299 +815,303 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   const int k_eff = get_c<COH>(a.nsel + bh);
   const int seq_len = seq_len_of();
   const int np = min(g.pages_per_split, k_eff - first);
-  if (np <= 0) return;  // uniform: nothing selected in this split
-  const int nchunks = (np + g.chunk_pages - 1) / g.chunk_pages;
-  // page list of the split: physical page (-1: skip), stored tokens (0 for a
-  // skipped page and past the list), mask value
-  if (tid < kMaxSplitPages) {
-    if (!a.sel_phys && tid < np && lp >= 0 && lp < g.max_pages)
-      phys = a.pt[(int64_t)b * g.max_pages + lp];
-    if (tid >= np || lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
-    s_phys[tid] = phys;
-    s_len[tid] = phys >= 0 ? max(0, min(g.P, seq_len - lp * g.P)) : 0;
-    s_mask[tid] = tid < np ? m : 0;
-  }
-
-  __syncthreads();  // page list ready
-
-  // ---- chunk staging: global -> registers -> LDS ----------------------------
-  const int pieces_per_thread = (TL::PIECES + nthreads - 1) / nthreads;
-  // Chunks whose loads are in flight ahead of the computation: two when a
-  // wavefront owns one row tile, one when it owns two (register budget).
-  constexpr int DEPTH = RTW == 1 ? 2 : 1;
-  uint4 stage[DEPTH][MAXP];
-  const T* kc = reinterpret_cast<const T*>(a.kc);
-  const T* vc = reinterpret_cast<const T*>(a.vc);
-
-  // The part of each piece's address that does not depend on the chunk: its
-  // 16-token tile (page of the chunk), its slot in the page, its element offset
-  // in the page's (h_k) block and whether it is a V^T piece.  Page blocks of K
-  // and V^T have the same size, P * d elements.
-  int pc_tile[MAXP], pc_slot[MAXP], pc_off[MAXP];
-  bool pc_v[MAXP];
-#pragma unroll
-  for (int i = 0; i < MAXP; ++i) {
-    const int e = min(tid + i * nthreads, TL::PIECES - 1);
-    int tile, slot, off;
-    const bool isv = e >= TL::K_PIECES;
-    if (!isv) {
-      const int tok = e / TL::KPR, q = e - tok * TL::KPR;
-      tile = tok >> 4;
-      slot = tok & 15;
-      off = q * TL::VEC;  // + slot * D below
-    } else {
-      const int ev = e - TL::K_PIECES;
-      tile = ev / (D * TL::VPR);
-      const int rem = ev - tile * (D * TL::VPR);
-      const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
-      slot = q * TL::TPP;
-      off = dr * g.P;  // + slot below
+  // A split with nothing selected still writes its (empty) partial: (0, -inf)
+  // for every row, so that the combine reads every split without first
+  // reading the selection count.
+  if (np > 0) {  // uniform
+    const int nchunks = (np + g.chunk_pages - 1) / g.chunk_pages;
+    // page list of the split: physical page (-1: skip), stored tokens (0 for a
+    // skipped page and past the list), mask value
+    if (tid < kMaxSplitPages) {
+      if (!a.sel_phys && tid < np && lp >= 0 && lp < g.max_pages)
+        phys = a.pt[(int64_t)b * g.max_pages + lp];
+      if (tid >= np || lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
+      s_phys[tid] = phys;
+      s_len[tid] = phys >= 0 ? max(0, min(g.P, seq_len - lp * g.P)) : 0;
+      s_mask[tid] = tid < np ? m : 0;
     }
-    if (g.chunk_pages == 1) slot += 16 * tile;  // both tiles lie in one page
-    pc_tile[i] = tile;
-    pc_slot[i] = slot;
-    pc_off[i] = isv ? off + slot : off + slot * D;
-    pc_v[i] = isv;
-  }
 
-  // Every piece is loaded without a branch around the load (a piece that holds
-  // no stored data reads a stand-in address, the cache's first 16 bytes), so
-  // the loads of a chunk are all in flight together; `keep` records how many
-  // leading elements of each piece hold stored data (4 bits per piece), and
-  // the rest is zeroed when the piece is written to LDS.
-  const int64_t blk_elems = (int64_t)g.P * D;
-  auto load_chunk = [&](int c, uint4* stage, uint32_t& keep) {
-    uint32_t kp = 0u;
-#pragma unroll
-    for (int i = 0; i < MAXP; ++i) {
-      const int pl = g.chunk_pages == 2 ? 2 * c + pc_tile[i] : c;
-      const int phys = s_phys[pl];
-      const int len = s_len[pl];
-      int n_el = pc_v[i] ? min(max(len - pc_slot[i], 0), TL::TPP) : (pc_slot[i] < len ? TL::VEC : 0);
-      if (i >= pieces_per_thread || tid + i * nthreads >= TL::PIECES) n_el = 0;
-      const T* src = kc;
-      if (n_el > 0)
-        src = (pc_v[i] ? vc : kc) + ((int64_t)phys * g.hk + h) * blk_elems + pc_off[i];
-      stage[i] = *reinterpret_cast<const uint4*>(src);
-      kp |= (uint32_t)n_el << (4 * i);
-    }
-    keep = kp;
-  };
+    __syncthreads();  // page list ready
 
-  auto store_chunk = [&](int buf, const uint4* stage, uint32_t keep) {
-    T* base = lds + buf * TL::BUF_ELEMS;
-#pragma unroll
+    // ---- chunk staging: global -> registers -> LDS ----------------------------
+    const int pieces_per_thread = (TL::PIECES + nthreads - 1) / nthreads;
+    // Chunks whose loads are in flight ahead of the computation: two when a
+    // wavefront owns one row tile, one when it owns two (register budget).
+    constexpr int DEPTH = RTW == 1 ? 2 : 1;
+    uint4 stage[DEPTH][MAXP];
+    const T* kc = reinterpret_cast<const T*>(a.kc);
+    const T* vc = reinterpret_cast<const T*>(a.vc);
+
+    // The part of each piece's address that does not depend on the chunk: its
+    // 16-token tile (page of the chunk), its slot in the page, its element offset
+    // in the page's (h_k) block and whether it is a V^T piece.  Page blocks of K
+    // and V^T have the same size, P * d elements.
+    int pc_tile[MAXP], pc_slot[MAXP], pc_off[MAXP];
+    bool pc_v[MAXP];
+  #pragma unroll
     for (int i = 0; i < MAXP; ++i) {
-      const int e = tid + i * nthreads;
-      if (i < pieces_per_thread && e < TL::PIECES) {
-        T* dst;
-        if (e < TL::K_PIECES) {
-          const int tok = e / TL::KPR, q = e - tok * TL::KPR;
-          dst = base + tok * TL::KROW + q * TL::VEC;
-        } else {
-          const int ev = e - TL::K_PIECES;
-          const int tile = ev / (D * TL::VPR);
-          const int rem = ev - tile * (D * TL::VPR);
-          const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
-          dst = base + TL::K_ELEMS + (tile * D + dr) * TL::VROW + q * TL::TPP;
-        }
-        const int n_el = (keep >> (4 * i)) & 15;
-        uint32_t w[4] = {stage[i].x, stage[i].y, stage[i].z, stage[i].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          if constexpr (sizeof(T) == 2) {
-            const uint32_t m = (2 * t < n_el ? 0x0000FFFFu : 0u) | (2 * t + 1 < n_el ? 0xFFFF0000u : 0u);
-            w[t] &= m;
-          } else {
-            w[t] = t < n_el ? w[t] : 0u;
-          }
-        }
-        *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+      const int e = min(tid + i * nthreads, TL::PIECES - 1);
+      int tile, slot, off;
+      const bool isv = e >= TL::K_PIECES;
+      if (!isv) {
+        const int tok = e / TL::KPR, q = e - tok * TL::KPR;
+        tile = tok >> 4;
+        slot = tok & 15;
+        off = q * TL::VEC;  // + slot * D below
+      } else {
+        const int ev = e - TL::K_PIECES;
+        tile = ev / (D * TL::VPR);
+        const int rem = ev - tile * (D * TL::VPR);
+        const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
+        slot = q * TL::TPP;
+        off = dr * g.P;  // + slot below
       }
-    }
-  };
-
-  // Attention over a group of NC chunks held in LDS (chunk c + i in buffer
-  // (buf0 + i) & 1; only the first nv hold data): S for all of the group's
-  // 16-token tiles, one online-softmax update over them, then O += P V per
-  // chunk.  Grouping two chunks gives each wavefront twice the independent
-  // matrix products per softmax step.
-  auto compute_group = [&](auto nc_tag, int c, int buf0, int nv) {
-    constexpr int NC = decltype(nc_tag)::value;
-    constexpr int NT = 2 * NC;  // tiles of the group
-    const T* Ks[NC];
-    const T* Vs[NC];
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      Ks[i] = lds + ((buf0 + i) & 1) * TL::BUF_ELEMS;
-      Vs[i] = Ks[i] + TL::K_ELEMS;
+      if (g.chunk_pages == 1) slot += 16 * tile;  // both tiles lie in one page
+      pc_tile[i] = tile;
+      pc_slot[i] = slot;
+      pc_off[i] = isv ? off + slot : off + slot * D;
+      pc_v[i] = isv;
     }
 
-    // page facts of the group's tiles: stored tokens from the tile's first
-    // slot (0 past the group's valid chunks), mask value
-    int tlen[NT], tmask[NT];
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt) {
-      const int cc = c + tt / 2, tile = tt & 1;
-      const int pl = g.chunk_pages == 2 ? 2 * cc + tile : cc;
-      const int so = g.chunk_pages == 2 ? 0 : 16 * tile;
-      const bool in = tt / 2 < nv;
-      tlen[tt] = in ? s_len[pl] - so : 0;
-      tmask[tt] = in ? s_mask[pl] : 0;
-    }
+    // Every piece is loaded without a branch around the load (a piece that holds
+    // no stored data reads a stand-in address, the cache's first 16 bytes), so
+    // the loads of a chunk are all in flight together; `keep` records how many
+    // leading elements of each piece hold stored data (4 bits per piece), and
+    // the rest is zeroed when the piece is written to LDS.
+    const int64_t blk_elems = (int64_t)g.P * D;
+    auto load_chunk = [&](int c, uint4* stage, uint32_t& keep) {
+      uint32_t kp = 0u;
+  #pragma unroll
+      for (int i = 0; i < MAXP; ++i) {
+        const int pl = g.chunk_pages == 2 ? 2 * c + pc_tile[i] : c;
+        const int phys = s_phys[pl];
+        const int len = s_len[pl];
+        int n_el = pc_v[i] ? min(max(len - pc_slot[i], 0), TL::TPP) : (pc_slot[i] < len ? TL::VEC : 0);
+        if (i >= pieces_per_thread || tid + i * nthreads >= TL::PIECES) n_el = 0;
+        const T* src = kc;
+        if (n_el > 0)
+          src = (pc_v[i] ? vc : kc) + ((int64_t)phys * g.hk + h) * blk_elems + pc_off[i];
+        stage[i] = *reinterpret_cast<const uint4*>(src);
+        kp |= (uint32_t)n_el << (4 * i);
+      }
+      keep = kp;
+    };
 
-#pragma unroll
-    for (int j = 0; j < RTW; ++j) {
-      const int lt = wave + j * nwaves;
-      if (lt >= g.tiles_per_group || rg * g.tiles_per_group + lt >= g.row_tiles) break;  // uniform
-
-      // ---- S^T = K . Q^T for every tile of the group
-      f32x4 s[NT];
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt) {
-        f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (tt / 2 < nv) {  // uniform
-          const T* krow = Ks[tt / 2] + ((tt & 1) * 16 + ln16) * TL::KROW;
-          if constexpr (sizeof(T) == 2) {
-#pragma unroll
-            for (int kk = 0; kk < D / 32; ++kk) {
-              const bf16x8 kv = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 8 * g4);
-              sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qop[j][kk], sacc, 0, 0, 0);
-            }
+    auto store_chunk = [&](int buf, const uint4* stage, uint32_t keep) {
+      T* base = lds + buf * TL::BUF_ELEMS;
+  #pragma unroll
+      for (int i = 0; i < MAXP; ++i) {
+        const int e = tid + i * nthreads;
+        if (i < pieces_per_thread && e < TL::PIECES) {
+          T* dst;
+          if (e < TL::K_PIECES) {
+            const int tok = e / TL::KPR, q = e - tok * TL::KPR;
+            dst = base + tok * TL::KROW + q * TL::VEC;
           } else {
-#pragma unroll
-            for (int kq = 0; kq < D / 16; ++kq) {
-              const f32x4 kv = *reinterpret_cast<const f32x4*>(krow + kq * 16 + 4 * g4);
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[e], qop[j][kq][e], sacc, 0, 0, 0);
+            const int ev = e - TL::K_PIECES;
+            const int tile = ev / (D * TL::VPR);
+            const int rem = ev - tile * (D * TL::VPR);
+            const int dr = rem / TL::VPR, q = rem - dr * TL::VPR;
+            dst = base + TL::K_ELEMS + (tile * D + dr) * TL::VROW + q * TL::TPP;
+          }
+          const int n_el = (keep >> (4 * i)) & 15;
+          uint32_t w[4] = {stage[i].x, stage[i].y, stage[i].z, stage[i].w};
+  #pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            if constexpr (sizeof(T) == 2) {
+              const uint32_t m = (2 * t < n_el ? 0x0000FFFFu : 0u) | (2 * t + 1 < n_el ? 0xFFFF0000u : 0u);
+              w[t] &= m;
+            } else {
+              w[t] = t < n_el ? w[t] : 0u;
             }
           }
-        }
-        s[tt] = sacc;
-      }
-
-      // ---- mask, scale, online softmax (this lane: row ln16 of the tile)
-      float x[NT][4];
-      float mloc = -INFINITY;
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt) {
-        const bool use = row_live[j] && tlen[tt] > 0 &&
-                         (row_r[j] == W || tmask[tt] < row_tau[j]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bool ok = use && (4 * g4 + i) < tlen[tt];
-          x[tt][i] = ok ? s[tt][i] * a.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, x[tt][i]);
+          *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
         }
       }
-      mloc = col_max4(mloc);
-      const float m_new = fmaxf(m_run[j], mloc);
-      const float mu = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run[j] - mu);
-      float p[NT][4];
-      float psum = 0.f;
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          p[tt][i] = exp2f(x[tt][i] - mu);
-          psum += p[tt][i];
-        }
-      l_run[j] = l_run[j] * alpha + psum;
-      m_run[j] = m_new;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) acc[j][dt] *= alpha;
+    };
 
-      // ---- O^T += V^T . P^T, chunk by chunk
-#pragma unroll
+    // Attention over a group of NC chunks held in LDS (chunk c + i in buffer
+    // (buf0 + i) & 1; only the first nv hold data): S for all of the group's
+    // 16-token tiles, one online-softmax update over them, then O += P V per
+    // chunk.  Grouping two chunks gives each wavefront twice the independent
+    // matrix products per softmax step.
+    auto compute_group = [&](auto nc_tag, int c, int buf0, int nv) {
+      constexpr int NC = decltype(nc_tag)::value;
+      constexpr int NT = 2 * NC;  // tiles of the group
+      const T* Ks[NC];
+      const T* Vs[NC];
+  #pragma unroll
       for (int i = 0; i < NC; ++i) {
-        if (i >= nv) break;  // uniform
-        if constexpr (sizeof(T) == 2) {
-          bf16x8 ph, pl;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float pv = p[2 * i + (e >> 2)][e & 3];
-            const __bf16 hi = (__bf16)pv;
-            ph[e] = hi;
-            pl[e] = (__bf16)(pv - (float)hi);
+        Ks[i] = lds + ((buf0 + i) & 1) * TL::BUF_ELEMS;
+        Vs[i] = Ks[i] + TL::K_ELEMS;
+      }
+
+      // page facts of the group's tiles: stored tokens from the tile's first
+      // slot (0 past the group's valid chunks), mask value
+      int tlen[NT], tmask[NT];
+  #pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const int cc = c + tt / 2, tile = tt & 1;
+        const int pl = g.chunk_pages == 2 ? 2 * cc + tile : cc;
+        const int so = g.chunk_pages == 2 ? 0 : 16 * tile;
+        const bool in = tt / 2 < nv;
+        tlen[tt] = in ? s_len[pl] - so : 0;
+        tmask[tt] = in ? s_mask[pl] : 0;
+      }
+
+  #pragma unroll
+      for (int j = 0; j < RTW; ++j) {
+        const int lt = wave + j * nwaves;
+        if (lt >= g.tiles_per_group || rg * g.tiles_per_group + lt >= g.row_tiles) break;  // uniform
+
+        // ---- S^T = K . Q^T for every tile of the group
+        f32x4 s[NT];
+  #pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (tt / 2 < nv) {  // uniform
+            const T* krow = Ks[tt / 2] + ((tt & 1) * 16 + ln16) * TL::KROW;
+            if constexpr (sizeof(T) == 2) {
+  #pragma unroll
+              for (int kk = 0; kk < D / 32; ++kk) {
+                const bf16x8 kv = *reinterpret_cast<const bf16x8*>(krow + kk * 32 + 8 * g4);
+                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qop[j][kk], sacc, 0, 0, 0);
+              }
+            } else {
+  #pragma unroll
+              for (int kq = 0; kq < D / 16; ++kq) {
+                const f32x4 kv = *reinterpret_cast<const f32x4*>(krow + kq * 16 + 4 * g4);
+  #pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  sacc = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[e], qop[j][kq][e], sacc, 0, 0, 0);
+              }
+            }
           }
-#pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt) {
-            const int dr = dt * 16 + ln16;
-            const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(Vs[i] + dr * TL::VROW + 4 * g4);
-            const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(Vs[i] + (D + dr) * TL::VROW + 4 * g4);
-            const bf16x8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-            acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, acc[j][dt], 0, 0, 0);
-            acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, acc[j][dt], 0, 0, 0);
+          s[tt] = sacc;
+        }
+
+        // ---- mask, scale, online softmax (this lane: row ln16 of the tile)
+        float x[NT][4];
+        float mloc = -INFINITY;
+  #pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          const bool use = row_live[j] && tlen[tt] > 0 &&
+                           (row_r[j] == W || tmask[tt] < row_tau[j]);
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool ok = use && (4 * g4 + i) < tlen[tt];
+            x[tt][i] = ok ? s[tt][i] * a.scale_log2 : -INFINITY;
+            mloc = fmaxf(mloc, x[tt][i]);
           }
-        } else {
-#pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt) {
-            const int dr = dt * 16 + ln16;
-#pragma unroll
-            for (int tile = 0; tile < 2; ++tile) {
-              const f32x4 vv =
-                  *reinterpret_cast<const f32x4*>(Vs[i] + (tile * D + dr) * TL::VROW + 4 * g4);
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[e], p[2 * i + tile][e],
-                                                                 acc[j][dt], 0, 0, 0);
+        }
+        mloc = col_max4(mloc);
+        const float m_new = fmaxf(m_run[j], mloc);
+        const float mu = (m_new == -INFINITY) ? 0.f : m_new;
+        const float alpha = exp2f(m_run[j] - mu);
+        float p[NT][4];
+        float psum = 0.f;
+  #pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            p[tt][i] = exp2f(x[tt][i] - mu);
+            psum += p[tt][i];
+          }
+        l_run[j] = l_run[j] * alpha + psum;
+        m_run[j] = m_new;
+  #pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) acc[j][dt] *= alpha;
+
+        // ---- O^T += V^T . P^T, chunk by chunk
+  #pragma unroll
+        for (int i = 0; i < NC; ++i) {
+          if (i >= nv) break;  // uniform
+          if constexpr (sizeof(T) == 2) {
+            bf16x8 ph, pl;
+  #pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float pv = p[2 * i + (e >> 2)][e & 3];
+              const __bf16 hi = (__bf16)pv;
+              ph[e] = hi;
+              pl[e] = (__bf16)(pv - (float)hi);
+            }
+  #pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt) {
+              const int dr = dt * 16 + ln16;
+              const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(Vs[i] + dr * TL::VROW + 4 * g4);
+              const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(Vs[i] + (D + dr) * TL::VROW + 4 * g4);
+              const bf16x8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+              acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, acc[j][dt], 0, 0, 0);
+              acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, acc[j][dt], 0, 0, 0);
+            }
+          } else {
+  #pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt) {
+              const int dr = dt * 16 + ln16;
+  #pragma unroll
+              for (int tile = 0; tile < 2; ++tile) {
+                const f32x4 vv =
+                    *reinterpret_cast<const f32x4*>(Vs[i] + (tile * D + dr) * TL::VROW + 4 * g4);
+  #pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  acc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[e], p[2 * i + tile][e],
+                                                                   acc[j][dt], 0, 0, 0);
+              }
             }
           }
         }
       }
-    }
-  };
-  auto compute_chunk = [&](int c, int buf) {
-    compute_group(std::integral_constant<int, 1>{}, c, buf, 1);
-  };
+    };
+    auto compute_chunk = [&](int c, int buf) {
+      compute_group(std::integral_constant<int, 1>{}, c, buf, 1);
+    };
 
-  // Chunk c goes through LDS buffer c & 1.  That buffer was last read while
-  // computing chunk c - 2, and every wavefront has since passed the barrier of
-  // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
-  // compile-time constants (two chunks per trip when DEPTH == 2).
-  uint32_t keep[DEPTH];
-  if constexpr (PAIR && DEPTH == 2) {
-    // chunks in pairs: both of a pair in LDS and computed together while the
-    // next pair's loads are in flight
-    load_chunk(0, stage[0], keep[0]);
-    if (nchunks > 1) load_chunk(1, stage[1], keep[1]);
-#pragma unroll 1
-    for (int c = 0; c < nchunks; c += 2) {
-      const int nv = min(2, nchunks - c);
-      store_chunk(0, stage[0], keep[0]);
-      if (nv > 1) store_chunk(1, stage[1], keep[1]);
-      if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
-      if (c + 3 < nchunks) load_chunk(c + 3, stage[1], keep[1]);
-      __syncthreads();
-      compute_group(std::integral_constant<int, 2>{}, c, 0, nv);
-      if (c + 2 < nchunks) __syncthreads();  // the buffers are rewritten next trip
-    }
-  } else if constexpr (DEPTH == 2) {
-    load_chunk(0, stage[0], keep[0]);
-    if (nchunks > 1) load_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
-#pragma unroll 1
-    for (int c = 0; c < nchunks; c += 2) {
-      store_chunk(0, stage[0], keep[0]);
-      if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
-      __syncthreads();
-      compute_chunk(c, 0);
-      if (c + 1 < nchunks) {
-        store_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
-        if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1], keep[DEPTH - 1]);
+    // Chunk c goes through LDS buffer c & 1.  That buffer was last read while
+    // computing chunk c - 2, and every wavefront has since passed the barrier of
+    // chunk c - 1, so it can be rewritten.  Staging registers are indexed with
+    // compile-time constants (two chunks per trip when DEPTH == 2).
+    uint32_t keep[DEPTH];
+    if constexpr (PAIR && DEPTH == 2) {
+      // chunks in pairs: both of a pair in LDS and computed together while the
+      // next pair's loads are in flight
+      load_chunk(0, stage[0], keep[0]);
+      if (nchunks > 1) load_chunk(1, stage[1], keep[1]);
+  #pragma unroll 1
+      for (int c = 0; c < nchunks; c += 2) {
+        const int nv = min(2, nchunks - c);
+        store_chunk(0, stage[0], keep[0]);
+        if (nv > 1) store_chunk(1, stage[1], keep[1]);
+        if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
+        if (c + 3 < nchunks) load_chunk(c + 3, stage[1], keep[1]);
         __syncthreads();
-        compute_chunk(c + 1, 1);
+        compute_group(std::integral_constant<int, 2>{}, c, 0, nv);
+        if (c + 2 < nchunks) __syncthreads();  // the buffers are rewritten next trip
       }
-    }
-  } else {
-    load_chunk(0, stage[0], keep[0]);
-#pragma unroll 1
-    for (int c = 0; c < nchunks; ++c) {
-      store_chunk(c & 1, stage[0], keep[0]);
-      if (c + 1 < nchunks) load_chunk(c + 1, stage[0], keep[0]);
-      __syncthreads();
-      compute_chunk(c, c & 1);
+    } else if constexpr (DEPTH == 2) {
+      load_chunk(0, stage[0], keep[0]);
+      if (nchunks > 1) load_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
+  #pragma unroll 1
+      for (int c = 0; c < nchunks; c += 2) {
+        store_chunk(0, stage[0], keep[0]);
+        if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
+        __syncthreads();
+        compute_chunk(c, 0);
+        if (c + 1 < nchunks) {
+          store_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
+          if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1], keep[DEPTH - 1]);
+          __syncthreads();
+          compute_chunk(c + 1, 1);
+        }
+      }
+    } else {
+      load_chunk(0, stage[0], keep[0]);
+  #pragma unroll 1
+      for (int c = 0; c < nchunks; ++c) {
+        store_chunk(c & 1, stage[0], keep[0]);
+        if (c + 1 < nchunks) load_chunk(c + 1, stage[0], keep[0]);
+        __syncthreads();
+        compute_chunk(c, c & 1);
+      }
     }
   }
 
@@ -1188,8 +1192,8 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
   const Geometry& g = a.g;
   const int lane = thread_index() & 63;
   const int e0 = lane * E;
-  const int nvs = min((get_c<COH>(a.nsel + bh) + g.pages_per_split - 1) / g.pages_per_split,
-                      g.n_splits);
+  // every split holds a partial, (0, -inf) if nothing was selected in it
+  const int nvs = g.n_splits;
   float m[NR], wl[NR], acc[NR][E];
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
