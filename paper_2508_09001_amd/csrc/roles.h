@@ -284,10 +284,12 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b
 // pages per wavefront; pass it covers the workgroup's pages it*nw*4 onwards).
 // COH: the token's key and value are read by other workgroups of the same
 // launch, so they are stored device-coherently.
-template <typename T, int D, int ITERS, bool COH = false>
+// The token and the number of pages of the sequence come from `tok_of(n_pages)`
+// (returns the StepToken, sets n_pages), called once the digest and query loads
+// are issued: its own loads (sequence length, page table) then overlap them.
+template <typename T, int D, int ITERS, bool COH, typename TokOf>
 __device__ __forceinline__ void score_role(const Geometry& g, int page0, int page_end, const T* q,
-                                           T* drow, int n_pages, float* srow, float* sq,
-                                           const StepToken<T> tok) {
+                                           T* drow, float* srow, float* sq, TokOf&& tok_of) {
 #pragma clang fp contract(off)
   using S = ScoreShape<T, D>;
   const int tid = thread_index();
@@ -317,6 +319,8 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
     const int e = (tid + r * blockDim.x) * QV;
     if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
+  int n_pages = 0;
+  const StepToken<T> tok = tok_of(n_pages);
   const bool has_tok = tok.lp >= 0 && tok.lp >= page0 && tok.lp < page_end;
   // the token's key and value, element tid, for the append at the end: read
   // now so that the append does not wait for a round trip of its own (every

@@ -89,17 +89,23 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
   const int page0 = blockIdx.x * ppb, page_end = min(page0 + ppb, g.max_pages);
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
-  const int pos = seq_lens[b];
-  StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
-  int seq_len = pos;
-  if (g.token_pending) {
-    const int phys = token_phys(g, ta.pt, b, pos);
-    if (phys >= 0) {
-      seq_len = pos + 1;
-      tk = make_step_token<T>(g, b, h, pos, phys, ta.k_new, ta.v_new, ta.kc, ta.vc);
+  // the step's token and the sequence's pages (after the digest loads are issued)
+  int n_pages = 0, tok_lp = -1;
+  auto tok_of = [&](int& np) {
+    const int pos = seq_lens[b];
+    StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
+    int seq_len = pos;
+    if (g.token_pending) {
+      const int phys = token_phys(g, ta.pt, b, pos);
+      if (phys >= 0) {
+        seq_len = pos + 1;
+        tk = make_step_token<T>(g, b, h, pos, phys, ta.k_new, ta.v_new, ta.kc, ta.vc);
+      }
     }
-  }
-  const int n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
+    np = n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
+    tok_lp = tk.lp;
+    return tk;
+  };
   int32_t warm_a = 0, warm_p = 0;
   if constexpr (PER > 0) {
     // Fetch this workgroup's last_loaded and page-table entries along with its
@@ -110,9 +116,9 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
       warm_p = sa.tk.pt[(int64_t)b * g.max_pages + p];
     }
   }
-  score_role<T, D, score_iters(PER)>(g, page0, page_end, q + b * q_bstride + (int64_t)h * g.G * D,
-                                dg + bh * g.max_pages * 2 * D, n_pages, scores + bh * g.max_pages,
-                                dyn_lds, tk);
+  score_role<T, D, score_iters(PER), false>(g, page0, page_end, q + b * q_bstride + (int64_t)h * g.G * D,
+                                dg + bh * g.max_pages * 2 * D, scores + bh * g.max_pages,
+                                dyn_lds, tok_of);
   if constexpr (PER > 0) {
     asm volatile("" : : "v"(warm_a), "v"(warm_p));  // keeps the two loads
     __shared__ int s_last;
@@ -141,7 +147,7 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
     if (s_last) {
       uint32_t* hist = reinterpret_cast<uint32_t*>(dyn_lds);
       int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-      topk_role<PER, score_threads(PER) / 64, false>(sa.tk, (int)bh, [&] { return n_pages; }, tk.lp, hist, small, [] {});
+      topk_role<PER, score_threads(PER) / 64, false>(sa.tk, (int)bh, [&] { return n_pages; }, tok_lp, hist, small, [] {});
     }
   }
 }

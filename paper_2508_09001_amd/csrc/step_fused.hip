@@ -131,8 +131,9 @@ step_kernel(StepArgs a) {
         score_role<T, D, kFusedScoreIters, true>(
             g, sub * ppb, min(sub * ppb + ppb, g.max_pages),
             reinterpret_cast<const T*>(a.q_cur) + b * a.q_bstride + (int64_t)h * g.G * D,
-            reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D, n_pages,
-            a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds), tk);
+            reinterpret_cast<T*>(a.dg) + (int64_t)bh * g.max_pages * 2 * D,
+            a.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds),
+            [&](int& np) { np = n_pages; return tk; });
         block_signal(cntA + kCtlStride * bh);
       } else if (role == 1) {
         topk_role<PER, kFusedWaves, true>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
