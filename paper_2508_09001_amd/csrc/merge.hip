@@ -26,17 +26,19 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   // units ordered (sequence, KV head, query head of the group, row slot), spread
   // so that a KV head's units share the XCD its attention splits ran on
   const Geometry& g = a.g;
-  if (blockIdx.x == 0 && g.token_pending && a.seq_lens) {
-    // no other workgroup of this launch reads seq_lens
-    for (int b = threadIdx.x; b < g.batch; b += blockDim.x) {
-      const int pos = a.seq_lens[b];
-      if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
-    }
-  }
   const int nunits = g.batch * g.hq * a.xs;
   const int u = xcd_remap(blockIdx.x, gridDim.x) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
   merge_unit<D, 32>(a, u);
+  if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
+    // after the unit's own loads (the two lookups here are dependent): the
+    // first wavefront advances every sequence; no other workgroup of this
+    // launch reads seq_lens
+    for (int b = threadIdx.x; b < g.batch; b += 64) {
+      const int pos = a.seq_lens[b];
+      if (token_phys(g, a.pt, b, pos) >= 0) a.seq_lens[b] = pos + 1;
+    }
+  }
 }
 
 }  // namespace
