@@ -19,7 +19,7 @@
 namespace retro {
 namespace {
 
-constexpr int kWaves = 4;  // wavefronts (work units) per workgroup
+constexpr int kWaves = 2;  // wavefronts (work units) per workgroup: 256 workgroups at the headline shape, one per CU
 
 template <int D>
 __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
