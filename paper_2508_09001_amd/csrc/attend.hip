@@ -35,9 +35,14 @@
 namespace retro {
 namespace {
 
+// Workgroups have eight wavefronts (the host checks); staging registers are
+// sized for that: a chunk's 16-byte pieces spread over 512 threads.
+constexpr int kAttendThreads = 512;
+
 template <typename T, int D, int RTW>
-__global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
+__global__ void __launch_bounds__(kAttendThreads) attend_kernel(AttendArgs a) {
   using TL = Tiles<T, D>;
+  constexpr int MAXP = (TL::PIECES + kAttendThreads - 1) / kAttendThreads;
   __shared__ __attribute__((aligned(16))) T lds[2 * TL::BUF_ELEMS];
   __shared__ int s_phys[kMaxSplitPages];
   __shared__ int s_page[kMaxSplitPages];
@@ -53,7 +58,7 @@ __global__ void __launch_bounds__(512) attend_kernel(AttendArgs a) {
   const int rg = u % g.n_rgroups;
   u /= g.n_rgroups;
   const int h = u % g.hk, b = u / g.hk;
-  attend_role<T, D, RTW, kMaxPieces, RTW == 1, false>(a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); },
+  attend_role<T, D, RTW, MAXP, RTW == 1, false>(a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); },
                          lds, s_phys, s_page, s_mask, [] {});
 }
 
@@ -61,7 +66,8 @@ template <typename T, int D, int RTW>
 hipError_t attend_t(const AttendArgs& a, hipStream_t s) {
   const Geometry& g = a.g;
   const int64_t n = (int64_t)g.n_splits * g.n_rgroups * g.hk * g.batch;
-  attend_kernel<T, D, RTW><<<(unsigned)n, 64 * g.waves, 0, s>>>(a);
+  if (64 * g.waves != kAttendThreads) return hipErrorInvalidValue;
+  attend_kernel<T, D, RTW><<<(unsigned)n, kAttendThreads, 0, s>>>(a);
   return hipGetLastError();
 }
 
