@@ -1011,14 +1011,17 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         mloc = col_max4(mloc);
         const float m_new = fmaxf(m_run[j], mloc);
         const float mu = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = exp2f(m_run[j] - mu);
+        // the hardware exp2 (v_exp_f32, ~1 ulp): arguments are <= 0, and a
+        // result below the normal range (a weight under 2^-126 of the row's
+        // largest) becomes 0 instead of a denormal
+        const float alpha = __builtin_amdgcn_exp2f(m_run[j] - mu);
         float p[NT][4];
         float psum = 0.f;
   #pragma unroll
         for (int tt = 0; tt < NT; ++tt)
   #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            p[tt][i] = exp2f(x[tt][i] - mu);
+            p[tt][i] = __builtin_amdgcn_exp2f(x[tt][i] - mu);
             psum += p[tt][i];
           }
         l_run[j] = l_run[j] * alpha + psum;
