@@ -199,6 +199,20 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
                                           const retro_selection* sel, void* workspace,
                                           size_t ws_bytes, void* stream);
 
+/* The selection (top-k + UpdateAndBuildMask's mask, Alg. 2) and attention pass
+ * of retro_step alone, as the one kernel launch retro_step runs for them: the
+ * page scores are those the last retro_step or retro_select_pages call with this
+ * workspace left in it, the sequence lengths those of `cache` (no pending token).
+ * Writes sel's rows, mask and count (mask values from last_loaded as it stands,
+ * which this call does not update) and the splits' partials in the workspace.
+ * Meant for timing the step's dominant kernel in isolation; returns
+ * RETRO_EUNSUPPORTED where retro_step selects in a launch of its own
+ * (max_pages > 6144). */
+retro_status retro_select_attend_partials(const retro_dims* dims, int32_t step,
+                                          const void* q_window, const retro_kv_cache* cache,
+                                          const retro_selection* sel, void* workspace,
+                                          size_t ws_bytes, void* stream);
+
 /* MergeOutput + CacheOutput (Alg. 1; eq. merged_attn_general) for step t.
  * For each query head and row r with tau = t-W+r >= 0:
  *   r == W   : out = part; pushed to slot t mod W;
@@ -215,7 +229,12 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
- * semantics, without materialising o_part / lse_part.
+ * semantics, without materialising o_part / lse_part.  Three launches: page
+ * scores (with the append); the selection in front of the attention; combine +
+ * merge (with the last_loaded update and the seq_lens advance).  With
+ * RETRO_SELECT_IN_SCORE=1 in the environment (read on every call), or for
+ * max_pages > 6144, the selection runs at the end of the score launch (or in a
+ * launch of its own) instead.
  * With RETRO_STEP_FUSED=1 in the environment (read on every call) the step runs
  * as one launch whose workgroups hand work to each other through counters kept
  * in `workspace` (zero-filled once, as for every call).  If a hand-off wait

@@ -96,6 +96,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256((kCtlCounts + 3 * bhs * kCtlStride) * sizeof(int32_t));
   x.ws_sel = off;  // per-head counters of the score + selection launch
   off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
+  x.ws_tok = off;  // per KV head: the step's token page when not kept (selection in attention)
+  off += align256(bhs * sizeof(int32_t));
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -238,6 +240,25 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
                                        (hipStream_t)stream));
 }
 
+retro_status retro_select_attend_partials(const retro_dims* dims, int32_t step,
+                                          const void* q_window, const retro_kv_cache* cache,
+                                          const retro_selection* sel, void* workspace,
+                                          size_t ws_bytes, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!q_window || !cache_ok(cache) || !sel_ok(sel)) return RETRO_EINVAL;
+  if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
+  if (!retro::attend_selects(g)) return RETRO_EUNSUPPORTED;
+  int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
+  int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
+  return from_hip(retro::launch_attend_select(g, step, q_window, *cache, *sel, phys,
+                                              ws_at(workspace, g.ws_scores),
+                                              ws_at(workspace, g.ws_opart),
+                                              ws_at(workspace, g.ws_lpart), tok,
+                                              (hipStream_t)stream));
+}
+
 retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, const float* o_part,
                                       const float* lse_part, const retro_output_cache* ocache,
                                       float* o_out, float* lse_out, void* stream) {
@@ -256,6 +277,13 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 namespace {
 // The single-launch step is chosen with RETRO_STEP_FUSED=1 in the environment
 // (read on every call); otherwise the step runs as five dependent launches.
+// RETRO_SELECT_IN_SCORE=1: the selection at the end of the score launch
+// instead of in front of the attention
+bool select_in_score_requested() {
+  const char* v = std::getenv("RETRO_SELECT_IN_SCORE");
+  return v && v[0] == '1';
+}
+
 bool fused_requested() {
   const char* v = std::getenv("RETRO_STEP_FUSED");
   return v && v[0] == '1';
@@ -290,6 +318,21 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   // (+ seq_lens advance)
   Geometry gp = g;
   gp.token_pending = 1;
+  if (retro::attend_selects(gp) && !select_in_score_requested()) {
+    // score (+ the token's append) -> attention with the selection in front ->
+    // combine + merge (+ last_loaded update, + seq_lens advance)
+    int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
+    hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores,
+                                       nullptr, nullptr, nullptr, s);
+    if (e == hipSuccess)
+      e = retro::launch_attend_select(gp, step, q_window, *cache, *sel, phys, scores, o_ws, l_ws,
+                                      tok, s);
+    if (e == hipSuccess)
+      e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
+                                      nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
+                                      sel->selected, tok);
+    return from_hip(e);
+  }
   int32_t* counters = reinterpret_cast<int32_t*>((char*)workspace + g.ws_sel);
   hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores, sel, phys,
                                      counters, s);

@@ -58,8 +58,9 @@ __global__ void __launch_bounds__(kAttendThreads) attend_kernel(AttendArgs a) {
   const int rg = u % g.n_rgroups;
   u /= g.n_rgroups;
   const int h = u % g.hk, b = u / g.hk;
-  attend_role<T, D, RTW, MAXP, RTW == 1, false>(a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); },
-                         lds, s_phys, s_page, s_mask, [] {});
+  attend_role<T, D, RTW, MAXP, RTW == 1, false>(
+      a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); }, lds, s_phys,
+      s_page, s_mask, [] {}, SelectionRows{});
 }
 
 template <typename T, int D, int RTW>
@@ -74,6 +75,124 @@ hipError_t attend_t(const AttendArgs& a, hipStream_t s) {
 template <typename T, int D>
 hipError_t attend_d(const AttendArgs& a, hipStream_t s) {
   return a.g.rtw == 1 ? attend_t<T, D, 1>(a, s) : attend_t<T, D, 2>(a, s);
+}
+
+// Attention with the page selection in front: every workgroup of a KV head
+// runs the head's top-k (the same computation on the same scores, so the same
+// result) and takes its split's slots of the selection from LDS, instead of
+// waiting for a selection launch and reading the rows back.  The workgroup of
+// split 0, row group 0 writes the selection rows, the count and, for the
+// step's token page, -1 when it is kept and its logical page otherwise
+// (tok_out[bh]); last_loaded is left alone here (other workgroups of the head
+// read it) and updated by the combine launch from those outputs.  The
+// selection's histograms share LDS with the chunk staging, which is only used
+// after the page list is in place.
+template <typename T, int D, int RTW, int PER>
+__global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArgs a, TopkArgs ta,
+                                                                       int32_t* tok_out) {
+  using TL = Tiles<T, D>;
+  constexpr int MAXP = (TL::PIECES + kAttendThreads - 1) / kAttendThreads;
+  constexpr int kStageBytes = 2 * TL::BUF_ELEMS * (int)sizeof(T);
+  constexpr int kSelectBytes = (kTopkHistWords + kTopkSmall) * 4;
+  __shared__ __attribute__((aligned(16))) char lds[std::max(kStageBytes, kSelectBytes)];
+  __shared__ int s_phys[kMaxSplitPages];
+  __shared__ int s_page[kMaxSplitPages];
+  __shared__ int s_mask[kMaxSplitPages];
+  __shared__ int l_lp[kMaxSplitPages], l_m[kMaxSplitPages], l_ph[kMaxSplitPages];
+  __shared__ int s_k;
+  const Geometry& g = a.g;
+  int u = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = u % g.n_splits;
+  u /= g.n_splits;
+  const int rg = u % g.n_rgroups;
+  u /= g.n_rgroups;
+  const int h = u % g.hk, b = u / g.hk;
+  const int bh = b * g.hk + h;
+  const bool writer = split == 0 && rg == 0;
+  const int first = split * g.pages_per_split;
+  const int tid = thread_index();
+  int seq_len = 0, tok_lp = -1;
+  auto select = [&] {
+    uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
+    int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
+    int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
+    int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
+    int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
+    const int k = topk_core<PER, kAttendThreads / 64>(
+        ta, bh,
+        [&] {
+          const int pos = a.seq_lens[b];
+          seq_len = pos;
+          tok_lp = -1;
+          if (g.token_pending && token_phys(g, a.pt, b, pos) >= 0) {
+            seq_len = pos + 1;
+            tok_lp = pos / g.P;
+          }
+          return min((seq_len + g.P - 1) / g.P, g.max_pages);
+        },
+        tok_lp, hist, small, [] {},
+        [&](int pos, int p, int a_old, int phys) {
+          const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
+          if (pos >= first && pos < first + g.pages_per_split) {
+            l_lp[pos - first] = p;
+            l_m[pos - first] = a_old;
+            l_ph[pos - first] = ph;
+          }
+          if (writer) {
+            if (pos >= 0) {
+              sel_row[pos] = p;
+              m_row[pos] = a_old;
+              ph_row[pos] = ph;
+            }
+            if (p == tok_lp) tok_out[bh] = pos < 0 ? p : -1;
+          }
+        });
+    if (writer) {
+      for (int i = k + tid; i < g.k_max; i += kAttendThreads) {
+        sel_row[i] = -1;
+        m_row[i] = -1;
+        ph_row[i] = -1;
+      }
+      if (tid == 0) {
+        ta.num_selected[bh] = k;
+        if (tok_lp < 0) tok_out[bh] = -1;
+      }
+    }
+    if (tid == 0) s_k = k;
+    __syncthreads();  // the split's page list and the count are in LDS
+  };
+  attend_role<T, D, RTW, MAXP, RTW == 1, false>(
+      a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
+      s_mask, select, [&](int t, int, int& lp, int& m, int& phys) {
+        if (t < g.pages_per_split) {
+          lp = l_lp[t];
+          m = l_m[t];
+          phys = l_ph[t];
+        }
+        return s_k;
+      });
+}
+
+template <typename T, int D, int PER>
+hipError_t attend_select_p(const AttendArgs& a, const TopkArgs& ta, int32_t* tok_out,
+                           hipStream_t s) {
+  const Geometry& g = a.g;
+  const int64_t n = (int64_t)g.n_splits * g.n_rgroups * g.hk * g.batch;
+  if (64 * g.waves != kAttendThreads || g.max_pages > PER * kAttendThreads) return hipErrorInvalidValue;
+  if (g.rtw == 1)
+    attend_select_kernel<T, D, 1, PER><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, tok_out);
+  else
+    attend_select_kernel<T, D, 2, PER><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, tok_out);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t attend_select_d(const AttendArgs& a, const TopkArgs& ta, int32_t* tok_out,
+                           hipStream_t s) {
+  const int mp = a.g.max_pages;
+  if (mp <= 2 * kAttendThreads) return attend_select_p<T, D, 2>(a, ta, tok_out, s);
+  if (mp <= 5 * kAttendThreads) return attend_select_p<T, D, 5>(a, ta, tok_out, s);
+  return attend_select_p<T, D, 12>(a, ta, tok_out, s);
 }
 
 }  // namespace
@@ -111,6 +230,23 @@ hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
   const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
   if (g.dtype == RETRO_BF16) return g.D == 128 ? attend_d<bf16_t, 128>(a, s) : attend_d<bf16_t, 64>(a, s);
   return g.D == 128 ? attend_d<float, 128>(a, s) : attend_d<float, 64>(a, s);
+}
+
+bool attend_selects(const Geometry& g) { return g.max_pages <= 12 * kAttendThreads; }
+
+hipError_t launch_attend_select(const Geometry& g, int step, const void* q_window,
+                                const retro_kv_cache& c, const retro_selection& sel,
+                                int32_t* sel_phys, const float* scores, float* o_ws, float* l_ws,
+                                int32_t* tok_out, hipStream_t s) {
+  if (!attend_selects(g) || !sel_phys || !tok_out) return hipErrorInvalidValue;
+  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
+  const TopkArgs ta{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
+                    sel.num_selected, sel_phys};
+  if (g.dtype == RETRO_BF16)
+    return g.D == 128 ? attend_select_d<bf16_t, 128>(a, ta, tok_out, s)
+                      : attend_select_d<bf16_t, 64>(a, ta, tok_out, s);
+  return g.D == 128 ? attend_select_d<float, 128>(a, ta, tok_out, s)
+                    : attend_select_d<float, 64>(a, ta, tok_out, s);
 }
 
 }  // namespace retro

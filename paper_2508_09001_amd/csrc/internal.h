@@ -58,7 +58,7 @@ struct Geometry {
   int64_t f_grid;
   bool fused;
   // workspace layout (bytes)
-  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_sel, ws_total;
+  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_sel, ws_tok, ws_total;
   // set for the launches of a step whose token is written by its score launch:
   // seq_lens does not count the token yet (the merge launch advances it), and
   // every launch uses the length with the token
@@ -109,17 +109,31 @@ hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
                          const retro_kv_cache& c, const retro_selection& sel,
                          const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s);
+// Attention with the page selection (top-k + Alg. 2's mask) computed by each
+// of its workgroups (attend_selects(g)); writes the selection outputs (rows,
+// mask, physical pages, count) but not last_loaded: the combine launch after
+// it takes `selected` = sel.selected and `tok_out` to update it.  scores: the
+// score launch's page scores; tok_out: [batch * h_k] ints of workspace.
+bool attend_selects(const Geometry& g);
+hipError_t launch_attend_select(const Geometry& g, int step, const void* q_window,
+                                const retro_kv_cache& c, const retro_selection& sel,
+                                int32_t* sel_phys, const float* scores, float* o_ws, float* l_ws,
+                                int32_t* tok_out, hipStream_t s);
 hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
                              const void* v_new, const retro_kv_cache& c,
                              const retro_selection& sel, const retro_output_cache* oc,
                              float* o_out, float* lse_out, void* workspace, hipStream_t s);
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
 // With g.token_pending and a cache, the launch also advances seq_lens past the
-// step's token (when its page is mapped).
+// step's token (when its page is mapped).  With `selected` and `tok_upd` (from
+// launch_attend_select; num_selected and cache required), it also applies the
+// step's last_loaded update.
 hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
                                 const float* l_ws, const int32_t* num_selected,
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
-                                float* lse_out, const retro_kv_cache* cache, hipStream_t s);
+                                float* lse_out, const retro_kv_cache* cache, hipStream_t s,
+                                const int32_t* selected = nullptr,
+                                const int32_t* tok_upd = nullptr);
 
 }  // namespace retro

@@ -21,13 +21,35 @@ namespace {
 
 constexpr int kWaves = 2;  // wavefronts (work units) per workgroup: 256 workgroups at the headline shape, one per CU
 
+__device__ __forceinline__ void update_last_loaded(const MergeArgs& a, int bh) {
+  const Geometry& g = a.g;
+  const int lane = threadIdx.x & 63;
+  const int k = a.nsel[bh];
+  const int tok = a.tok_upd[bh];
+  const int32_t* srow = a.sel_upd + (int64_t)bh * g.k_max;
+  int32_t* arow = a.a_upd + (int64_t)bh * g.max_pages;
+  for (int i = lane; i < k && i < g.k_max; i += 64) {
+    const int p = srow[i];
+    if (p >= 0 && p < g.max_pages) arow[p] = a.step;
+  }
+  if (lane == 0 && tok >= 0 && tok < g.max_pages) arow[tok] = a.step - 1;
+}
+
 template <int D>
 __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
   // units ordered (sequence, KV head, query head of the group, row slot), spread
   // so that a KV head's units share the XCD its attention splits ran on
   const Geometry& g = a.g;
   const int nunits = g.batch * g.hq * a.xs;
-  const int u = xcd_remap(blockIdx.x, gridDim.x) * kWaves + (threadIdx.x >> 6);
+  const int mblocks = (nunits + kWaves - 1) / kWaves;
+  if ((int)blockIdx.x >= mblocks) {
+    // workgroups past the merge units: Alg. 2's last_loaded update, one KV
+    // head per wavefront
+    const int bh = ((int)blockIdx.x - mblocks) * kWaves + (threadIdx.x >> 6);
+    if (bh < g.batch * g.hk) update_last_loaded(a, bh);
+    return;
+  }
+  const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
   merge_unit<D, 32>(a, u);
   if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
@@ -65,6 +87,9 @@ MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_
   a.l_out = lse_out;
   a.seq_lens = nullptr;
   a.pt = nullptr;
+  a.a_upd = nullptr;
+  a.sel_upd = nullptr;
+  a.tok_upd = nullptr;
   return a;
 }
 
@@ -72,15 +97,24 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
                                 const float* l_ws, const int32_t* num_selected,
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
-                                float* lse_out, const retro_kv_cache* cache, hipStream_t s) {
+                                float* lse_out, const retro_kv_cache* cache, hipStream_t s,
+                                const int32_t* selected, const int32_t* tok_upd) {
   MergeArgs a = make_merge_args(g, step, mode, o_ws, l_ws, num_selected, o_part, l_part,
                                 o_part_out, l_part_out, oc, o_out, lse_out);
   if (cache) {
     a.seq_lens = cache->seq_lens;
     a.pt = cache->page_table;
   }
+  int64_t upd_blocks = 0;
+  if (selected && tok_upd) {
+    if (!cache || !num_selected) return hipErrorInvalidValue;
+    a.a_upd = cache->last_loaded;
+    a.sel_upd = selected;
+    a.tok_upd = tok_upd;
+    upd_blocks = ((int64_t)g.batch * g.hk + kWaves - 1) / kWaves;
+  }
   const int64_t units = (int64_t)g.batch * g.hq * a.xs;
-  const unsigned blocks = (unsigned)((units + kWaves - 1) / kWaves);
+  const unsigned blocks = (unsigned)((units + kWaves - 1) / kWaves + upd_blocks);
   if (g.D == 128)
     combine_merge_kernel<128><<<blocks, 64 * kWaves, 0, s>>>(a);
   else

@@ -445,21 +445,25 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
 
+// The selection itself, without its outputs: returns k, the pages kept, and
+// calls `on_page(pos, p, a_old, phys)` for every stripe slot of every thread
+// (p: logical page, a_old: its last_loaded value as Alg. 2 reads it, phys: its
+// page-table entry; pos: its rank among the kept pages in page order, or -1
+// when it is not kept or past the sequence).
 // THREADS = blockDim.x threads (at most MAXW wavefronts); page i of the
 // sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
 // loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by
-// this step's token (-1: none): Alg. 2's first line applies to it, so its
-// last_loaded entry is taken as step - 1, and set to step - 1 if the page is
-// not kept.  `pages_of()` gives n, the pages of the sequence; it is called once
-// the loads are issued.  hist: kTopkHistWords uint32 of LDS; small: kTopkSmall
-// ints of LDS.
+// this step's token (-1: none), read after `pages_of()` (which may set it):
+// Alg. 2's first line applies to it, so its last_loaded entry is taken as
+// step - 1.  `pages_of()` gives n, the pages of the sequence; it is called once
+// the loads are issued.  hist: kTopkHistWords
+// uint32 of LDS; small: kTopkSmall ints of LDS.
 // `wait()` is called after the page-table and last_loaded loads are issued and
 // before the scores are read.
-// COH: the selection is read by other workgroups of the same launch, so it is
-// stored device-coherently.
-template <int PER, int MAXW, bool COH, typename PagesOf, typename Wait>
-__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
-                                          uint32_t* hist, int* small, Wait&& wait) {
+template <int PER, int MAXW, typename PagesOf, typename Wait, typename OnPage>
+__device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, PagesOf&& pages_of, const int& tok_lp,
+                                         uint32_t* hist, int* small, Wait&& wait,
+                                         OnPage&& on_page) {
   constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
   static_assert(PER * MAXW <= kTopkSmall - 36 && MAXW <= 16 && PER <= 32, "top-k shape");
   const int THREADS = blockDim.x, NW = THREADS >> 6;
@@ -469,7 +473,7 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = bh / g.hk;
   const float* srow = ta.scores + (int64_t)bh * g.max_pages;
-  int32_t* a_row = ta.A + (int64_t)bh * g.max_pages;
+  const int32_t* a_row = ta.A + (int64_t)bh * g.max_pages;
   const int32_t* p_row = ta.pt + (int64_t)b * g.max_pages;
   int* red = small;        // [32]
   int* res = small + 32;   // [4]: T's digit, keys above its bin, keys in it
@@ -663,9 +667,6 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
     sc[c] = incl - val;
     carry = __builtin_amdgcn_readlane(incl, 63);
   }
-  int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
-  int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
-  int32_t* ph_row = ta.sel_phys ? ta.sel_phys + (int64_t)bh * g.k_max : nullptr;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int e = j * NW + wave;
@@ -680,16 +681,39 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
     int pos = -1;
     if (is_gt) pos = gb + min(eb, (int)need);
     if (is_eq && eb < (int)need) pos = gb + eb;
-    const int p = j * THREADS + tid;
-    if (pos >= 0 && pos < k) {  // always true for a kept page; guards the writes
-      put_c<COH>(sel_row + pos, p);
-      put_c<COH>(m_row + pos, a_old[j]);
-      a_row[p] = step;
-      if (ph_row) put_c<COH>(ph_row + pos, (phys[j] >= 0 && phys[j] < g.num_phys) ? phys[j] : -1);
-    } else if (p == tok_lp) {
-      a_row[p] = step - 1;  // the token's page, not kept
-    }
+    // pos < k always holds for a kept page; the test guards the writes
+    on_page(pos < k ? pos : -1, j * THREADS + tid, a_old[j], phys[j]);
   }
+  return k;
+}
+
+// Selection of KV head bh with its outputs: the selected pages in page order,
+// their mask values M (last_loaded before the step) and physical pages, -1
+// past the k kept ones, the count, and last_loaded set to the step for the kept
+// pages (step - 1 for the token's page when it is not kept).  Arguments as
+// topk_core's.  COH: the selection is read by other workgroups of the same
+// launch, so it is stored device-coherently.
+template <int PER, int MAXW, bool COH, typename PagesOf, typename Wait>
+__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
+                                          uint32_t* hist, int* small, Wait&& wait) {
+  const Geometry& g = ta.g;
+  const int step = ta.step;
+  int32_t* a_row = ta.A + (int64_t)bh * g.max_pages;
+  int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
+  int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
+  int32_t* ph_row = ta.sel_phys ? ta.sel_phys + (int64_t)bh * g.k_max : nullptr;
+  const int k = topk_core<PER, MAXW>(
+      ta, bh, pages_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
+        if (pos >= 0) {
+          put_c<COH>(sel_row + pos, p);
+          put_c<COH>(m_row + pos, a_old);
+          a_row[p] = step;
+          if (ph_row) put_c<COH>(ph_row + pos, (phys >= 0 && phys < g.num_phys) ? phys : -1);
+        } else if (p == tok_lp) {
+          a_row[p] = step - 1;  // the token's page, not kept
+        }
+      });
+  const int tid = thread_index(), THREADS = blockDim.x;
   for (int i = k + tid; i < g.k_max; i += THREADS) {
     put_c<COH>(sel_row + i, -1);
     put_c<COH>(m_row + i, -1);
@@ -745,10 +769,18 @@ struct AttendArgs {
 // sequence length in effect; it is called once the page-list loads are issued.
 // COH: the selection comes from, and the partials go to, other workgroups of
 // the same launch: device-coherent loads and stores.
-template <typename T, int D, int RTW, int MAXP, bool PAIR, bool COH, typename SeqLen, typename Wait>
+// The split's page list comes from the selection rows in memory (COH: written
+// by other workgroups of the same launch) when `list` is a SelectionRows, else
+// `list(tid, first, lp, m, phys)` gives thread tid's slot of it (slot tid of
+// the selection row from `first` on: logical page, mask value, physical page;
+// left as passed in for tid >= pages_per_split) and returns the number of
+// selected pages of the row.
+struct SelectionRows {};
+template <typename T, int D, int RTW, int MAXP, bool PAIR, bool COH, typename SeqLen, typename Wait,
+          typename List = SelectionRows>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
                                             SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
-                                            int* s_mask, Wait&& wait) {
+                                            int* s_mask, Wait&& wait, List&& list) {
   using TL = Tiles<T, D>;
   const Geometry& g = a.g;
   const int bh = b * g.hk + h;
@@ -810,13 +842,18 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   // handles slot i (kMaxSplitPages <= workgroup size).
   const int first = split * g.pages_per_split;
   int lp = -1, m = 0, phys = -1;
-  if (tid < g.pages_per_split && first + tid < g.k_max) {
-    const int64_t o = (int64_t)bh * g.k_max + first + tid;
-    lp = get_c<COH>(a.sel + o);
-    m = get_c<COH>(a.msk + o);
-    if (a.sel_phys) phys = get_c<COH>(a.sel_phys + o);
+  int k_eff;
+  if constexpr (std::is_same<typename std::decay<List>::type, SelectionRows>::value) {
+    if (tid < g.pages_per_split && first + tid < g.k_max) {
+      const int64_t o = (int64_t)bh * g.k_max + first + tid;
+      lp = get_c<COH>(a.sel + o);
+      m = get_c<COH>(a.msk + o);
+      if (a.sel_phys) phys = get_c<COH>(a.sel_phys + o);
+    }
+    k_eff = get_c<COH>(a.nsel + bh);
+  } else {
+    k_eff = list(tid, first, lp, m, phys);
   }
-  const int k_eff = get_c<COH>(a.nsel + bh);
   const int seq_len = seq_len_of();
   const int np = min(g.pages_per_split, k_eff - first);
   // A split with nothing selected still writes its (empty) partial: (0, -inf)
@@ -1176,6 +1213,12 @@ struct MergeArgs {
   float* l_out;
   int32_t* seq_lens;    // advanced past a pending token (Geometry::token_pending), or null
   const int32_t* pt;
+  // last_loaded update of the step (Alg. 2) when the selection was made without
+  // it: the kept pages (selection rows, counts) get the step, the token page
+  // tok_upd[bh] (-1: none) step - 1.  Null: no update.
+  int32_t* a_upd;
+  const int32_t* sel_upd;
+  const int32_t* tok_upd;
 };
 
 template <int D>

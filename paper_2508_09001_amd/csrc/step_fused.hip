@@ -143,7 +143,8 @@ step_kernel(StepArgs a) {
       } else if (role == 2) {
         const int rg = sub / g.n_splits, split = sub - rg * g.n_splits;
         attend_role<T, D, 1, MAXP, false, true>(a.at, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys,
-                               s_page, s_mask, [&] { block_wait(cntB + kCtlStride * bh, 1, err); });
+                               s_page, s_mask, [&] { block_wait(cntB + kCtlStride * bh, 1, err); },
+                               SelectionRows{});
         block_signal(cntC + kCtlStride * bh);
       } else {
         block_wait(cntC + kCtlStride * bh, g.fC, err);

@@ -110,6 +110,12 @@ class RetroLayer:
         B.retro_decode_attend_partials(self.dims, step, q_window, self.cache, self.sel,
                                        self.workspace, self.ws_bytes, stream)
 
+    def select_attend_partials(self, step: int, q_window: torch.Tensor, stream=None) -> None:
+        """The step's selection + attention kernel alone, on the page scores the last
+        step left in the workspace (overwrites the selection outputs, not last_loaded)."""
+        B.retro_select_attend_partials(self.dims, step, q_window, self.cache, self.sel,
+                                       self.workspace, self.ws_bytes, stream)
+
     def merge(self, step: int, stream=None) -> None:
         B.retro_merge_output_cache(self.dims, step, self.o_part, self.lse_part, self.ocache,
                                    self.o_out, self.lse_out, stream)

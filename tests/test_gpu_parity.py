@@ -101,3 +101,41 @@ def test_five_row_tiles_fp32():
     spec = W.Spec("edge-5tiles-f32", batch=1, num_kv_heads=2, group=2, head_dim=128, page_size=16,
                   budget=384, window=34, steps=40, dtype="f32", prefill=(1500,), seed=14)
     run_parity(spec, 40, label="edge 5 row tiles f32")
+
+
+def test_select_attend_partials_entry_point():
+    """The timing entry point of the step's selection + attention kernel, run
+    after a step on the scores that step left, selects the same pages; its mask
+    values are last_loaded as the step left it, which it does not change."""
+    import numpy as np
+    import torch
+    from gpu_harness import _gpu_layer
+    spec = W.config(1)
+    gen = W.Generator(spec)
+    layer = _gpu_layer(spec, 6)
+    for b, (k, v) in enumerate(gen.prefill()):
+        layer.prefill(b, k, v)
+    qw = W.QueryWindow(spec)
+    for t in range(6):
+        k_new, v_new, q = gen.step(t)
+        win = qw.push(q).copy()
+        for j in range(k_new.shape[0] - 1):
+            layer.append(t, k_new[j], v_new[j])
+        layer.step(t, win, k_new[-1], v_new[-1])
+    torch.cuda.synchronize()
+    sel0 = layer.selected.cpu().numpy().copy()
+    num0 = layer.num_selected.cpu().numpy().copy()
+    A0 = layer.last_loaded.cpu().numpy().copy()
+    print(f"[entry] retro_select_attend_partials after step {t}", flush=True)
+    layer.select_attend_partials(t, layer._dev(win))
+    torch.cuda.synchronize()
+    assert np.array_equal(layer.num_selected.cpu().numpy(), num0)
+    assert np.array_equal(layer.selected.cpu().numpy(), sel0)
+    assert np.array_equal(layer.last_loaded.cpu().numpy(), A0)
+    msk = layer.mask.cpu().numpy()
+    want = np.full_like(sel0, -1)
+    for b in range(sel0.shape[0]):
+        for h in range(sel0.shape[1]):
+            k = int(num0[b, h])
+            want[b, h, :k] = A0[b, h, sel0[b, h, :k]]
+    assert np.array_equal(msk, want)
