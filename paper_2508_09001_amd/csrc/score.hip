@@ -21,17 +21,16 @@
 namespace retro {
 namespace {
 
-// Workgroup shape.  Four pages per wavefront and pass.  Without the selection
-// epilogue: four wavefronts, one pass (many small workgroups hide the dependent
-// add chains of the tree).  With it: sixteen wavefronts, so that the
-// selection's per-thread share of the head's pages is small, and up to two
-// passes: a KV head's pages are spread over as many workgroups as fit on the
-// chip at once (one sixteen-wavefront workgroup per compute unit), since a
-// workgroup that waits for a free unit starts about 1.3 us after one ends and
-// holds up its head's selection; a wavefront with no page in the second pass
-// skips it.
-constexpr int score_threads(int per) { return per > 0 ? 1024 : 256; }
-constexpr int score_iters(int per) { return per > 0 ? 2 : 1; }
+// Workgroup shape.  Four pages per wavefront and pass, sixteen wavefronts (with
+// the selection epilogue, the selection's per-thread share of the head's pages
+// is then small), up to two passes: a KV head's pages are spread over as many
+// workgroups as fit on the chip at once (one sixteen-wavefront workgroup per
+// compute unit), since a workgroup that waits for a free unit starts about
+// 1.3 us after one ends (and would hold up its head's selection); a wavefront
+// with no page in the second pass skips it.  (Without the epilogue this is
+// also 0.16 us per step faster than four-wavefront workgroups of 16 pages.)
+constexpr int score_threads(int) { return 1024; }
+constexpr int score_iters(int) { return 2; }
 // most pages a workgroup scores
 constexpr int score_pages_per_block(int per) { return score_threads(per) / 64 * 4 * score_iters(per); }
 
@@ -48,7 +47,7 @@ int compute_units() {
   return cus[dev];
 }
 
-// Workgroups per KV head and pages per workgroup of the selecting launch.
+// Workgroups per KV head and pages per workgroup of a score launch.
 void select_split(const Geometry& g, int* nbh, int* ppb) {
   const int one_pass = score_threads(1) / 64 * 4;
   const int fit = std::max(1, compute_units() / std::max(1, g.hk * g.batch));
@@ -195,8 +194,7 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
     // one counter per head up to 32 workgroups, else groups of at least 16
     sa.group = sa.nbh <= 32 ? sa.nbh : std::max(16, (sa.nbh + kSelMaxGroups - 1) / kSelMaxGroups);
   } else {
-    sa.ppb = score_pages_per_block(0);
-    sa.nbh = (g.max_pages + sa.ppb - 1) / sa.ppb;
+    select_split(g, &sa.nbh, &sa.ppb);
   }
   if (g.dtype == RETRO_BF16)
     return g.D == 128 ? score_d<bf16_t, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s)
