@@ -98,6 +98,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
   x.ws_tok = off;  // per KV head: the step's token page when not kept (selection in attention)
   off += align256(bhs * sizeof(int32_t));
+  x.ws_full = off;  // per KV head: arrival and release counters of the one-launch attention
+  off += align256(2 * bhs * kSelCounterInts * sizeof(int32_t));
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -284,6 +286,13 @@ bool select_in_score_requested() {
   return v && v[0] == '1';
 }
 
+// RETRO_SCORE_LAUNCH=1: the page scores in a launch of their own, before the
+// selection + attention launch
+bool score_launch_requested() {
+  const char* v = std::getenv("RETRO_SCORE_LAUNCH");
+  return v && v[0] == '1';
+}
+
 bool fused_requested() {
   const char* v = std::getenv("RETRO_STEP_FUSED");
   return v && v[0] == '1';
@@ -318,6 +327,21 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   // (+ seq_lens advance)
   Geometry gp = g;
   gp.token_pending = 1;
+  if (retro::attend_full_supported(gp, retro::compute_units()) && !select_in_score_requested() &&
+      !score_launch_requested()) {
+    // scores (+ the token's append), selection and attention in one launch ->
+    // combine + merge (+ last_loaded update, + seq_lens advance)
+    int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
+    int32_t* cnt = reinterpret_cast<int32_t*>((char*)workspace + g.ws_full);
+    int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
+    hipError_t e = retro::launch_attend_full(gp, step, q_window, k_new, v_new, *cache, *sel, phys,
+                                             scores, o_ws, l_ws, tok, cnt, err, s);
+    if (e == hipSuccess)
+      e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
+                                      nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
+                                      sel->selected, tok);
+    return from_hip(e);
+  }
   if (retro::attend_selects(gp) && !select_in_score_requested()) {
     // score (+ the token's append) -> attention with the selection in front ->
     // combine + merge (+ last_loaded update, + seq_lens advance)

@@ -195,6 +195,165 @@ hipError_t attend_select_d(const AttendArgs& a, const TopkArgs& ta, int32_t* tok
   return attend_select_p<T, D, 12>(a, ta, tok_out, s);
 }
 
+// Scoring in the same launch (see attend_full_kernel).
+struct ScoreInArgs {
+  const void* q;      // current query rows: sequence b's at q + b * q_bstride
+  int64_t q_bstride;  // elements
+  void* dg;           // digests
+  float* scores;      // [batch][h_k][max_pages]
+  const void* k_new;  // the step's token, [batch][h_k][d]
+  const void* v_new;
+  int32_t* cnt;       // per KV head: an arrival and a release counter, a line each
+  int32_t* err;       // set when a wait runs past its bound
+  int ppb;            // pages scored per workgroup
+};
+
+// Page scores, the token's append, the selection and the attention in one
+// launch.  Each workgroup of a KV head scores its share of the head's pages
+// (appending the token if its page is in that share), writes the scores (and
+// the token) device-coherently, waits for its own stores, meets at a barrier
+// and counts itself in on the head's arrival counter; then it polls the counter
+// until the whole head has arrived, and runs the selection and attention as
+// attend_select_kernel does.  The host launches this form only when every
+// workgroup fits on the chip at once (no more workgroups than compute units,
+// one per unit), so every wait ends; it is bounded all the same (past
+// kSpinLimit polls the error word is set and the workgroup goes on).  Each
+// workgroup then counts itself out on the release counter; the last one of a
+// head clears both for the next launch.
+template <typename T, int D, int PER, int SITERS>
+__global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs a, TopkArgs ta,
+                                                                     ScoreInArgs sc,
+                                                                     int32_t* tok_out) {
+  using TL = Tiles<T, D>;
+  constexpr int MAXP = (TL::PIECES + kAttendThreads - 1) / kAttendThreads;
+  constexpr int kStageBytes = 2 * TL::BUF_ELEMS * (int)sizeof(T);
+  constexpr int kSelectBytes = (kTopkHistWords + kTopkSmall) * 4;
+  __shared__ __attribute__((aligned(16))) char lds[std::max(kStageBytes, kSelectBytes)];
+  __shared__ int s_phys[kMaxSplitPages];
+  __shared__ int s_page[kMaxSplitPages];
+  __shared__ int s_mask[kMaxSplitPages];
+  __shared__ int l_lp[kMaxSplitPages], l_m[kMaxSplitPages], l_ph[kMaxSplitPages];
+  __shared__ int s_k;
+  const Geometry& g = a.g;
+  int u = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = u % g.n_splits;
+  u /= g.n_splits;
+  const int rg = u % g.n_rgroups;
+  u /= g.n_rgroups;
+  const int h = u % g.hk, b = u / g.hk;
+  const int bh = b * g.hk + h;
+  const int per_head = g.n_splits * g.n_rgroups;
+  const bool writer = split == 0 && rg == 0;
+  const int first = split * g.pages_per_split;
+  const int tid = thread_index();
+  int32_t* arrive = sc.cnt + (int64_t)bh * 2 * kSelCounterInts;
+  int32_t* release = arrive + kSelCounterInts;
+
+  // ---- this workgroup's share of the head's page scores
+  int seq_len = 0, tok_lp = -1, n_pages = 0;
+  {
+    const int page0 = (rg * g.n_splits + split) * sc.ppb;
+    const int page_end = min(page0 + sc.ppb, g.max_pages);
+    score_role<T, D, SITERS, true>(
+        g, page0, page_end,
+        reinterpret_cast<const T*>(sc.q) + b * sc.q_bstride + (int64_t)h * g.G * D,
+        reinterpret_cast<T*>(sc.dg) + (int64_t)bh * g.max_pages * 2 * D,
+        sc.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds),
+        [&](int& np) {
+          const int pos = a.seq_lens[b];
+          StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
+          seq_len = pos;
+          if (g.token_pending) {
+            const int phys = token_phys(g, a.pt, b, pos);
+            if (phys >= 0) {
+              seq_len = pos + 1;
+              tk = make_step_token<T>(g, b, h, pos, phys, sc.k_new, sc.v_new,
+                                      const_cast<void*>(a.kc), const_cast<void*>(a.vc));
+            }
+          }
+          np = n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
+          tok_lp = tk.lp;
+          return tk;
+        });
+    block_signal(arrive);
+  }
+
+  auto select = [&] {
+    block_wait(arrive, per_head, sc.err);
+    if (tid == 0 &&
+        __hip_atomic_fetch_add(release, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == per_head - 1) {
+      // every workgroup of the head is past its wait
+      __hip_atomic_store(arrive, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(release, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
+    int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
+    int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
+    int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
+    int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
+    const int k = topk_core<PER, kAttendThreads / 64>(
+        ta, bh, [&] { return n_pages; }, tok_lp, hist, small, [] {},
+        [&](int pos, int p, int a_old, int phys) {
+          const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
+          if (pos >= first && pos < first + g.pages_per_split) {
+            l_lp[pos - first] = p;
+            l_m[pos - first] = a_old;
+            l_ph[pos - first] = ph;
+          }
+          if (writer) {
+            if (pos >= 0) {
+              sel_row[pos] = p;
+              m_row[pos] = a_old;
+              ph_row[pos] = ph;
+            }
+            if (p == tok_lp) tok_out[bh] = pos < 0 ? p : -1;
+          }
+        });
+    if (writer) {
+      for (int i = k + tid; i < g.k_max; i += kAttendThreads) {
+        sel_row[i] = -1;
+        m_row[i] = -1;
+        ph_row[i] = -1;
+      }
+      if (tid == 0) {
+        ta.num_selected[bh] = k;
+        if (tok_lp < 0) tok_out[bh] = -1;
+      }
+    }
+    if (tid == 0) s_k = k;
+    __syncthreads();  // the split's page list and the count are in LDS
+  };
+  attend_role<T, D, 1, MAXP, true, false>(
+      a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
+      s_mask, select, [&](int t, int, int& lp, int& m, int& phys) {
+        if (t < g.pages_per_split) {
+          lp = l_lp[t];
+          m = l_m[t];
+          phys = l_ph[t];
+        }
+        return s_k;
+      });
+}
+
+template <typename T, int D, int PER>
+hipError_t attend_full_p(const AttendArgs& a, const TopkArgs& ta, const ScoreInArgs& sc,
+                         int32_t* tok_out, hipStream_t s) {
+  const Geometry& g = a.g;
+  const int64_t n = (int64_t)g.n_splits * g.n_rgroups * g.hk * g.batch;
+  if (64 * g.waves != kAttendThreads || g.rtw != 1 || g.max_pages > PER * kAttendThreads ||
+      sc.ppb < 1 || sc.ppb > 3 * (kAttendThreads / 64) * 4)
+    return hipErrorInvalidValue;
+  attend_full_kernel<T, D, PER, 3><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t attend_full_d(const AttendArgs& a, const TopkArgs& ta, const ScoreInArgs& sc,
+                         int32_t* tok_out, hipStream_t s) {
+  if (a.g.max_pages <= 2 * kAttendThreads) return attend_full_p<T, D, 2>(a, ta, sc, tok_out, s);
+  return attend_full_p<T, D, 5>(a, ta, sc, tok_out, s);
+}
+
 }  // namespace
 
 int attend_min_waves(int dtype, int D) {
@@ -247,6 +406,44 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
                       : attend_select_d<bf16_t, 64>(a, ta, tok_out, s);
   return g.D == 128 ? attend_select_d<float, 128>(a, ta, tok_out, s)
                     : attend_select_d<float, 64>(a, ta, tok_out, s);
+}
+
+bool attend_full_supported(const Geometry& g, int compute_units) {
+  const int per_head = g.n_splits * g.n_rgroups;
+  const int ppb = (g.max_pages + per_head - 1) / per_head;
+  // the score role loads the group's queries as at most two 16-byte pieces per
+  // thread and keeps them in LDS as fp32 (within the selection's share)
+  const bool q_fits = g.G * g.D <= 2 * kAttendThreads * (16 / g.elt) &&
+                      g.G * g.D <= kTopkHistWords + kTopkSmall;
+  return q_fits && g.rtw == 1 && g.max_pages <= 5 * kAttendThreads &&
+         ppb <= 3 * (kAttendThreads / 64) * 4 && (int64_t)per_head * g.hk * g.batch <= compute_units;
+}
+
+hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window, const void* k_new,
+                              const void* v_new, const retro_kv_cache& c,
+                              const retro_selection& sel, int32_t* sel_phys, float* scores,
+                              float* o_ws, float* l_ws, int32_t* tok_out, int32_t* counters,
+                              int32_t* err, hipStream_t s) {
+  if (!sel_phys || !tok_out || !counters || !err) return hipErrorInvalidValue;
+  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
+  const TopkArgs ta{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
+                    sel.num_selected, sel_phys};
+  ScoreInArgs sc;
+  sc.q = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
+  sc.q_bstride = (int64_t)(g.W + 1) * g.hq * g.D;
+  sc.dg = c.digest;
+  sc.scores = scores;
+  sc.k_new = k_new;
+  sc.v_new = v_new;
+  sc.cnt = counters;
+  sc.err = err;
+  const int per_head = g.n_splits * g.n_rgroups;
+  sc.ppb = (g.max_pages + per_head - 1) / per_head;
+  if (g.dtype == RETRO_BF16)
+    return g.D == 128 ? attend_full_d<bf16_t, 128>(a, ta, sc, tok_out, s)
+                      : attend_full_d<bf16_t, 64>(a, ta, sc, tok_out, s);
+  return g.D == 128 ? attend_full_d<float, 128>(a, ta, sc, tok_out, s)
+                    : attend_full_d<float, 64>(a, ta, sc, tok_out, s);
 }
 
 }  // namespace retro

@@ -34,18 +34,6 @@ constexpr int score_iters(int) { return 2; }
 // most pages a workgroup scores
 constexpr int score_pages_per_block(int per) { return score_threads(per) / 64 * 4 * score_iters(per); }
 
-int compute_units() {
-  static int cus[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] <= 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cus[dev] = n;
-  }
-  return cus[dev];
-}
 
 // Workgroups per KV head and pages per workgroup of a score launch.
 void select_split(const Geometry& g, int* nbh, int* ppb) {
@@ -178,6 +166,19 @@ hipError_t score_d(const Geometry& g, int step, const void* q, int64_t qbs,
 }
 
 }  // namespace
+
+int compute_units() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
 
 bool score_selects(const Geometry& g) { return g.max_pages <= score_threads(1) * 6; }
 
