@@ -15,8 +15,8 @@ replayed back to back in the timed region.
 
 Prints one JSON line with the throughput (effective HBM GB/s of the whole step,
 algorithmic bytes / time), microseconds per layer per step, the roofline of the
-dominant kernel (the step's selection + page-gather attention kernel, timed
-alone with HIP events) and the CPU oracle's rate on a bounded sample.
+dominant kernel (the step's scores + selection + page-gather attention
+kernel, timed alone with HIP events) and the CPU oracle's rate on a bounded sample.
 """
 from __future__ import annotations
 
@@ -35,7 +35,7 @@ METRIC = "retro_step µs/layer/decode-step + effective HBM GB/s (% peak), 32K ct
 PEAK_HBM_GBS = 8000.0
 ATTEND_SRC = [os.path.join(ROOT, "paper_2508_09001_amd", "csrc", f)
               for f in ("attend.hip", "roles.h", "internal.h")]
-COUNTERS = os.path.join(ROOT, "profiles", "attend_select_kernel_llama3-8b-32k_counters.json")
+COUNTERS = os.path.join(ROOT, "profiles", "attend_full_kernel_llama3-8b-32k_counters.json")
 
 
 def _args():
@@ -46,7 +46,7 @@ def _args():
     p.add_argument("--layers", type=int, default=32, help="layer replicas rotated per step")
     p.add_argument("--config", type=int, default=1, help="workload index (1 = headline)")
     p.add_argument("--attend-reps", type=int, default=4,
-                   help="selection + attention kernel launches per layer in the roofline measurement")
+                   help="scores + selection + attention launches per layer in the roofline measurement")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="budget of the CPU oracle sample (0 skips it)")
     p.add_argument("--calib-copy", action="store_true",
@@ -60,6 +60,19 @@ def _sha(paths):
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def _step_path():
+    """The launch sequence retro_step takes at the headline shape (the environment
+    switches it reads on every call)."""
+    env = os.environ
+    if env.get("RETRO_STEP_FUSED") == "1":
+        return "single launch"
+    if env.get("RETRO_SELECT_IN_SCORE") == "1":
+        return "three launches: scores + selection, attention, combine"
+    if env.get("RETRO_SCORE_LAUNCH") == "1":
+        return "three launches: scores, selection + attention, combine"
+    return "two launches: scores + selection + attention, combine"
 
 
 def algorithmic_bytes(spec, seq_lens, num_selected):
@@ -76,8 +89,8 @@ def algorithmic_bytes(spec, seq_lens, num_selected):
     out = b * (W + 1) * hq * (d + 1) * 4
     mask = 12 * k_sum
     append = b * hk * d * elt * 2 + b * hk * 2 * d * elt * 2
-    # what the selection reads: page scores and last_loaded per (b, h), the page table per b
-    select_reads = n_pages * hk * 4 * 2 + n_pages * 4
+    # what the selection reads besides the scores: last_loaded per (b, h), the page table per b
+    select_reads = n_pages * hk * 4 + n_pages * 4
     return dict(total=digest + gather + queries + ring + out + mask + append, digest=digest,
                 gather=gather, queries=queries, ring=ring, out=out, mask=mask, append=append,
                 select_reads=select_reads)
@@ -180,15 +193,15 @@ def main():
     torch.cuda.synchronize()
     ms_eager = ev0.elapsed_time(ev1)
 
-    # ---- dominant kernel: the selection + attention kernel alone (on the page
-    # scores of the last step), graph of L * reps launches
+    # ---- dominant kernel: the step's scores + selection + attention launch
+    # alone, graph of L * reps launches
     last = t1 + args.steps - 1
     win_last = steps_in[last][0]
     ga = torch.cuda.CUDAGraph()
     with torch.cuda.graph(ga):
         for _ in range(args.attend_reps):
             for lay in layers:
-                lay.select_attend_partials(last, win_last)
+                lay.step_attend_partials(last, win_last)
     torch.cuda.synchronize()
     ev0.record()
     ga.replay()
@@ -200,7 +213,9 @@ def main():
     nbytes = algorithmic_bytes(spec, seq_mid, nsel)
     us_layer_step = ms_graph * 1000.0 / (args.steps * L)
     gbs = nbytes["total"] / (us_layer_step * 1e-6) / 1e9
-    kernel_bytes = nbytes["gather"] + nbytes["select_reads"]
+    # the dominant launch: digests -> scores -> selection -> gather, queries
+    kernel_bytes = (nbytes["digest"] + nbytes["gather"] + nbytes["queries"] +
+                    nbytes["select_reads"])
     gather_gbs = kernel_bytes / (us_attend * 1e-6) / 1e9
 
     traffic = None
@@ -228,13 +243,12 @@ def main():
                    "context": int(spec.prefill[0]), "page_size": spec.page_size,
                    "budget_tokens": spec.budget, "window": spec.window, "layers_rotated": L,
                    "launch": "hip-graph per step",
-                   "step_path": ("single launch" if os.environ.get("RETRO_STEP_FUSED") == "1"
-                                 else "three launches")},
+                   "step_path": _step_path()},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
         "bytes_per_layer_step": nbytes,
-        "roofline": {"bound": "hbm", "kernel": "attend_select_kernel",
+        "roofline": {"bound": "hbm", "kernel": "attend_full_kernel",
                      "achieved": round(gather_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gather_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
                      "bytes_per_launch": kernel_bytes, "us_per_launch": round(us_attend, 3),

@@ -199,16 +199,18 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
                                           const retro_selection* sel, void* workspace,
                                           size_t ws_bytes, void* stream);
 
-/* The selection (top-k + UpdateAndBuildMask's mask, Alg. 2) and attention pass
- * of retro_step alone, as the one kernel launch retro_step runs for them: the
- * page scores are those the last retro_step or retro_select_pages call with this
- * workspace left in it, the sequence lengths those of `cache` (no pending token).
- * Writes sel's rows, mask and count (mask values from last_loaded as it stands,
- * which this call does not update) and the splits' partials in the workspace.
- * Meant for timing the step's dominant kernel in isolation; returns
- * RETRO_EUNSUPPORTED where retro_step selects in a launch of its own
- * (max_pages > 6144). */
-retro_status retro_select_attend_partials(const retro_dims* dims, int32_t step,
+/* The kernel launch of retro_step that ends in the attention partials, alone:
+ * page scores (eq. quest_score), selection (top-k + UpdateAndBuildMask's mask,
+ * Alg. 2) and attention, with the sequence lengths of `cache` (no token is
+ * appended).  Where retro_step scores in a launch of its own (see retro_step),
+ * the launch starts from the page scores the last retro_step or
+ * retro_select_pages call with this workspace left in it.  Writes the page
+ * scores, sel's rows, mask and count (mask values from last_loaded as it
+ * stands, which this call does not update) and the splits' partials in the
+ * workspace.  Meant for timing the step's dominant kernel in isolation;
+ * returns RETRO_EUNSUPPORTED where retro_step selects outside the attention
+ * launch (max_pages > 6144). */
+retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
                                           const void* q_window, const retro_kv_cache* cache,
                                           const retro_selection* sel, void* workspace,
                                           size_t ws_bytes, void* stream);
@@ -229,12 +231,16 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
- * semantics, without materialising o_part / lse_part.  Three launches: page
- * scores (with the append); the selection in front of the attention; combine +
- * merge (with the last_loaded update and the seq_lens advance).  With
- * RETRO_SELECT_IN_SCORE=1 in the environment (read on every call), or for
- * max_pages > 6144, the selection runs at the end of the score launch (or in a
- * launch of its own) instead.
+ * semantics, without materialising o_part / lse_part.  Two launches where the
+ * attention's workgroups all fit on the GPU at once (rtw 1, max_pages <= 2560):
+ * page scores (with the append), selection and attention, the workgroups of a
+ * KV head meeting on a counter kept in `workspace` between scores and
+ * selection; then combine + merge (with the last_loaded update and the seq_lens
+ * advance).  Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read
+ * on every call), the scores take a launch of their own first; with
+ * RETRO_SELECT_IN_SCORE=1, or for max_pages > 6144, the selection runs at the
+ * end of the score launch (or in a launch of its own) instead of in front of
+ * the attention.
  * With RETRO_STEP_FUSED=1 in the environment (read on every call) the step runs
  * as one launch whose workgroups hand work to each other through counters kept
  * in `workspace` (zero-filled once, as for every call).  If a hand-off wait

@@ -20,7 +20,7 @@ RETRO_F32, RETRO_BF16 = 0, 1
 
 EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_workspace_size",
             "retro_prefill_kv", "retro_append_kv", "retro_select_pages", "retro_decode_attend",
-            "retro_decode_attend_partials", "retro_select_attend_partials",
+            "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_merge_output_cache", "retro_step")
 
 
@@ -82,7 +82,7 @@ def load_library(path: str = LIB_PATH):
                                  C.c_size_t, P], C.c_int),
         "retro_decode_attend_partials": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
                                           C.c_size_t, P], C.c_int),
-        "retro_select_attend_partials": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
+        "retro_step_attend_partials": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
                                           C.c_size_t, P], C.c_int),
         "retro_merge_output_cache": ([D, i32, P, P, C.POINTER(OutputCache), P, P, P], C.c_int),
         "retro_step": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
@@ -173,12 +173,12 @@ def retro_decode_attend_partials(dims: Dims, step: int, q_window, cache: KVCache
            "retro_decode_attend_partials")
 
 
-def retro_select_attend_partials(dims: Dims, step: int, q_window, cache: KVCache, sel: Selection,
+def retro_step_attend_partials(dims: Dims, step: int, q_window, cache: KVCache, sel: Selection,
                                  workspace, ws_bytes: int, stream=None) -> None:
-    _check(load_library().retro_select_attend_partials(C.byref(dims), step, _ptr(q_window),
+    _check(load_library().retro_step_attend_partials(C.byref(dims), step, _ptr(q_window),
                                                        C.byref(cache), C.byref(sel),
                                                        _ptr(workspace), ws_bytes, _stream(stream)),
-           "retro_select_attend_partials")
+           "retro_step_attend_partials")
 
 
 def retro_merge_output_cache(dims: Dims, step: int, o_part, lse_part, ocache: OutputCache, o_out,

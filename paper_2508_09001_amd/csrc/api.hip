@@ -242,7 +242,7 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
                                        (hipStream_t)stream));
 }
 
-retro_status retro_select_attend_partials(const retro_dims* dims, int32_t step,
+retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
                                           const void* q_window, const retro_kv_cache* cache,
                                           const retro_selection* sel, void* workspace,
                                           size_t ws_bytes, void* stream) {
@@ -254,6 +254,15 @@ retro_status retro_select_attend_partials(const retro_dims* dims, int32_t step,
   if (!retro::attend_selects(g)) return RETRO_EUNSUPPORTED;
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
   int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
+  if (retro::attend_full_supported(g, retro::compute_units())) {
+    int32_t* cnt = reinterpret_cast<int32_t*>((char*)workspace + g.ws_full);
+    int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
+    return from_hip(retro::launch_attend_full(g, step, q_window, nullptr, nullptr, *cache, *sel,
+                                              phys, ws_at(workspace, g.ws_scores),
+                                              ws_at(workspace, g.ws_opart),
+                                              ws_at(workspace, g.ws_lpart), tok, cnt, err,
+                                              (hipStream_t)stream));
+  }
   return from_hip(retro::launch_attend_select(g, step, q_window, *cache, *sel, phys,
                                               ws_at(workspace, g.ws_scores),
                                               ws_at(workspace, g.ws_opart),

@@ -110,10 +110,11 @@ class RetroLayer:
         B.retro_decode_attend_partials(self.dims, step, q_window, self.cache, self.sel,
                                        self.workspace, self.ws_bytes, stream)
 
-    def select_attend_partials(self, step: int, q_window: torch.Tensor, stream=None) -> None:
-        """The step's selection + attention kernel alone, on the page scores the last
-        step left in the workspace (overwrites the selection outputs, not last_loaded)."""
-        B.retro_select_attend_partials(self.dims, step, q_window, self.cache, self.sel,
+    def step_attend_partials(self, step: int, q_window: torch.Tensor, stream=None) -> None:
+        """The step's launch that ends in the attention partials (scores where the step
+        computes them there, selection, attention) alone; overwrites the selection
+        outputs, not last_loaded."""
+        B.retro_step_attend_partials(self.dims, step, q_window, self.cache, self.sel,
                                        self.workspace, self.ws_bytes, stream)
 
     def merge(self, step: int, stream=None) -> None:

@@ -103,10 +103,11 @@ def test_five_row_tiles_fp32():
     run_parity(spec, 40, label="edge 5 row tiles f32")
 
 
-def test_select_attend_partials_entry_point():
-    """The timing entry point of the step's selection + attention kernel, run
-    after a step on the scores that step left, selects the same pages; its mask
-    values are last_loaded as the step left it, which it does not change."""
+def test_step_attend_partials_entry_point():
+    """The timing entry point of the step's scores + selection + attention
+    launch, run after a step (same query row, the token now stored), selects
+    the same pages; its mask values are last_loaded as the step left it, which
+    it does not change."""
     import numpy as np
     import torch
     from gpu_harness import _gpu_layer
@@ -126,8 +127,8 @@ def test_select_attend_partials_entry_point():
     sel0 = layer.selected.cpu().numpy().copy()
     num0 = layer.num_selected.cpu().numpy().copy()
     A0 = layer.last_loaded.cpu().numpy().copy()
-    print(f"[entry] retro_select_attend_partials after step {t}", flush=True)
-    layer.select_attend_partials(t, layer._dev(win))
+    print(f"[entry] retro_step_attend_partials after step {t}", flush=True)
+    layer.step_attend_partials(t, layer._dev(win))
     torch.cuda.synchronize()
     assert np.array_equal(layer.num_selected.cpu().numpy(), num0)
     assert np.array_equal(layer.selected.cpu().numpy(), sel0)
