@@ -137,10 +137,11 @@ const char* retro_status_string(int32_t status);
 retro_status retro_k_max(const retro_dims* dims, int32_t* k_max);
 
 /* Bytes of scratch the select / attend / step calls need for these dims.  The
- * workspace holds, besides scratch, counters that let one launch hand work from
- * its workgroups to a last one: zero-fill it once before its first use (every
- * call leaves those counters at zero again when it completes), and let one call
- * at a time use it (calls sharing a workspace are ordered on one stream). */
+ * workspace holds, besides scratch, counters through which the workgroups of
+ * one launch hand work to each other: zero-fill it once before its first use,
+ * use it with the dims it was sized for only (one of its counters grows by a
+ * dims-dependent amount every call instead of returning to zero), and let one
+ * call at a time use it (calls sharing a workspace are ordered on one stream). */
 retro_status retro_workspace_size(const retro_dims* dims, size_t* bytes);
 
 /* Bulk-store n_tokens tokens of sequence `seq` at positions start_pos ..

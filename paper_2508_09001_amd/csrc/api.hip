@@ -98,8 +98,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
   x.ws_tok = off;  // per KV head: the step's token page when not kept (selection in attention)
   off += align256(bhs * sizeof(int32_t));
-  x.ws_full = off;  // per KV head: arrival and release counters of the one-launch attention
-  off += align256(2 * bhs * kSelCounterInts * sizeof(int32_t));
+  x.ws_full = off;  // per KV head: the arrival counter of the one-launch attention
+  off += align256(bhs * kSelCounterInts * sizeof(int32_t));
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -255,7 +255,7 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
   int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
   if (retro::attend_full_supported(g, retro::compute_units())) {
-    int32_t* cnt = reinterpret_cast<int32_t*>((char*)workspace + g.ws_full);
+    uint64_t* cnt = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_full);
     int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
     return from_hip(retro::launch_attend_full(g, step, q_window, nullptr, nullptr, *cache, *sel,
                                               phys, ws_at(workspace, g.ws_scores),
@@ -341,7 +341,7 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
     // scores (+ the token's append), selection and attention in one launch ->
     // combine + merge (+ last_loaded update, + seq_lens advance)
     int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
-    int32_t* cnt = reinterpret_cast<int32_t*>((char*)workspace + g.ws_full);
+    uint64_t* cnt = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_full);
     int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
     hipError_t e = retro::launch_attend_full(gp, step, q_window, k_new, v_new, *cache, *sel, phys,
                                              scores, o_ws, l_ws, tok, cnt, err, s);

@@ -203,7 +203,7 @@ struct ScoreInArgs {
   float* scores;      // [batch][h_k][max_pages]
   const void* k_new;  // the step's token, [batch][h_k][d]
   const void* v_new;
-  int32_t* cnt;       // per KV head: an arrival and a release counter, a line each
+  uint64_t* cnt;      // per KV head: an arrival counter, a 128-byte line each
   int32_t* err;       // set when a wait runs past its bound
   int ppb;            // pages scored per workgroup
 };
@@ -217,9 +217,14 @@ struct ScoreInArgs {
 // attend_select_kernel does.  The host launches this form only when every
 // workgroup fits on the chip at once (no more workgroups than compute units,
 // one per unit), so every wait ends; it is bounded all the same (past
-// kSpinLimit polls the error word is set and the workgroup goes on).  Each
-// workgroup then counts itself out on the release counter; the last one of a
-// head clears both for the next launch.
+// kSpinLimit polls the error word is set and the workgroup goes on).
+// The counter is never reset: it grows by the head's workgroup count every
+// launch (64 bits), and a workgroup that counts itself in as the i-th arrival
+// ever waits for the count to reach the end of i's launch, i.e. the next
+// multiple of that count.  (Every arrival of a launch precedes every arrival of
+// the next one, which starts after it ends.)  Resetting it instead would take a
+// second counter whose returning atomic kept the selection's first wavefront
+// waiting about a microsecond.
 template <typename T, int D, int PER, int SITERS>
 __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs a, TopkArgs ta,
                                                                      ScoreInArgs sc,
@@ -246,8 +251,8 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
   const bool writer = split == 0 && rg == 0;
   const int first = split * g.pages_per_split;
   const int tid = thread_index();
-  int32_t* arrive = sc.cnt + (int64_t)bh * 2 * kSelCounterInts;
-  int32_t* release = arrive + kSelCounterInts;
+  uint64_t* arrive = sc.cnt + (int64_t)bh * (kSelCounterInts / 2);
+  uint64_t target = 0;  // thread 0: the arrival count that completes this launch's head
 
   // ---- this workgroup's share of the head's page scores
   int seq_len = 0, tok_lp = -1, n_pages = 0;
@@ -275,17 +280,26 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
           tok_lp = tk.lp;
           return tk;
         });
-    block_signal(arrive);
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's score and token stores have completed
+    __syncthreads();
+    if (tid == 0) {
+      const uint64_t k = __hip_atomic_fetch_add(arrive, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      target = (k / per_head + 1) * per_head;
+    }
   }
 
   auto select = [&] {
-    block_wait(arrive, per_head, sc.err);
-    if (tid == 0 &&
-        __hip_atomic_fetch_add(release, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == per_head - 1) {
-      // every workgroup of the head is past its wait
-      __hip_atomic_store(arrive, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(release, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) {
+      int it = 0;
+      while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (++it > kSpinLimit) {
+          __hip_atomic_store(sc.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(8);  // ~0.2 us between polls
+      }
     }
+    __syncthreads();
     uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
     int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
     int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
@@ -422,7 +436,7 @@ bool attend_full_supported(const Geometry& g, int compute_units) {
 hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window, const void* k_new,
                               const void* v_new, const retro_kv_cache& c,
                               const retro_selection& sel, int32_t* sel_phys, float* scores,
-                              float* o_ws, float* l_ws, int32_t* tok_out, int32_t* counters,
+                              float* o_ws, float* l_ws, int32_t* tok_out, uint64_t* counters,
                               int32_t* err, hipStream_t s) {
   if (!sel_phys || !tok_out || !counters || !err) return hipErrorInvalidValue;
   const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);

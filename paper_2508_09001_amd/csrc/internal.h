@@ -123,15 +123,16 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
 // the workgroups of a KV head score its pages, wait for each other on a
 // per-head counter, then run launch_attend_select's work.  Only when every
 // workgroup is resident at once (attend_full_supported; rtw == 1, max_pages <=
-// 2560, at most 96 pages scored per workgroup).  counters: 2 * batch * h_k
-// lines of kSelCounterInts ints in the workspace, zero between launches; err:
-// set if a wait ran past its bound.  The combine launch after it updates
-// last_loaded as for launch_attend_select.
+// 2560, at most 96 pages scored per workgroup).  counters: batch * h_k lines
+// of kSelCounterInts ints in the workspace, zero-filled once and then only
+// grown by this launch (by the head's workgroup count each time, so always with
+// the same geometry); err: set if a wait ran past its bound.  The combine
+// launch after it updates last_loaded as for launch_attend_select.
 bool attend_full_supported(const Geometry& g, int compute_units);
 hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window, const void* k_new,
                               const void* v_new, const retro_kv_cache& c,
                               const retro_selection& sel, int32_t* sel_phys, float* scores,
-                              float* o_ws, float* l_ws, int32_t* tok_out, int32_t* counters,
+                              float* o_ws, float* l_ws, int32_t* tok_out, uint64_t* counters,
                               int32_t* err, hipStream_t s);
 int compute_units();
 hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
