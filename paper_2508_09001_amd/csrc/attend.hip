@@ -288,7 +288,9 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     }
   }
 
-  auto select = [&] {
+  // the head's arrival wait, run by the selection once its last_loaded and
+  // page-table loads are in flight and its histograms are cleared
+  auto head_wait = [&] {
     if (tid == 0) {
       int it = 0;
       while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
@@ -300,13 +302,15 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
       }
     }
     __syncthreads();
+  };
+  auto select = [&] {
     uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
     int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
     int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
     int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
     int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
     const int k = topk_core<PER, kAttendThreads / 64>(
-        ta, bh, [&] { return n_pages; }, tok_lp, hist, small, [] {},
+        ta, bh, [&] { return n_pages; }, tok_lp, hist, small, head_wait,
         [&](int pos, int p, int a_old, int phys) {
           const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
           if (pos >= first && pos < first + g.pages_per_split) {
