@@ -233,11 +233,17 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
  * semantics, without materialising o_part / lse_part.  Two launches where the
- * attention's workgroups all fit on the GPU at once (rtw 1, max_pages <= 2560):
- * page scores (with the append), selection and attention, the workgroups of a
- * KV head meeting on a counter kept in `workspace` between scores and
- * selection; then combine + merge (with the last_loaded update and the seq_lens
- * advance).  Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read
+ * attention's workgroups all fit on the GPU at once (rtw 1, max_pages <= 2560,
+ * no more workgroups than compute units): page scores (with the append),
+ * selection and attention, the workgroups of a KV head meeting on a counter
+ * kept in `workspace` between scores and selection; then combine + merge (with
+ * the last_loaded update and the seq_lens advance).  The meeting needs every
+ * workgroup of the launch resident at once: work of other streams or processes
+ * holding compute units delays it until they free them; a wait that runs past
+ * its bound (tens of milliseconds) sets a sticky word in `workspace`, and that
+ * step's outputs, and those of every later step with this workspace until it
+ * is zero-filled again, are NaN (RETRO_TEST_WAIT_TIMEOUT=1 in the environment
+ * makes every such wait give up at once, for tests of that path).  Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read
  * on every call), the scores take a launch of their own first; with
  * RETRO_SELECT_IN_SCORE=1, or for max_pages > 6144, the selection runs at the
  * end of the score launch (or in a launch of its own) instead of in front of

@@ -348,7 +348,7 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
     if (e == hipSuccess)
       e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
                                       nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
-                                      sel->selected, tok);
+                                      sel->selected, tok, err);
     return from_hip(e);
   }
   if (retro::attend_selects(gp) && !select_in_score_requested()) {

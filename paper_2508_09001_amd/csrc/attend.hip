@@ -30,6 +30,8 @@
 //
 // Output: per split and row, the normalised partial output and its natural-log
 // normaliser, combined across splits by the merge kernel.
+#include <cstdlib>
+
 #include "roles.h"
 
 namespace retro {
@@ -206,6 +208,8 @@ struct ScoreInArgs {
   uint64_t* cnt;      // per KV head: an arrival counter, a 128-byte line each
   int32_t* err;       // set when a wait runs past its bound
   int ppb;            // pages scored per workgroup
+  int spin_limit;     // polls before a wait gives up
+  uint64_t target_bias;  // added to every wait's target (a test makes waits time out with it)
 };
 
 // Page scores, the token's append, the selection and the attention in one
@@ -284,7 +288,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     __syncthreads();
     if (tid == 0) {
       const uint64_t k = __hip_atomic_fetch_add(arrive, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      target = (k / per_head + 1) * per_head;
+      target = (k / per_head + 1) * per_head + sc.target_bias;
     }
   }
 
@@ -294,7 +298,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     if (tid == 0) {
       int it = 0;
       while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-        if (++it > kSpinLimit) {
+        if (++it > sc.spin_limit) {
           __hip_atomic_store(sc.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           break;
         }
@@ -457,6 +461,12 @@ hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window,
   sc.err = err;
   const int per_head = g.n_splits * g.n_rgroups;
   sc.ppb = (g.max_pages + per_head - 1) / per_head;
+  // RETRO_TEST_WAIT_TIMEOUT=1 (tests of the failure path): every wait gives up
+  // after a few polls, its target being out of reach
+  const char* t = std::getenv("RETRO_TEST_WAIT_TIMEOUT");
+  const bool timeout = t && t[0] == '1';
+  sc.spin_limit = timeout ? 4 : kSpinLimit;
+  sc.target_bias = timeout ? (1ull << 40) : 0ull;
   if (g.dtype == RETRO_BF16)
     return g.D == 128 ? attend_full_d<bf16_t, 128>(a, ta, sc, tok_out, s)
                       : attend_full_d<bf16_t, 64>(a, ta, sc, tok_out, s);

@@ -143,13 +143,15 @@ hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, 
 // With g.token_pending and a cache, the launch also advances seq_lens past the
 // step's token (when its page is mapped).  With `selected` and `tok_upd` (from
 // launch_attend_select; num_selected and cache required), it also applies the
-// step's last_loaded update.
+// step's last_loaded update.  With `err` (mode 2), rows are written as NaN if
+// that word is set (a bounded wait of the launch before ran out).
 hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const float* o_ws,
                                 const float* l_ws, const int32_t* num_selected,
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
                                 float* lse_out, const retro_kv_cache* cache, hipStream_t s,
                                 const int32_t* selected = nullptr,
-                                const int32_t* tok_upd = nullptr);
+                                const int32_t* tok_upd = nullptr,
+                                const int32_t* err = nullptr);
 
 }  // namespace retro

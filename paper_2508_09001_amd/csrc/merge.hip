@@ -35,6 +35,26 @@ __device__ __forceinline__ void update_last_loaded(const MergeArgs& a, int bh) {
   if (lane == 0 && tok >= 0 && tok < g.max_pages) arow[tok] = a.step - 1;
 }
 
+// The rows merge unit `unit` writes (mode 2), as NaN.
+template <int D>
+__device__ void poison_unit(const MergeArgs& a, int unit) {
+  const Geometry& g = a.g;
+  int u = unit;
+  const int x = u % a.xs;
+  u /= a.xs;
+  const int gq = u % g.G;
+  u /= g.G;
+  const int h = u % g.hk, b = u / g.hk;
+  const int qh = h * g.G + gq;
+  const int64_t out_row = (int64_t)b * (g.W + 1);
+  Row<D> p;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) p.o[e] = __builtin_nanf("");
+  p.z = __builtin_nanf("");
+  put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, p);
+  if (x == 0 && g.W > 0) put<D>(a.o_out, a.l_out, (out_row + g.W) * g.hq + qh, p);
+}
+
 template <int D>
 __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
   // units ordered (sequence, KV head, query head of the group, row slot), spread
@@ -51,7 +71,9 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   }
   const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
+  const bool failed = a.err && *a.err != 0;
   merge_unit<D, 32>(a, u);
+  if (failed && a.mode == 2) poison_unit<D>(a, u);
   if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
     // after the unit's own loads (the two lookups here are dependent): the
     // first wavefront advances every sequence; no other workgroup of this
@@ -90,6 +112,7 @@ MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_
   a.a_upd = nullptr;
   a.sel_upd = nullptr;
   a.tok_upd = nullptr;
+  a.err = nullptr;
   return a;
 }
 
@@ -98,13 +121,15 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
                                 const float* o_part, const float* l_part, float* o_part_out,
                                 float* l_part_out, const retro_output_cache* oc, float* o_out,
                                 float* lse_out, const retro_kv_cache* cache, hipStream_t s,
-                                const int32_t* selected, const int32_t* tok_upd) {
+                                const int32_t* selected, const int32_t* tok_upd,
+                                const int32_t* err) {
   MergeArgs a = make_merge_args(g, step, mode, o_ws, l_ws, num_selected, o_part, l_part,
                                 o_part_out, l_part_out, oc, o_out, lse_out);
   if (cache) {
     a.seq_lens = cache->seq_lens;
     a.pt = cache->page_table;
   }
+  a.err = err;
   int64_t upd_blocks = 0;
   if (selected && tok_upd) {
     if (!cache || !num_selected) return hipErrorInvalidValue;

@@ -1219,6 +1219,9 @@ struct MergeArgs {
   int32_t* a_upd;
   const int32_t* sel_upd;
   const int32_t* tok_upd;
+  // sticky error word of the launch that produced the partials (a bounded wait
+  // ran out there), or null: when set, the rows are written as NaN
+  const int32_t* err;
 };
 
 template <int D>

@@ -140,3 +140,35 @@ def test_step_attend_partials_entry_point():
             k = int(num0[b, h])
             want[b, h, :k] = A0[b, h, sel0[b, h, :k]]
     assert np.array_equal(msk, want)
+
+
+def test_attention_wait_timeout_gives_nan_outputs(monkeypatch):
+    """Failure path of the two-launch step, forced from the host: every
+    per-head wait of the attention launch is made to give up after a few polls
+    (its target out of reach), so every workgroup still runs to its end; the
+    step's outputs must then be NaN, and stay NaN for the next step with that
+    workspace (the error word is sticky), whose waits are normal again."""
+    import numpy as np
+    import torch
+    from gpu_harness import _gpu_layer
+    spec = W.config(0)
+    gen = W.Generator(spec)
+    layer = _gpu_layer(spec, None)
+    for b, (k, v) in enumerate(gen.prefill()):
+        layer.prefill(b, k, v)
+    qw = W.QueryWindow(spec)
+    for t in range(3):
+        k_new, v_new, q = gen.step(t)
+        win = qw.push(q).copy()
+        if t == 1:
+            monkeypatch.setenv("RETRO_TEST_WAIT_TIMEOUT", "1")
+        print(f"[timeout] step {t} forced={t == 1}", flush=True)
+        layer.step(t, win, k_new[-1], v_new[-1])
+        monkeypatch.delenv("RETRO_TEST_WAIT_TIMEOUT", raising=False)
+        torch.cuda.synchronize()
+        o = layer.o_out.cpu().numpy()
+        z = layer.lse_out.cpu().numpy()
+        if t == 0:
+            assert np.isfinite(o).all() and not np.isnan(z).any()
+        else:
+            assert np.isnan(o).all() and np.isnan(z).all()
