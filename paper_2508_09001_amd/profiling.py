@@ -1,9 +1,12 @@
 """Summaries of rocprofv3 output for the library's kernels.
 
-    python -m paper_2508_09001_amd.profiling stats <dir>
+    python -m paper_2508_09001_amd.profiling stats <dir> [--last N --kernel S]
         per-kernel dispatch count and duration (avg/min/max/total, microseconds)
         from a `rocprofv3 --kernel-trace --stats` output directory (CSV or the
-        SQLite database rocprofv3 writes by default).
+        SQLite database rocprofv3 writes by default); with --last, also the
+        average duration of the last N dispatches (by start time) of the kernels
+        whose name contains S (bench.py ends with a graph of launches of its
+        dominant kernel alone).
 
     python -m paper_2508_09001_amd.profiling traffic --kernel attend_kernel \\
         --fetch <dir> --write <dir> --calib-fetch <dir> --calib-write <dir> \\
@@ -86,6 +89,22 @@ def stats_table(out_dir: str) -> str:
     return "\n".join(lines)
 
 
+def last_dispatches_avg(out_dir: str, kernel_substr: str, n: int) -> tuple:
+    """(count, average duration in us) of the last n dispatches, by start time,
+    of the kernels whose name contains kernel_substr (CSV kernel trace)."""
+    spans = []
+    for path in glob.glob(os.path.join(out_dir, "**", "*kernel_trace.csv"), recursive=True):
+        with open(path, newline="") as f:
+            for row in csv.DictReader(f):
+                if kernel_substr in row["Kernel_Name"]:
+                    spans.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"])))
+    spans.sort()
+    last = spans[-n:] if n > 0 else []
+    if not last:
+        return 0, float("nan")
+    return len(last), sum(e - s for s, e in last) / len(last) / 1e3
+
+
 def counter_per_dispatch(out_dir: str, counter: str, kernel_substr: str) -> list:
     """Values of `counter` (summed over its instances) for every dispatch whose
     kernel name contains `kernel_substr`."""
@@ -141,6 +160,8 @@ def main(argv=None):
     sub = p.add_subparsers(dest="cmd", required=True)
     s = sub.add_parser("stats")
     s.add_argument("dir")
+    s.add_argument("--last", type=int, default=0)
+    s.add_argument("--kernel", default="")
     t = sub.add_parser("traffic")
     t.add_argument("--kernel", required=True)
     t.add_argument("--fetch", required=True)
@@ -154,6 +175,9 @@ def main(argv=None):
     a = p.parse_args(argv)
     if a.cmd == "stats":
         print(stats_table(a.dir))
+        if a.last > 0:
+            n, avg = last_dispatches_avg(a.dir, a.kernel, a.last)
+            print(f"\nlast {n} dispatches of {a.kernel}: {avg:.2f} us average")
         return
     res = traffic(a)
     text = json.dumps(res, indent=1)

@@ -42,6 +42,16 @@ def test_stats_table(tmp_path):
     assert "| 1 | 0.50 |" in lines[3]
 
 
+def test_last_dispatches_average(tmp_path):
+    hdr = ["Kernel_Name", "Start_Timestamp", "End_Timestamp"]
+    _write(str(tmp_path / "s" / "run_kernel_trace.csv"), hdr,
+           [[NAME, 50000, 54000], [NAME, 1000, 11000], [COPY, 0, 500], [NAME, 60000, 62000]])
+    n, avg = profiling.last_dispatches_avg(str(tmp_path / "s"), "attend_kernel", 2)
+    assert n == 2 and avg == pytest.approx(3.0)   # the two latest: 4 us and 2 us
+    n, avg = profiling.last_dispatches_avg(str(tmp_path / "s"), "attend_kernel", 10)
+    assert n == 3 and avg == pytest.approx(16.0 / 3)
+
+
 def test_traffic_scaling(tmp_path):
     # the kernel's counters are per dispatch, summed over counter instances; the
     # calibration copy of N bytes reports N/2 KiB for FETCH_SIZE, N KiB for WRITE_SIZE
