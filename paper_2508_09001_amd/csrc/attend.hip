@@ -79,6 +79,60 @@ hipError_t attend_d(const AttendArgs& a, hipStream_t s) {
   return a.g.rtw == 1 ? attend_t<T, D, 1>(a, s) : attend_t<T, D, 2>(a, s);
 }
 
+// The selection of KV head bh as every attention workgroup of the head runs it
+// (topk_core over the head's scores, the same result in each): slots [first,
+// first + pages_per_split) of the kept pages go to l_lp / l_m / l_ph (logical
+// page, mask value, physical page) and the count to *s_k; the `writer`
+// workgroup also writes the selection rows (-1 past the count), the count, and
+// tok_out[bh] = the step token's page if it is not kept, else -1.  Ends with a
+// barrier.  pages_of / tok_lp / wait as for topk_core.
+template <int PER, typename PagesOf, typename Wait>
+__device__ __forceinline__ void select_for_split(const TopkArgs& ta, int bh, int first, bool writer,
+                                                 PagesOf&& pages_of, const int& tok_lp,
+                                                 Wait&& wait, char* lds,
+                                                 int (&l_lp)[kMaxSplitPages],
+                                                 int (&l_m)[kMaxSplitPages],
+                                                 int (&l_ph)[kMaxSplitPages], int& s_k,
+                                                 int32_t* tok_out) {
+  const Geometry& g = ta.g;
+  const int tid = thread_index();
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
+  int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
+  int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
+  int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
+  int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
+  const int k = topk_core<PER, kAttendThreads / 64>(
+      ta, bh, pages_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
+        const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
+        if (pos >= first && pos < first + g.pages_per_split) {
+          l_lp[pos - first] = p;
+          l_m[pos - first] = a_old;
+          l_ph[pos - first] = ph;
+        }
+        if (writer) {
+          if (pos >= 0) {
+            sel_row[pos] = p;
+            m_row[pos] = a_old;
+            ph_row[pos] = ph;
+          }
+          if (p == tok_lp) tok_out[bh] = pos < 0 ? p : -1;
+        }
+      });
+  if (writer) {
+    for (int i = k + tid; i < g.k_max; i += kAttendThreads) {
+      sel_row[i] = -1;
+      m_row[i] = -1;
+      ph_row[i] = -1;
+    }
+    if (tid == 0) {
+      ta.num_selected[bh] = k;
+      if (tok_lp < 0) tok_out[bh] = -1;
+    }
+  }
+  if (tid == 0) s_k = k;
+  __syncthreads();  // the split's page list and the count are in LDS
+}
+
 // Attention with the page selection in front: every workgroup of a KV head
 // runs the head's top-k (the same computation on the same scores, so the same
 // result) and takes its split's slots of the selection from LDS, instead of
@@ -112,16 +166,10 @@ __global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArg
   const int bh = b * g.hk + h;
   const bool writer = split == 0 && rg == 0;
   const int first = split * g.pages_per_split;
-  const int tid = thread_index();
   int seq_len = 0, tok_lp = -1;
   auto select = [&] {
-    uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
-    int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-    int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
-    int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
-    int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
-    const int k = topk_core<PER, kAttendThreads / 64>(
-        ta, bh,
+    select_for_split<PER>(
+        ta, bh, first, writer,
         [&] {
           const int pos = a.seq_lens[b];
           seq_len = pos;
@@ -132,36 +180,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArg
           }
           return min((seq_len + g.P - 1) / g.P, g.max_pages);
         },
-        tok_lp, hist, small, [] {},
-        [&](int pos, int p, int a_old, int phys) {
-          const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
-          if (pos >= first && pos < first + g.pages_per_split) {
-            l_lp[pos - first] = p;
-            l_m[pos - first] = a_old;
-            l_ph[pos - first] = ph;
-          }
-          if (writer) {
-            if (pos >= 0) {
-              sel_row[pos] = p;
-              m_row[pos] = a_old;
-              ph_row[pos] = ph;
-            }
-            if (p == tok_lp) tok_out[bh] = pos < 0 ? p : -1;
-          }
-        });
-    if (writer) {
-      for (int i = k + tid; i < g.k_max; i += kAttendThreads) {
-        sel_row[i] = -1;
-        m_row[i] = -1;
-        ph_row[i] = -1;
-      }
-      if (tid == 0) {
-        ta.num_selected[bh] = k;
-        if (tok_lp < 0) tok_out[bh] = -1;
-      }
-    }
-    if (tid == 0) s_k = k;
-    __syncthreads();  // the split's page list and the count are in LDS
+        tok_lp, [] {}, lds, l_lp, l_m, l_ph, s_k, tok_out);
   };
   attend_role<T, D, RTW, MAXP, RTW == 1, false>(
       a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
@@ -308,42 +327,8 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     __syncthreads();
   };
   auto select = [&] {
-    uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
-    int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-    int32_t* sel_row = ta.selected + (int64_t)bh * g.k_max;
-    int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
-    int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
-    const int k = topk_core<PER, kAttendThreads / 64>(
-        ta, bh, [&] { return n_pages; }, tok_lp, hist, small, head_wait,
-        [&](int pos, int p, int a_old, int phys) {
-          const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
-          if (pos >= first && pos < first + g.pages_per_split) {
-            l_lp[pos - first] = p;
-            l_m[pos - first] = a_old;
-            l_ph[pos - first] = ph;
-          }
-          if (writer) {
-            if (pos >= 0) {
-              sel_row[pos] = p;
-              m_row[pos] = a_old;
-              ph_row[pos] = ph;
-            }
-            if (p == tok_lp) tok_out[bh] = pos < 0 ? p : -1;
-          }
-        });
-    if (writer) {
-      for (int i = k + tid; i < g.k_max; i += kAttendThreads) {
-        sel_row[i] = -1;
-        m_row[i] = -1;
-        ph_row[i] = -1;
-      }
-      if (tid == 0) {
-        ta.num_selected[bh] = k;
-        if (tok_lp < 0) tok_out[bh] = -1;
-      }
-    }
-    if (tid == 0) s_k = k;
-    __syncthreads();  // the split's page list and the count are in LDS
+    select_for_split<PER>(ta, bh, first, writer, [&] { return n_pages; }, tok_lp, head_wait,
+                          lds, l_lp, l_m, l_ph, s_k, tok_out);
   };
   attend_role<T, D, 1, MAXP, true, false>(
       a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
