@@ -242,12 +242,14 @@ struct ScoreInArgs {
 // one per unit), so every wait ends; it is bounded all the same (past
 // kSpinLimit polls the error word is set and the workgroup goes on).
 // The counter is never reset: it grows by the head's workgroup count every
-// launch (64 bits), and a workgroup that counts itself in as the i-th arrival
-// ever waits for the count to reach the end of i's launch, i.e. the next
-// multiple of that count.  (Every arrival of a launch precedes every arrival of
-// the next one, which starts after it ends.)  Resetting it instead would take a
-// second counter whose returning atomic kept the selection's first wavefront
-// waiting about a microsecond.
+// launch (64 bits).  Every arrival of a launch precedes every arrival of the
+// next one, which starts after it ends, so a count read by a workgroup of the
+// launch before it counts itself in lies in [n * c, n * c + c - 1] (c: the
+// head's workgroups, n: the launches before) and the workgroup waits for the
+// next multiple of c.  Reading it at the start takes the round trip of a
+// returning atomic off the path of the head's last arrival; resetting the
+// counter instead would take a second counter whose returning atomic kept the
+// selection's first wavefront waiting about a microsecond.
 template <typename T, int D, int PER, int SITERS>
 __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs a, TopkArgs ta,
                                                                      ScoreInArgs sc,
@@ -275,7 +277,10 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
   const int first = split * g.pages_per_split;
   const int tid = thread_index();
   uint64_t* arrive = sc.cnt + (int64_t)bh * (kSelCounterInts / 2);
-  uint64_t target = 0;  // thread 0: the arrival count that completes this launch's head
+  // thread 0: the head's arrival count before this workgroup counts itself in,
+  // read now so that counting in needs no returning atomic (see below)
+  uint64_t before = 0, target = 0;
+  if (tid == 0) before = __hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
   // ---- this workgroup's share of the head's page scores
   int seq_len = 0, tok_lp = -1, n_pages = 0;
@@ -306,8 +311,8 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     __builtin_amdgcn_s_waitcnt(0);  // this wavefront's score and token stores have completed
     __syncthreads();
     if (tid == 0) {
-      const uint64_t k = __hip_atomic_fetch_add(arrive, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      target = (k / per_head + 1) * per_head + sc.target_bias;
+      __hip_atomic_fetch_add(arrive, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      target = (before / per_head + 1) * per_head + sc.target_bias;
     }
   }
 
