@@ -1,7 +1,7 @@
 /*
  * retro.h — C ABI of an MI355X (gfx950) library for one decode step of
  * retrospective sparse attention ("Retrospective Sparse Attention for
- * Efficient Long-Context Generation", Alg. 1 without its UpdateKV line).
+ * Efficient Long-Context Generation", Alg. 1 without its UpdateKV step).
  *
  * One step of one attention layer, for a batch of sequences:
  *   1. append the step's key/value to a paged KV cache and keep per-page key
@@ -156,7 +156,7 @@ retro_status retro_prefill_kv(const retro_dims* dims, const retro_kv_cache* cach
 /* AppendKV (Alg. 1) of one token per sequence (k_new, v_new: [batch][h_k][d] dtype)
  * at position seq_lens[b], which is then incremented.  The page's digest widens to
  * the new key (or starts at it for the page's first slot), and last_loaded of that
- * page is set to step-1 for every head: the first line of Alg. 2, applied when a
+ * page is set to step-1 for every head: Alg. 2's current-page rule, applied when a
  * page receives a key newer than every past query.  May be called several times
  * per step (several tokens per step).  A token whose logical page is not mapped
  * (page_table entry < 0 or >= num_phys_pages, or position >= max_pages*P) is

@@ -186,7 +186,7 @@ class Oracle:
                               _p(self.lse_cache), _p(o_out), _p(z_out))
         return o_out, z_out
 
-    # -- one decode step (Alg. 1 without its UpdateKV line) ----------------------
+    # -- one decode step (Alg. 1 without its UpdateKV step) ----------------------
     def step(self, t: int, k_new: np.ndarray, v_new: np.ndarray, q_window: np.ndarray,
              attend: bool = True) -> Dict[str, np.ndarray]:
         """k_new, v_new: [T][batch][h_k][d] (T tokens appended this step, the query

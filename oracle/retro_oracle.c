@@ -12,7 +12,7 @@
  *   - page score:   eq. (quest_score), evaluated in fp32 in one fixed order
  *                   (see oracle_score) so that a selection is reproducible;
  *   - page select:  the k best pages, ties to the lower page index;
- *   - mask:         Alg. 2 (UpdateAndBuildMask), with its first line applied
+ *   - mask:         Alg. 2 (UpdateAndBuildMask), with its current-page rule applied
  *                   to every page written during the step (oracle_append);
  *   - attention:    eq. (update-org) for the current query and
  *                   eq. (update-sup) for the past queries of the window,
@@ -111,7 +111,7 @@ int oracle_prefill(const oracle_dims* g, int32_t b, int32_t n, int32_t* seq_lens
 
 /* AppendKV (Alg. 1) for one token per sequence (k_new, v_new: [batch][h_k][d]).
  * The page that receives the token then holds a key newer than every past query
- * of the window, so Alg. 2's first line, A[p_curr] <- t - 1, is applied to it
+ * of the window, so Alg. 2's current-page rule, A[p_curr] <- t - 1, is applied to it
  * here, at the moment it is written (for every head).  When a step appends
  * several tokens each written page gets the same treatment, which is what keeps
  * past queries away from any page holding a key newer than themselves. */
@@ -232,7 +232,7 @@ void oracle_select(const oracle_dims* g, const float* scores, const int32_t* seq
 /* ---------------------------------------------------------------------------
  * UpdateAndBuildMask (Alg. 2), one KV head at a time: for every selected page,
  * in order, M gets the step in which the page was last loaded and A records the
- * current step.  (Its first line, the override of the current page, happens at
+ * current step.  (Its current-page rule, the override of the current page, happens at
  * append time, see oracle_append.)  Padding entries of M are -1.
  * ------------------------------------------------------------------------- */
 void oracle_build_mask(const oracle_dims* g, int32_t step, const int32_t* selected,

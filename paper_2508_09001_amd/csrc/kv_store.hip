@@ -1,6 +1,6 @@
 // KV storage: AppendKV (Alg. 1) and bulk prefill, keeping the Quest page digests
 // (element-wise key min / max of each page, Sec. 2.1) and, on append, the
-// retrospective-mask override of Alg. 2's first line.
+// retrospective-mask override of Alg. 2's current-page rule.
 #include "internal.h"
 
 namespace retro {

@@ -226,7 +226,7 @@ __device__ __forceinline__ void f32_to_words(const float* in, uint32_t* w) {
 }
 
 // The step's own token, appended by the score block whose pages include it:
-// AppendKV and the digest update.  Alg. 2's first line (last_loaded of the
+// AppendKV and the digest update.  Alg. 2's current-page rule (last_loaded of the
 // token's page = step - 1) is applied by the selection (topk_role), which owns
 // every last_loaded write of the step.
 template <typename T>
@@ -454,7 +454,7 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 // sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
 // loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by
 // this step's token (-1: none), read after `pages_of()` (which may set it):
-// Alg. 2's first line applies to it, so its last_loaded entry is taken as
+// Alg. 2's current-page rule applies to it, so its last_loaded entry is taken as
 // step - 1.  `pages_of()` gives n, the pages of the sequence; it is called once
 // the loads are issued.  hist: kTopkHistWords
 // uint32 of LDS; small: kTopkSmall ints of LDS.

@@ -1,5 +1,5 @@
 // The whole decode step in one launch: AppendKV + page scores, top-k + mask,
-// attention, combine + merge (Alg. 1 without its UpdateKV line).
+// attention, combine + merge (Alg. 1 without its UpdateKV step).
 //
 // Each KV head of the batch (bh = b * h_k + h) belongs to lane bh mod 8.  A lane
 // has its own ticket counter; the workgroups with blockIdx mod 8 == lane (those

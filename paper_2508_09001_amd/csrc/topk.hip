@@ -34,7 +34,7 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
   __shared__ int small[kTopkSmall];
   const int bh = blockIdx.x;
   const int b = bh / ta.g.hk;
-  // a pending token (Geometry::token_pending) gets Alg. 2's first line here
+  // a pending token (Geometry::token_pending) gets Alg. 2's current-page rule here
   int tok_lp = -1;
   if (ta.g.token_pending) {
     const int pos = seq_lens[b];

@@ -7,7 +7,7 @@ from eq. (update-sup), which pages a past query may still attend:
     eligible(t, tau) = S_t  minus  (S_tau u ... u S_{t-1})
                        minus  { p : p holds a key newer than tau's query }
 
-(the last term is the causality rule that Alg. 2's first line enforces), and,
+(the last term is the causality rule that Alg. 2's current-page rule enforces), and,
 for brute force, the set of token positions each query has attended so far.
 """
 from __future__ import annotations
