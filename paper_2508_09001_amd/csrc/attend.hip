@@ -250,7 +250,7 @@ struct ScoreInArgs {
 // returning atomic off the path of the head's last arrival; resetting the
 // counter instead would take a second counter whose returning atomic kept the
 // selection's first wavefront waiting about a microsecond.
-template <typename T, int D, int PER, int SITERS>
+template <typename T, int D, int PER, int SITERS, int GC>
 __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs a, TopkArgs ta,
                                                                      ScoreInArgs sc,
                                                                      int32_t* tok_out) {
@@ -287,7 +287,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
   {
     const int page0 = (rg * g.n_splits + split) * sc.ppb;
     const int page_end = min(page0 + sc.ppb, g.max_pages);
-    score_role<T, D, SITERS, true>(
+    score_role<T, D, SITERS, true, GC>(
         g, page0, page_end,
         reinterpret_cast<const T*>(sc.q) + b * sc.q_bstride + (int64_t)h * g.G * D,
         reinterpret_cast<T*>(sc.dg) + (int64_t)bh * g.max_pages * 2 * D,
@@ -355,7 +355,11 @@ hipError_t attend_full_p(const AttendArgs& a, const TopkArgs& ta, const ScoreInA
   if (64 * g.waves != kAttendThreads || g.rtw != 1 || g.max_pages > PER * kAttendThreads ||
       sc.ppb < 1 || sc.ppb > 3 * (kAttendThreads / 64) * 4)
     return hipErrorInvalidValue;
-  attend_full_kernel<T, D, PER, 3><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
+  // the headline group size (4 query heads per KV head) gets an unrolled score loop
+  if (g.G == 4)
+    attend_full_kernel<T, D, PER, 3, 4><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
+  else
+    attend_full_kernel<T, D, PER, 3, 0><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
   return hipGetLastError();
 }
 
