@@ -212,9 +212,9 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
  * returns RETRO_EUNSUPPORTED where retro_step selects outside the attention
  * launch (max_pages > 6144). */
 retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
-                                          const void* q_window, const retro_kv_cache* cache,
-                                          const retro_selection* sel, void* workspace,
-                                          size_t ws_bytes, void* stream);
+                                        const void* q_window, const retro_kv_cache* cache,
+                                        const retro_selection* sel, void* workspace,
+                                        size_t ws_bytes, void* stream);
 
 /* MergeOutput + CacheOutput (Alg. 1; eq. merged_attn_general) for step t.
  * For each query head and row r with tau = t-W+r >= 0:
@@ -243,8 +243,9 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
  * its bound (tens of milliseconds) sets a sticky word in `workspace`, and that
  * step's outputs, and those of every later step with this workspace until it
  * is zero-filled again, are NaN (RETRO_TEST_WAIT_TIMEOUT=1 in the environment
- * makes every such wait give up at once, for tests of that path).  Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read
- * on every call), the scores take a launch of their own first; with
+ * makes every such wait give up at once, for tests of that path).
+ * Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read on every
+ * call), the scores take a launch of their own first; with
  * RETRO_SELECT_IN_SCORE=1, or for max_pages > 6144, the selection runs at the
  * end of the score launch (or in a launch of its own) instead of in front of
  * the attention.

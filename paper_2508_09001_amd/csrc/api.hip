@@ -243,9 +243,9 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
 }
 
 retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
-                                          const void* q_window, const retro_kv_cache* cache,
-                                          const retro_selection* sel, void* workspace,
-                                          size_t ws_bytes, void* stream) {
+                                        const void* q_window, const retro_kv_cache* cache,
+                                        const retro_selection* sel, void* workspace,
+                                        size_t ws_bytes, void* stream) {
   Geometry g;
   retro_status st = prepare(dims, step, &g);
   if (st != RETRO_OK) return st;
