@@ -60,19 +60,24 @@ typedef enum { RETRO_F32 = 0, RETRO_BF16 = 1 } retro_dtype;
 
 /* Problem statement of one layer.  Supported: head_dim 64 or 128; page_size
  * 16 or 32; 1 <= group <= 16; 0 <= window <= 64; (window+1)*group <= 1024;
- * page_size <= budget_tokens; max_pages <= 16384. */
+ * page_size <= budget_tokens; 0 <= budget_permille <= 1000; max_pages <= 16384. */
 typedef struct retro_dims {
   int32_t batch;           /* sequences in the batch                                   */
   int32_t num_kv_heads;    /* h_k                                                      */
   int32_t group;           /* G query heads per KV head; h_q = h_k * G (GQA)            */
   int32_t head_dim;        /* d                                                        */
   int32_t page_size;       /* P tokens per page                                        */
-  int32_t budget_tokens;   /* B; each step keeps k = min(B / P, pages of the sequence) */
+  int32_t budget_tokens;   /* B; each step keeps k = min(B_t / P, pages of the sequence) */
   int32_t window;          /* W past queries revisited per step                        */
   int32_t max_pages;       /* length of a page-table row (logical pages per sequence)  */
   int32_t num_phys_pages;  /* physical pages in k_cache / v_cache / digest             */
   int32_t dtype;           /* retro_dtype of queries, keys, values and digests         */
   float sm_scale;          /* softmax scale applied to q.k; 0 selects 1/sqrt(d)         */
+  int32_t budget_permille; /* relative budget (Sec. 4 ablation; Table 1's setting of
+                              0.15 = 150): B_t = max(B, floor(L * budget_permille /
+                              1000)) tokens for a sequence of L tokens (the step's
+                              token included); 0: B_t = B.  k_max covers the largest
+                              B_t of a full page-table row.                          */
 } retro_dims;
 
 /* The paged KV cache of one layer (Sec. 2.1; pages as in a vLLM-style pool).

@@ -36,7 +36,8 @@ def build(force: bool = True) -> str:
 class _Dims(C.Structure):
     _fields_ = [("batch", C.c_int32), ("num_kv_heads", C.c_int32), ("group", C.c_int32),
                 ("head_dim", C.c_int32), ("page_size", C.c_int32), ("budget", C.c_int32),
-                ("window", C.c_int32), ("max_tokens", C.c_int32), ("sm_scale", C.c_double)]
+                ("window", C.c_int32), ("max_tokens", C.c_int32), ("sm_scale", C.c_double),
+                ("budget_permille", C.c_int32)]
 
 
 _lib = None
@@ -101,12 +102,12 @@ class Oracle:
 
     def __init__(self, batch: int, num_kv_heads: int, group: int, head_dim: int,
                  page_size: int, budget: int, window: int, max_tokens: int,
-                 sm_scale: Optional[float] = None):
+                 sm_scale: Optional[float] = None, budget_permille: int = 0):
         self.lib = _load()
         if sm_scale is None:
             sm_scale = float(np.float32(1.0 / np.sqrt(head_dim)))
         self.dims = _Dims(batch, num_kv_heads, group, head_dim, page_size, budget, window,
-                          max_tokens, sm_scale)
+                          max_tokens, sm_scale, budget_permille)
         self._d = C.byref(self.dims)
         self.batch, self.hk, self.G, self.d = batch, num_kv_heads, group, head_dim
         self.P, self.W, self.max_tokens = page_size, window, max_tokens
@@ -127,7 +128,8 @@ class Oracle:
     def for_spec(cls, spec, sm_scale: Optional[float] = None, **over) -> "Oracle":
         kw = dict(batch=spec.batch, num_kv_heads=spec.num_kv_heads, group=spec.group,
                   head_dim=spec.head_dim, page_size=spec.page_size, budget=spec.budget,
-                  window=spec.window, max_tokens=spec.max_tokens, sm_scale=sm_scale)
+                  window=spec.window, max_tokens=spec.max_tokens, sm_scale=sm_scale,
+                  budget_permille=spec.budget_permille)
         kw.update(over)
         return cls(**kw)
 

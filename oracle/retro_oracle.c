@@ -36,7 +36,8 @@
  *   o_part/out  [batch][W+1][h_q][d]          double
  *   lse_*       [batch][W+1][h_q]             double (natural log)
  * with h_q = h_k * group, max_pages = ceil(max_tokens / P) and
- * k_max = min(budget / P, max_pages).
+ * k_max = min(B_max / P, max_pages), B_max the budget of a sequence of
+ * max_pages * P tokens (see budget_tokens_at).
  */
 #include <math.h>
 #include <stdint.h>
@@ -53,15 +54,29 @@ typedef struct {
   int32_t window;
   int32_t max_tokens;
   double sm_scale;
+  int32_t budget_permille; /* relative budget in thousandths; 0: the fixed budget */
 } oracle_dims;
 
 static int64_t max_pages_of(const oracle_dims* g) {
   return (g->max_tokens + g->page_size - 1) / g->page_size;
 }
 
+/* The token budget of a step whose sequence holds len tokens (the step's own
+ * token included): the fixed budget B, or with a relative budget (Sec. 4,
+ * ablation; the setting of Table 1) len times the fraction, rounded down, but
+ * at least B. */
+static int64_t budget_tokens_at(const oracle_dims* g, int64_t len) {
+  int64_t b = g->budget;
+  if (g->budget_permille > 0) {
+    const int64_t rel = len * g->budget_permille / 1000;
+    if (rel > b) b = rel;
+  }
+  return b;
+}
+
 int32_t oracle_k_max(const oracle_dims* g) {
-  int64_t k = g->budget / g->page_size;
   int64_t mp = max_pages_of(g);
+  int64_t k = budget_tokens_at(g, mp * g->page_size) / g->page_size;
   return (int32_t)(k < mp ? k : mp);
 }
 
@@ -181,7 +196,7 @@ void oracle_score(const oracle_dims* g, const float* q_cur, const float* kmin,
 }
 
 /* ---------------------------------------------------------------------------
- * PageSelect (Alg. 1): keep the k = min(budget / P, n_pages) best pages of the
+ * PageSelect (Alg. 1): keep the k = min(B_t / P, n_pages) best pages of the
  * current query, ordered by (score descending, page index ascending); emit them
  * in ascending page order, padding the row with -1.
  * ------------------------------------------------------------------------- */
@@ -212,7 +227,9 @@ void oracle_select(const oracle_dims* g, const float* scores, const int32_t* seq
   for (int b = 0; b < g->batch; ++b) {
     for (int h = 0; h < hk; ++h) {
       const int n = (seq_lens[b] + P - 1) / P;
-      const int k = kmax < n ? kmax : n;
+      const int64_t kb = budget_tokens_at(g, seq_lens[b]) / P;
+      int k = kb < n ? (int)kb : n;
+      if (k > kmax) k = kmax;
       scored_page* all = (scored_page*)malloc(sizeof(scored_page) * (n > 0 ? n : 1));
       for (int p = 0; p < n; ++p) {
         all[p].s = scores[((int64_t)b * hk + h) * mp + p];

@@ -34,7 +34,7 @@ class Dims(C.Structure):
     _fields_ = [("batch", C.c_int32), ("num_kv_heads", C.c_int32), ("group", C.c_int32),
                 ("head_dim", C.c_int32), ("page_size", C.c_int32), ("budget_tokens", C.c_int32),
                 ("window", C.c_int32), ("max_pages", C.c_int32), ("num_phys_pages", C.c_int32),
-                ("dtype", C.c_int32), ("sm_scale", C.c_float)]
+                ("dtype", C.c_int32), ("sm_scale", C.c_float), ("budget_permille", C.c_int32)]
 
 
 class KVCache(C.Structure):

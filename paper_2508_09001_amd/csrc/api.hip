@@ -33,6 +33,7 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   if (d->group > 16 || d->window > 64) return RETRO_EUNSUPPORTED;
   if ((int64_t)(d->window + 1) * d->group > 1024) return RETRO_EUNSUPPORTED;
   if (d->budget_tokens < d->page_size) return RETRO_EINVAL;
+  if (d->budget_permille < 0 || d->budget_permille > 1000) return RETRO_EINVAL;
   if (d->max_pages > 16384) return RETRO_EUNSUPPORTED;
   if ((int64_t)d->batch * d->num_kv_heads > 65535) return RETRO_EUNSUPPORTED;
 
@@ -50,7 +51,14 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.num_phys = d->num_phys_pages;
   x.dtype = d->dtype;
   x.elt = d->dtype == RETRO_BF16 ? 2 : 4;
-  x.k_max = std::min(d->budget_tokens / d->page_size, d->max_pages);
+  x.budget_permille = d->budget_permille;
+  {
+    // the largest budget of any step: that of a full page-table row
+    int64_t bt = d->budget_tokens;
+    if (d->budget_permille > 0)
+      bt = std::max<int64_t>(bt, (int64_t)d->max_pages * d->page_size * d->budget_permille / 1000);
+    x.k_max = (int)std::min<int64_t>(bt / d->page_size, d->max_pages);
+  }
   x.sm_scale = d->sm_scale > 0.f ? d->sm_scale : 1.0f / sqrtf((float)d->head_dim);
 
   x.chunk_pages = 32 / x.P;

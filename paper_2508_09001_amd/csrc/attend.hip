@@ -85,10 +85,10 @@ hipError_t attend_d(const AttendArgs& a, hipStream_t s) {
 // page, mask value, physical page) and the count to *s_k; the `writer`
 // workgroup also writes the selection rows (-1 past the count), the count, and
 // tok_out[bh] = the step token's page if it is not kept, else -1.  Ends with a
-// barrier.  pages_of / tok_lp / wait as for topk_core.
-template <int PER, typename PagesOf, typename Wait>
+// barrier.  len_of / tok_lp / wait as for topk_core.
+template <int PER, typename LenOf, typename Wait>
 __device__ __forceinline__ void select_for_split(const TopkArgs& ta, int bh, int first, bool writer,
-                                                 PagesOf&& pages_of, const int& tok_lp,
+                                                 LenOf&& len_of, const int& tok_lp,
                                                  Wait&& wait, char* lds,
                                                  int (&l_lp)[kMaxSplitPages],
                                                  int (&l_m)[kMaxSplitPages],
@@ -102,7 +102,7 @@ __device__ __forceinline__ void select_for_split(const TopkArgs& ta, int bh, int
   int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
   int32_t* ph_row = ta.sel_phys + (int64_t)bh * g.k_max;
   const int k = topk_core<PER, kAttendThreads / 64>(
-      ta, bh, pages_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
+      ta, bh, len_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
         const int ph = (phys >= 0 && phys < g.num_phys) ? phys : -1;
         if (pos >= first && pos < first + g.pages_per_split) {
           l_lp[pos - first] = p;
@@ -178,7 +178,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArg
             seq_len = pos + 1;
             tok_lp = pos / g.P;
           }
-          return min((seq_len + g.P - 1) / g.P, g.max_pages);
+          return seq_len;
         },
         tok_lp, [] {}, lds, l_lp, l_m, l_ph, s_k, tok_out);
   };
@@ -332,7 +332,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs 
     __syncthreads();
   };
   auto select = [&] {
-    select_for_split<PER>(ta, bh, first, writer, [&] { return n_pages; }, tok_lp, head_wait,
+    select_for_split<PER>(ta, bh, first, writer, [&] { return seq_len; }, tok_lp, head_wait,
                           lds, l_lp, l_m, l_ph, s_k, tok_out);
   };
   attend_role<T, D, 1, MAXP, true, false>(

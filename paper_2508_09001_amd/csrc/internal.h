@@ -38,6 +38,7 @@ __device__ __forceinline__ float to_f32(bf16_t x) {
 struct Geometry {
   int batch, hk, G, hq, D, P, budget, W, R, max_pages, num_phys, dtype, elt;
   int k_max;          // selection row length
+  int budget_permille;  // relative budget (0: the fixed budget B only)
   float sm_scale;     // resolved (never 0)
   // attention split geometry
   int chunk_pages;    // pages per 32-token chunk (2 for P=16, 1 for P=32)

@@ -428,6 +428,16 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
   }
 }
 
+// Pages of the step's budget for a sequence of `len` tokens: B / P with a fixed
+// budget; with a relative one (the ablation of Sec. 4, Table 1's setting) the
+// budget is max(B, floor(len * permille / 1000)) tokens, len counting the
+// step's token.
+__device__ __forceinline__ int budget_pages(const Geometry& g, int len) {
+  int b = g.budget;
+  if (g.budget_permille > 0) b = max(b, (int)((int64_t)len * g.budget_permille / 1000));
+  return b / g.P;
+}
+
 // ============================================================================
 // Top-k + mask role: PageSelect and UpdateAndBuildMask (Alg. 1, Alg. 2) for
 // one (sequence, KV head); see topk.hip for the algorithm.
@@ -463,15 +473,16 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 // THREADS = blockDim.x threads (at most MAXW wavefronts); page i of the
 // sequence is held by thread i mod THREADS in stripe i / THREADS (coalesced
 // loads).  ceil(max_pages / THREADS) <= PER.  tok_lp: logical page written by
-// this step's token (-1: none), read after `pages_of()` (which may set it):
+// this step's token (-1: none), read after `len_of()` (which may set it):
 // Alg. 2's current-page rule applies to it, so its last_loaded entry is taken as
-// step - 1.  `pages_of()` gives n, the pages of the sequence; it is called once
+// step - 1.  `len_of()` gives the sequence's length in tokens (with the step's
+// token when it is stored), which fixes n = its pages and the budget; it is called once
 // the loads are issued.  hist: kTopkHistWords
 // uint32 of LDS; small: kTopkSmall ints of LDS.
 // `wait()` is called after the page-table and last_loaded loads are issued and
 // before the scores are read.
-template <int PER, int MAXW, typename PagesOf, typename Wait, typename OnPage>
-__device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, PagesOf&& pages_of, const int& tok_lp,
+template <int PER, int MAXW, typename LenOf, typename Wait, typename OnPage>
+__device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, LenOf&& len_of, const int& tok_lp,
                                          uint32_t* hist, int* small, Wait&& wait,
                                          OnPage&& on_page) {
   constexpr int NCH = (PER * MAXW + 63) / 64;  // 64-entry chunks of the count table
@@ -507,7 +518,8 @@ __device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, PagesOf&& p
   for (int j = 0; j < PER; ++j)
     sv[j] = __hip_atomic_load(srow + min(j * THREADS + tid, last), __ATOMIC_RELAXED,
                               __HIP_MEMORY_SCOPE_AGENT);
-  const int n = pages_of();
+  const int len = len_of();
+  const int n = min((len + g.P - 1) / g.P, g.max_pages);
   auto valid = [&](int j) { return j * THREADS + tid < n; };
 #pragma unroll
   for (int j = 0; j < PER; ++j)
@@ -535,7 +547,7 @@ __device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, PagesOf&& p
   kmax = wave_umax(lane < NW ? (uint32_t)red[16 + lane] : 0u);
   const uint32_t range = kmax - kmin;
   const int nbits = range ? 32 - __clz((int)range) : 1;
-  const int k = min(g.budget / g.P, n);
+  const int k = min(min(budget_pages(g, len), n), g.k_max);
 
   // Radix select: pass p histograms the next digit of the keys that still match
   // T's prefix into its own histogram.  After a barrier, wavefront 0 alone
@@ -703,8 +715,8 @@ __device__ __forceinline__ int topk_core(const TopkArgs& ta, int bh, PagesOf&& p
 // pages (step - 1 for the token's page when it is not kept).  Arguments as
 // topk_core's.  COH: the selection is read by other workgroups of the same
 // launch, so it is stored device-coherently.
-template <int PER, int MAXW, bool COH, typename PagesOf, typename Wait>
-__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& pages_of, int tok_lp,
+template <int PER, int MAXW, bool COH, typename LenOf, typename Wait>
+__device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, LenOf&& len_of, int tok_lp,
                                           uint32_t* hist, int* small, Wait&& wait) {
   const Geometry& g = ta.g;
   const int step = ta.step;
@@ -713,7 +725,7 @@ __device__ __forceinline__ void topk_role(const TopkArgs& ta, int bh, PagesOf&& 
   int32_t* m_row = ta.mask + (int64_t)bh * g.k_max;
   int32_t* ph_row = ta.sel_phys ? ta.sel_phys + (int64_t)bh * g.k_max : nullptr;
   const int k = topk_core<PER, MAXW>(
-      ta, bh, pages_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
+      ta, bh, len_of, tok_lp, hist, small, wait, [&](int pos, int p, int a_old, int phys) {
         if (pos >= 0) {
           put_c<COH>(sel_row + pos, p);
           put_c<COH>(m_row + pos, a_old);

@@ -77,7 +77,7 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
   // the step's token and the sequence's pages (after the digest loads are issued)
-  int n_pages = 0, tok_lp = -1;
+  int n_pages = 0, tok_lp = -1, live_len = 0;
   auto tok_of = [&](int& np) {
     const int pos = seq_lens[b];
     StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
@@ -91,6 +91,7 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
     }
     np = n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
     tok_lp = tk.lp;
+    live_len = seq_len;
     return tk;
   };
   int32_t warm_a = 0, warm_p = 0;
@@ -134,7 +135,7 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
     if (s_last) {
       uint32_t* hist = reinterpret_cast<uint32_t*>(dyn_lds);
       int* small = reinterpret_cast<int*>(hist + kTopkHistWords);
-      topk_role<PER, score_threads(PER) / 64, false>(sa.tk, (int)bh, [&] { return n_pages; }, tok_lp, hist, small, [] {});
+      topk_role<PER, score_threads(PER) / 64, false>(sa.tk, (int)bh, [&] { return live_len; }, tok_lp, hist, small, [] {});
     }
   }
 }

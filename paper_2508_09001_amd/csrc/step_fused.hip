@@ -136,7 +136,7 @@ step_kernel(StepArgs a) {
             [&](int& np) { np = n_pages; return tk; });
         block_signal(cntA + kCtlStride * bh);
       } else if (role == 1) {
-        topk_role<PER, kFusedWaves, true>(a.tk, bh, [&] { return n_pages; }, tok_ok ? lp : -1,
+        topk_role<PER, kFusedWaves, true>(a.tk, bh, [&] { return seq_len; }, tok_ok ? lp : -1,
                                   reinterpret_cast<uint32_t*>(lds), small,
                                   [&] { block_wait(cntA + kCtlStride * bh, g.fA, err); });
         block_signal(cntB + kCtlStride * bh);

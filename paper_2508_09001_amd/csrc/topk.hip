@@ -42,7 +42,7 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
   }
   topk_role<PER, THREADS / 64, false>(
       ta, bh,
-      [&] { return min((live_seq_len(ta.g, seq_lens, ta.pt, b) + ta.g.P - 1) / ta.g.P, ta.g.max_pages); },
+      [&] { return live_seq_len(ta.g, seq_lens, ta.pt, b); },
       tok_lp, hist, small, [] {});
 }
 

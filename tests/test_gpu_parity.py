@@ -172,3 +172,18 @@ def test_attention_wait_timeout_gives_nan_outputs(monkeypatch):
             assert np.isfinite(o).all() and not np.isnan(z).any()
         else:
             assert np.isnan(o).all() and np.isnan(z).all()
+
+
+def test_relative_budget_grows_with_context():
+    # relative budget of 0.15 with a 256-token floor: sequence 1 crosses from
+    # 16 to 17 pages per step (0.15 * 1814 = 272.1 tokens) during the run
+    spec = W.Spec("relative-budget", batch=2, num_kv_heads=2, group=4, head_dim=128, page_size=16,
+                  budget=256, window=4, steps=20, dtype="bf16", prefill=(1700, 1810), seed=21,
+                  budget_permille=150)
+    run_parity(spec, 20, page_perm_seed=7, label="relative budget 0.15, min 256")
+
+
+def test_relative_budget_llama_layer_32k():
+    # the headline layer with the paper's relative budget: 307+ pages per step
+    spec = W.config(1).replace(budget_permille=150)
+    run_parity(spec, 10, label="32k relative budget 0.15")

@@ -167,6 +167,35 @@ def test_select_equals_stable_sort_by_score_then_index(n, budget_pages):
             assert np.all(sel[b, h, k:] == -1)
 
 
+def test_relative_budget_pages():
+    """Relative budget (Sec. 4 ablation, Table 1's setting: fraction 0.15 of the
+    context, at least 256 tokens): k = min(floor(max(256, floor(0.15 L)) / P),
+    pages of the sequence), the counts below worked by hand for P = 16."""
+    P = 16
+    lens = [100, 1707, 1813, 1814, 10000, 20000]
+    # 100 tokens: 7 pages; 256/16; floor(271.95) = 271 -> 16; 272/16; 1500/16; 3000/16
+    want_k = [7, 16, 16, 17, 93, 187]
+    o = oracle.Oracle(batch=len(lens), num_kv_heads=1, group=1, head_dim=8, page_size=P,
+                      budget=256, window=0, max_tokens=20000, budget_permille=150)
+    assert o.k_max == 187                 # the budget of a full 1250-page row
+    rng = np.random.default_rng(3)
+    scores = rng.standard_normal((len(lens), 1, o.max_pages)).astype(np.float32)
+    o.seq_lens[:] = lens
+    sel, num = o.select(scores)
+    for b, (L, k) in enumerate(zip(lens, want_k)):
+        assert num[b, 0] == k
+        nb = -(-L // P)
+        order = np.lexsort((np.arange(nb), -scores[b, 0, :nb].astype(np.float64)))
+        np.testing.assert_array_equal(sel[b, 0, :k], np.sort(order[:k]))
+        assert np.all(sel[b, 0, k:] == -1)
+    fixed = oracle.Oracle(batch=len(lens), num_kv_heads=1, group=1, head_dim=8, page_size=P,
+                          budget=256, window=0, max_tokens=20000)
+    assert fixed.k_max == 16
+    fixed.seq_lens[:] = lens
+    _, num = fixed.select(scores)
+    assert list(num[:, 0]) == [7, 16, 16, 16, 16, 16]
+
+
 # ----------------------------------------------------------------------------- Alg. 2
 def test_alg2_golden_walk():
     gold = _load("alg2_walk.json")

@@ -50,7 +50,7 @@ class Spec:
     group: int              # query heads per KV head (GQA); h_q = num_kv_heads * group
     head_dim: int
     page_size: int
-    budget: int             # token budget B; pages per step = budget // page_size
+    budget: int             # token budget B (the minimum one with budget_permille)
     window: int             # W = number of past queries revisited each step
     steps: int
     dtype: str              # "f32" or "bf16"
@@ -61,6 +61,7 @@ class Spec:
     outlier_scale: float = 1.0
     drift_step: float = 0.0
     seed: int = 0
+    budget_permille: int = 0  # relative budget: max(B, len * permille / 1000) tokens per step
 
     @property
     def num_q_heads(self) -> int:
