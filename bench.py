@@ -45,6 +45,10 @@ def _args():
     p.add_argument("--warmup", type=int, default=4, help="untimed decode steps")
     p.add_argument("--layers", type=int, default=32, help="layer replicas rotated per step")
     p.add_argument("--config", type=int, default=1, help="workload index (1 = headline)")
+    p.add_argument("--window", type=int, default=None,
+                   help="override the workload's window W (W = 0: no retrospection)")
+    p.add_argument("--budget-permille", type=int, default=None,
+                   help="relative budget in thousandths of the context (0: fixed budget)")
     p.add_argument("--attend-reps", type=int, default=4,
                    help="scores + selection + attention launches per layer in the roofline measurement")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -130,6 +134,10 @@ def main():
         return
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     base_spec = W.config(args.config)
+    if args.window is not None:
+        base_spec = base_spec.replace(window=args.window)
+    if args.budget_permille is not None:
+        base_spec = base_spec.replace(budget_permille=args.budget_permille)
     need = args.warmup + 2 * args.steps
     spec = base_spec if need <= base_spec.steps else base_spec.replace(steps=need)
     L = args.layers
@@ -241,7 +249,8 @@ def main():
         "config": {"workload": spec.name, "batch": spec.batch, "kv_heads": spec.num_kv_heads,
                    "q_heads": spec.num_q_heads, "head_dim": spec.head_dim,
                    "context": int(spec.prefill[0]), "page_size": spec.page_size,
-                   "budget_tokens": spec.budget, "window": spec.window, "layers_rotated": L,
+                   "budget_tokens": spec.budget, "budget_permille": spec.budget_permille,
+                   "window": spec.window, "layers_rotated": L,
                    "launch": "hip-graph per step",
                    "step_path": _step_path()},
         "us_per_layer_step": round(us_layer_step, 3),
