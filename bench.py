@@ -49,6 +49,8 @@ def _args():
                    help="override the workload's window W (W = 0: no retrospection)")
     p.add_argument("--budget-permille", type=int, default=None,
                    help="relative budget in thousandths of the context (0: fixed budget)")
+    p.add_argument("--update-kv", action="store_true",
+                   help="UpdateKV of the window's W past tokens before every step (Alg. 1)")
     p.add_argument("--attend-reps", type=int, default=4,
                    help="scores + selection + attention launches per layer in the roofline measurement")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -162,9 +164,21 @@ def main():
         lay._lens = list(layers[0]._lens)
     torch.cuda.synchronize()
 
+    # UpdateKV inputs: seeded synthetic re-embedded keys / values of the W past
+    # tokens, resident on the device like the step's other inputs
+    upd = None
+    if args.update_kv and spec.window > 0:
+        gen_u = torch.Generator().manual_seed(7)
+        td = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+        shape = (spec.batch, spec.window, spec.num_kv_heads, spec.head_dim)
+        upd = [tuple(torch.randn(shape, generator=gen_u).to("cuda", dtype=td) for _ in range(2))
+               for _ in range(4)]
+
     def run_step(t):
         win, k_new, v_new = steps_in[t]
         for lay in layers:
+            if upd is not None and t > 0:
+                lay.update_kv(*upd[t % len(upd)])
             for j in range(k_new.shape[0] - 1):
                 lay.append(t, k_new[j], v_new[j])
             lay.step(t, win, k_new[-1], v_new[-1])
@@ -250,7 +264,8 @@ def main():
                    "q_heads": spec.num_q_heads, "head_dim": spec.head_dim,
                    "context": int(spec.prefill[0]), "page_size": spec.page_size,
                    "budget_tokens": spec.budget, "budget_permille": spec.budget_permille,
-                   "window": spec.window, "layers_rotated": L,
+                   "window": spec.window, "update_kv": bool(upd is not None),
+                   "layers_rotated": L,
                    "launch": "hip-graph per step",
                    "step_path": _step_path()},
         "us_per_layer_step": round(us_layer_step, 3),

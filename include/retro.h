@@ -169,13 +169,26 @@ retro_status retro_prefill_kv(const retro_dims* dims, const retro_kv_cache* cach
 retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_kv_cache* cache,
                              const void* k_new, const void* v_new, void* stream);
 
+/* UpdateKV (Alg. 1; Sec. 3.3, retrospective KV cache update): the keys and values
+ * of the n_tokens most recent stored tokens of every sequence b (positions
+ * seq_lens[b] - n_tokens .. seq_lens[b] - 1; those below 0 are skipped) are
+ * overwritten with k_upd / v_upd [batch][n_tokens][h_k][d] (dtype; row j is
+ * position seq_lens[b] - n_tokens + j), e.g. re-embedded from the previous
+ * layer's updated outputs, and the digest of every page they touch is recomputed
+ * as the element-wise min / max over its stored keys.  Called before the step's
+ * append (Alg. 1 order), with n_tokens = W for the window's past tokens.
+ * last_loaded and seq_lens are unchanged.  n_tokens = 0 does nothing. */
+retro_status retro_update_kv(const retro_dims* dims, const retro_kv_cache* cache,
+                             int32_t n_tokens, const void* k_upd, const void* v_upd,
+                             void* stream);
+
 /* PageSelect + UpdateAndBuildMask (Alg. 1, Alg. 2) for the current query
  * q_cur [batch][h_q][d] (dtype).
  *   score of page p of KV head h = sum over the G query heads g of h of
  *     sum_i max(q_gi * Kmin_pi, q_gi * Kmax_pi)                  eq. (quest_score)
  *   evaluated in fp32: products rounded to fp32, the d terms summed as a perfect
  *   binary tree over index order, the G head sums added in order, then + 0.0f.
- *   The k = min(B/P, ceil(seq_len/P)) best pages by (score descending, page index
+ *   The k = min(B_t/P, ceil(seq_len/P)) best pages by (score descending, page index
  *   ascending) are written in ascending order; then for each selected page p, in
  *   order: mask = last_loaded[p]; last_loaded[p] = step.
  * Page selection is exact: it depends on no floating-point reduction order other

@@ -58,6 +58,8 @@ def _load():
         lib.oracle_prefill.restype = C.c_int
         lib.oracle_append.argtypes = [D, i32, P, P, P, P, P, P, P, P]
         lib.oracle_append.restype = C.c_int
+        lib.oracle_update_kv.argtypes = [D, i32, P, P, P, P, P, P, P]
+        lib.oracle_update_kv.restype = None
         lib.oracle_score.argtypes = [D, P, P, P, P, P]
         lib.oracle_score.restype = None
         lib.oracle_select.argtypes = [D, P, P, P, P]
@@ -150,6 +152,14 @@ class Oracle:
                                     _p(v_new))
         if rc != 0:
             raise ValueError("append exceeds max_tokens")
+
+    def update_kv(self, k_upd: np.ndarray, v_upd: np.ndarray) -> None:
+        """UpdateKV (Alg. 1): k_upd, v_upd [batch][n][h_k][d] replace the n most recent
+        stored tokens of every sequence; their pages' digests are recomputed."""
+        k_upd = np.ascontiguousarray(k_upd, np.float32)
+        v_upd = np.ascontiguousarray(v_upd, np.float32)
+        self.lib.oracle_update_kv(self._d, k_upd.shape[1], _p(self.seq_lens), _p(self.K),
+                                  _p(self.V), _p(self.kmin), _p(self.kmax), _p(k_upd), _p(v_upd))
 
     def score(self, q_cur: np.ndarray) -> np.ndarray:
         q_cur = np.ascontiguousarray(q_cur, np.float32)

@@ -147,6 +147,47 @@ int oracle_append(const oracle_dims* g, int32_t step, int32_t* seq_lens, float* 
 }
 
 /* ---------------------------------------------------------------------------
+ * UpdateKV (Alg. 1; Sec. 3.3, retrospective KV cache update): the keys and
+ * values of the n most recent stored tokens of every sequence b (positions
+ * seq_lens[b] - n .. seq_lens[b] - 1, those below 0 skipped) are replaced by
+ * k_upd / v_upd ([batch][n][h_k][d], row j = position seq_lens[b] - n + j),
+ * and the digest of every page holding one of them becomes the element-wise
+ * min / max over all of that page's stored keys again.
+ * ------------------------------------------------------------------------- */
+void oracle_update_kv(const oracle_dims* g, int32_t n, const int32_t* seq_lens, float* K,
+                      float* V, float* kmin, float* kmax, const float* k_upd,
+                      const float* v_upd) {
+  const int hk = g->num_kv_heads, d = g->head_dim, P = g->page_size;
+  const int64_t mp = max_pages_of(g);
+  for (int b = 0; b < g->batch; ++b) {
+    const int len = seq_lens[b];
+    const int first = len - n;
+    for (int pos = first < 0 ? 0 : first; pos < len; ++pos)
+      for (int h = 0; h < hk; ++h)
+        for (int i = 0; i < d; ++i) {
+          const int64_t src = (((int64_t)b * n + (pos - first)) * hk + h) * d + i;
+          const int64_t dst = (((int64_t)b * hk + h) * g->max_tokens + pos) * d + i;
+          K[dst] = k_upd[src];
+          V[dst] = v_upd[src];
+        }
+    if (len <= 0 || n <= 0) continue;
+    const int p0 = (first < 0 ? 0 : first) / P, p1 = (len - 1) / P;
+    for (int page = p0; page <= p1; ++page)
+      for (int h = 0; h < hk; ++h)
+        for (int i = 0; i < d; ++i) {
+          float lo = 0.f, hi = 0.f;
+          for (int pos = page * P; pos < (page + 1) * P && pos < len; ++pos) {
+            const float x = K[(((int64_t)b * hk + h) * g->max_tokens + pos) * d + i];
+            if (pos == page * P || x < lo) lo = x;
+            if (pos == page * P || x > hi) hi = x;
+          }
+          kmin[(((int64_t)b * hk + h) * mp + page) * d + i] = lo;
+          kmax[(((int64_t)b * hk + h) * mp + page) * d + i] = hi;
+        }
+  }
+}
+
+/* ---------------------------------------------------------------------------
  * Page score, eq. (quest_score): score_j(Q) = sum_i max(Q_i Kmin_i, Q_i Kmax_i).
  * A KV head's page is scored for the sum over the query heads of its group
  * (page selection is per KV head, Sec. "Retrospective Mask").

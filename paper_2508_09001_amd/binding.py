@@ -19,7 +19,8 @@ RETRO_OK, RETRO_EINVAL, RETRO_EUNSUPPORTED, RETRO_EHIP, RETRO_EWORKSPACE = 0, -1
 RETRO_F32, RETRO_BF16 = 0, 1
 
 EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_workspace_size",
-            "retro_prefill_kv", "retro_append_kv", "retro_select_pages", "retro_decode_attend",
+            "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
+            "retro_decode_attend",
             "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_merge_output_cache", "retro_step")
 
@@ -76,6 +77,7 @@ def load_library(path: str = LIB_PATH):
         "retro_workspace_size": ([D, C.POINTER(C.c_size_t)], C.c_int),
         "retro_prefill_kv": ([D, C.POINTER(KVCache), i32, i32, i32, P, P, P], C.c_int),
         "retro_append_kv": ([D, i32, C.POINTER(KVCache), P, P, P], C.c_int),
+        "retro_update_kv": ([D, C.POINTER(KVCache), i32, P, P, P], C.c_int),
         "retro_select_pages": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
                                 C.c_size_t, P], C.c_int),
         "retro_decode_attend": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P, P, P,
@@ -148,6 +150,11 @@ def retro_prefill_kv(dims: Dims, cache: KVCache, seq: int, start_pos: int, n_tok
 def retro_append_kv(dims: Dims, step: int, cache: KVCache, k_new, v_new, stream=None) -> None:
     _check(load_library().retro_append_kv(C.byref(dims), step, C.byref(cache), _ptr(k_new),
                                           _ptr(v_new), _stream(stream)), "retro_append_kv")
+
+
+def retro_update_kv(dims: Dims, cache: KVCache, n_tokens: int, k_upd, v_upd, stream=None) -> None:
+    _check(load_library().retro_update_kv(C.byref(dims), C.byref(cache), n_tokens, _ptr(k_upd),
+                                          _ptr(v_upd), _stream(stream)), "retro_update_kv")
 
 
 def retro_select_pages(dims: Dims, step: int, q_cur, cache: KVCache, sel: Selection, workspace,

@@ -199,6 +199,19 @@ retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_k
   return from_hip(retro::launch_append(g, step, *cache, k_new, v_new, (hipStream_t)stream));
 }
 
+retro_status retro_update_kv(const retro_dims* dims, const retro_kv_cache* cache,
+                             int32_t n_tokens, const void* k_upd, const void* v_upd,
+                             void* stream) {
+  Geometry g;
+  retro_status st = make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  if (!cache_ok(cache) || n_tokens < 0) return RETRO_EINVAL;
+  if (n_tokens == 0) return RETRO_OK;
+  if (!k_upd || !v_upd) return RETRO_EINVAL;
+  if (n_tokens > g.max_pages * g.P) return RETRO_EINVAL;
+  return from_hip(retro::launch_update_kv(g, *cache, n_tokens, k_upd, v_upd, (hipStream_t)stream));
+}
+
 retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void* q_cur,
                                 const retro_kv_cache* cache, const retro_selection* sel,
                                 void* workspace, size_t ws_bytes, void* stream) {

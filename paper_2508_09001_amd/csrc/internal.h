@@ -94,6 +94,10 @@ hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, c
                          const void* v_new, hipStream_t s);
 hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
                           const void* k_src, const void* v_src, hipStream_t s);
+// UpdateKV: the n most recent stored tokens of every sequence get new keys and
+// values (k_upd, v_upd: [batch][n][h_k][d]); their pages' digests are recomputed.
+hipError_t launch_update_kv(const Geometry& g, const retro_kv_cache& c, int n, const void* k_upd,
+                            const void* v_upd, hipStream_t s);
 // With g.token_pending, the score launch also appends the step's token
 // (k_new, v_new: [batch][h_k][d]) as AppendKV does, without advancing seq_lens.
 // With a selection, counters ([batch * h_k] ints of the workspace, zero

@@ -124,6 +124,84 @@ __global__ void __launch_bounds__(128) prefill_digest_kernel(Geometry g, int seq
   }
 }
 
+// UpdateKV (Alg. 1; Sec. 3.3, retrospective KV cache update): the n most recent
+// stored tokens of every sequence are overwritten with their re-embedded keys and
+// values, and the digest of each page they touch is recomputed from the page's
+// stored keys (a min / max cannot be narrowed incrementally).  One workgroup per
+// (touched page, KV head, sequence), one thread per element of d: each slot's key
+// is the update when its position is in the updated run, else the stored one;
+// all of a page's loads are issued before the min / max chain uses them.
+__device__ __forceinline__ float key_f32(float x) { return x; }
+__device__ __forceinline__ float key_f32(bf16_t x) { return to_f32(x); }
+__device__ __forceinline__ void from_key(float x, float* d) { *d = x; }
+__device__ __forceinline__ void from_key(float x, bf16_t* d) {
+  d->bits = (uint16_t)(__float_as_uint(x) >> 16);  // exact: x holds a bf16 value
+}
+
+template <typename T, int PS>
+__global__ void __launch_bounds__(128) update_kv_kernel(Geometry g, int n, T* __restrict__ kc,
+                                                        T* __restrict__ vc, T* __restrict__ dg,
+                                                        const int32_t* __restrict__ pt,
+                                                        const int32_t* __restrict__ seq_lens,
+                                                        const T* __restrict__ k_upd,
+                                                        const T* __restrict__ v_upd) {
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int len = seq_lens[b];
+  const int start = max(len - n, 0);
+  const int lp = start / PS + blockIdx.x;
+  if (lp >= g.max_pages || lp * PS >= len) return;
+  const int phys = pt[(int64_t)b * g.max_pages + lp];
+  if (phys < 0 || phys >= g.num_phys) return;
+  const int filled = min(PS, len - lp * PS);
+  const int64_t ph = (int64_t)phys * g.hk + h;
+  T* drow = dg + ((((int64_t)b * g.hk + h) * g.max_pages + lp) * 2) * g.D;
+  for (int i = threadIdx.x; i < g.D; i += blockDim.x) {
+    float f[PS];
+#pragma unroll
+    for (int s = 0; s < PS; ++s) {
+      const int pos = lp * PS + s;
+      if (s < filled) {  // uniform
+        if (pos >= start) {
+          const int64_t e = (((int64_t)b * n + (pos - (len - n))) * g.hk + h) * g.D + i;
+          const T kv = k_upd[e];
+          kc[(ph * PS + s) * g.D + i] = kv;
+          vc[(ph * g.D + i) * PS + s] = v_upd[e];
+          f[s] = key_f32(kv);
+        } else {
+          f[s] = key_f32(kc[(ph * PS + s) * g.D + i]);
+        }
+      }
+    }
+    float lo = f[0], hi = f[0];
+#pragma unroll
+    for (int s = 1; s < PS; ++s) {
+      if (s < filled) {
+        if (f[s] < lo) lo = f[s];
+        if (hi < f[s]) hi = f[s];
+      }
+    }
+    from_key(lo, drow + i);
+    from_key(hi, drow + g.D + i);
+  }
+}
+
+template <typename T>
+hipError_t update_kv_t(const Geometry& g, const retro_kv_cache& c, int n, const void* k_upd,
+                       const void* v_upd, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  // the run [len - n, len) spans at most ceil(n / P) + 1 pages
+  const dim3 grid((unsigned)((n + g.P - 1) / g.P + 1), (unsigned)g.hk, (unsigned)g.batch);
+  if (g.P == 16)
+    update_kv_kernel<T, 16><<<grid, 128, 0, s>>>(g, n, (T*)c.k_cache, (T*)c.v_cache, (T*)c.digest,
+                                                 c.page_table, c.seq_lens, (const T*)k_upd,
+                                                 (const T*)v_upd);
+  else
+    update_kv_kernel<T, 32><<<grid, 128, 0, s>>>(g, n, (T*)c.k_cache, (T*)c.v_cache, (T*)c.digest,
+                                                 c.page_table, c.seq_lens, (const T*)k_upd,
+                                                 (const T*)v_upd);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t append_t(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
                     const void* v_new, hipStream_t s) {
@@ -162,6 +240,12 @@ hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, i
                           const void* k_src, const void* v_src, hipStream_t s) {
   return g.dtype == RETRO_BF16 ? prefill_t<bf16_t>(g, c, seq, start, n, k_src, v_src, s)
                                : prefill_t<float>(g, c, seq, start, n, k_src, v_src, s);
+}
+
+hipError_t launch_update_kv(const Geometry& g, const retro_kv_cache& c, int n, const void* k_upd,
+                            const void* v_upd, hipStream_t s) {
+  return g.dtype == RETRO_BF16 ? update_kv_t<bf16_t>(g, c, n, k_upd, v_upd, s)
+                               : update_kv_t<float>(g, c, n, k_upd, v_upd, s);
 }
 
 }  // namespace retro

@@ -112,6 +112,13 @@ class RetroLayer:
         B.retro_decode_attend_partials(self.dims, step, q_window, self.cache, self.sel,
                                        self.workspace, self.ws_bytes, stream)
 
+    def update_kv(self, k_upd, v_upd, stream=None) -> None:
+        """UpdateKV: new keys / values [batch][n][h_k][d] for the n most recent stored
+        tokens of every sequence (their pages' digests are recomputed)."""
+        k_upd, v_upd = self._dev(k_upd), self._dev(v_upd)
+        B.retro_update_kv(self.dims, self.cache, int(k_upd.shape[1]), k_upd, v_upd, stream)
+        self._keep_upd = (k_upd, v_upd)
+
     def step_attend_partials(self, step: int, q_window: torch.Tensor, stream=None) -> None:
         """The step's launch that ends in the attention partials (scores where the step
         computes them there, selection, attention) alone; overwrites the selection

@@ -62,8 +62,30 @@ def compare_step(t, layer, ref, tol, stats: Stats, outputs=True):
     stats.steps += 1
 
 
+def reembedded_kv(orc, n: int, rng, dtype: str):
+    """Synthetic UpdateKV inputs: the n most recent stored keys / values of every
+    sequence, perturbed by 5 % (keys) and 10 % (values) of their rms, as a
+    re-embedding through the next layer would change them; [batch][n][h_k][d]."""
+    b_, hk, d = orc.batch, orc.hk, orc.d
+    ku = np.zeros((b_, n, hk, d), np.float32)
+    vu = np.zeros((b_, n, hk, d), np.float32)
+    for b in range(b_):
+        L = int(orc.seq_lens[b])
+        for j in range(n):
+            pos = L - n + j
+            if pos < 0:
+                continue
+            k, v = orc.K[b, :, pos], orc.V[b, :, pos]
+            ku[b, j] = k + 0.05 * np.sqrt(np.mean(k * k)) * rng.standard_normal(k.shape)
+            vu[b, j] = v + 0.10 * np.sqrt(np.mean(v * v)) * rng.standard_normal(v.shape)
+    if dtype == "bf16":
+        ku, vu = W.round_bf16(ku), W.round_bf16(vu)
+    return ku.astype(np.float32), vu.astype(np.float32)
+
+
 def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_calls=False,
-               check_outputs_from: int = 0, tol: Optional[float] = None, label: str = "") -> Stats:
+               check_outputs_from: int = 0, tol: Optional[float] = None, label: str = "",
+               update_kv: bool = False) -> Stats:
     """Run `steps` decode steps on GPU and oracle; compare every step's selection,
     mask and A exactly, and the outputs of the steps >= check_outputs_from (the
     oracle runs attention only from check_outputs_from - W on, which is enough
@@ -72,7 +94,8 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
     tol = TOL[spec.dtype] if tol is None else tol
     print(f"[parity] {label or spec.name}: batch={spec.batch} hk={spec.num_kv_heads} "
           f"G={spec.group} d={spec.head_dim} P={spec.page_size} B={spec.budget} W={spec.window} "
-          f"steps={steps} tps={spec.tokens_per_step} perm={page_perm_seed} split={split_calls}",
+          f"steps={steps} tps={spec.tokens_per_step} perm={page_perm_seed} split={split_calls} "
+          f"update_kv={update_kv}",
           flush=True)
     gen = W.Generator(spec)
     orc = oracle.Oracle.for_spec(spec)
@@ -83,9 +106,15 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
     qw = W.QueryWindow(spec)
     stats = Stats()
     attend_from = max(0, check_outputs_from - spec.window)
+    rng_upd = np.random.default_rng(1234)
     for t in range(steps):
         k_new, v_new, q = gen.step(t)
         win = qw.push(q).copy()
+        if update_kv and spec.window > 0 and t > 0:
+            # UpdateKV of the window's past tokens, before the step's append (Alg. 1)
+            ku, vu = reembedded_kv(orc, spec.window, rng_upd, spec.dtype)
+            orc.update_kv(ku, vu)
+            layer.update_kv(ku, vu)
         ref = orc.step(t, k_new, v_new, win, attend=t >= attend_from)
         ref["A"] = orc.A
         T = k_new.shape[0]

@@ -187,3 +187,18 @@ def test_relative_budget_llama_layer_32k():
     # the headline layer with the paper's relative budget: 307+ pages per step
     spec = W.config(1).replace(budget_permille=150)
     run_parity(spec, 10, label="32k relative budget 0.15")
+
+
+def test_update_kv_tiny_fp32():
+    # UpdateKV of the W = 4 past tokens before every step (Alg. 1 order)
+    run_parity(W.config(0), 16, update_kv=True, label="tiny-fp32 + UpdateKV")
+
+
+def test_update_kv_llama_layer_32k():
+    run_parity(W.config(1), 10, page_perm_seed=3, update_kv=True, label="32k + UpdateKV")
+
+
+def test_update_kv_short_sequences_and_partial_pages():
+    spec = W.Spec("edge-short", batch=3, num_kv_heads=2, group=3, head_dim=64, page_size=16,
+                  budget=64, window=5, steps=20, dtype="bf16", prefill=(1, 17, 40), seed=9)
+    run_parity(spec, 20, page_perm_seed=3, update_kv=True, label="edge short + UpdateKV")

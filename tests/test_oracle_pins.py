@@ -61,6 +61,45 @@ def test_digest_is_elementwise_min_max_of_stored_keys(tps):
             np.testing.assert_array_equal(o.kmax[b, :, p], keys.max(axis=0))
 
 
+# ----------------------------------------------------------------------------- UpdateKV
+def test_update_kv_overwrites_recent_tokens_and_recomputes_digests():
+    """UpdateKV (Alg. 1; Sec. 3.3): the n most recent stored tokens of each sequence
+    take the new keys and values, nothing else changes, and every page digest is
+    again the element-wise min / max over the page's stored keys: here the update
+    lowers a page maximum, which widening could not produce."""
+    P, d, hk = 4, 8, 2
+    o = oracle.Oracle(batch=2, num_kv_heads=hk, group=1, head_dim=d, page_size=P, budget=P,
+                      window=0, max_tokens=40)
+    rng = np.random.default_rng(5)
+    lens = [13, 2]
+    for b, L in enumerate(lens):
+        k = rng.standard_normal((L, hk, d)).astype(np.float32)
+        v = rng.standard_normal((L, hk, d)).astype(np.float32)
+        k[L - 1, 0, 3] = 50.0                       # the page maximum, about to be replaced
+        o.prefill(b, k, v)
+    K0, V0 = o.K.copy(), o.V.copy()
+    old_max = o.kmax[0, 0, (lens[0] - 1) // P, 3]
+    n = 3                                           # sequence 1 holds only 2 tokens
+    ku = rng.standard_normal((2, n, hk, d)).astype(np.float32)
+    vu = rng.standard_normal((2, n, hk, d)).astype(np.float32)
+    o.update_kv(ku, vu)
+    for b, L in enumerate(lens):
+        for j in range(n):
+            pos = L - n + j
+            if pos < 0:
+                continue
+            np.testing.assert_array_equal(o.K[b, :, pos], ku[b, j])
+            np.testing.assert_array_equal(o.V[b, :, pos], vu[b, j])
+        keep = max(L - n, 0)
+        np.testing.assert_array_equal(o.K[b, :, :keep], K0[b, :, :keep])
+        np.testing.assert_array_equal(o.V[b, :, :keep], V0[b, :, :keep])
+        for page in range(-(-L // P)):
+            toks = o.K[b, :, page * P:min((page + 1) * P, L)]
+            np.testing.assert_array_equal(o.kmin[b, :, page], toks.min(axis=1))
+            np.testing.assert_array_equal(o.kmax[b, :, page], toks.max(axis=1))
+    assert o.kmax[0, 0, (lens[0] - 1) // P, 3] < old_max
+
+
 # ----------------------------------------------------------------------------- score
 def _score_setup(dtype, d, G, seed):
     spec = _tiny_spec(head_dim=d, group=G, dtype=dtype, prefill=(70, 70), steps=0, seed=seed)
