@@ -64,8 +64,9 @@ def compare_step(t, layer, ref, tol, stats: Stats, outputs=True):
 
 def reembedded_kv(orc, n: int, rng, dtype: str):
     """Synthetic UpdateKV inputs: the n most recent stored keys / values of every
-    sequence, perturbed by 5 % (keys) and 10 % (values) of their rms, as a
-    re-embedding through the next layer would change them; [batch][n][h_k][d]."""
+    sequence, perturbed by 5 % (keys) and 10 % (values) of their rms, the size of
+    one retrospective update's change the paper reports for keys and values
+    (appendix, evolving query representations); [batch][n][h_k][d]."""
     b_, hk, d = orc.batch, orc.hk, orc.d
     ku = np.zeros((b_, n, hk, d), np.float32)
     vu = np.zeros((b_, n, hk, d), np.float32)
