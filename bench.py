@@ -55,6 +55,11 @@ def _args():
                    help="scores + selection + attention launches per layer in the roofline measurement")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="budget of the CPU oracle sample (0 skips it)")
+    p.add_argument("--decoder", type=int, default=0,
+                   help="instead: a stack of this many layers with projections and "
+                        "re-embedding, timed per token at each --decoder-windows value")
+    p.add_argument("--decoder-windows", default="0,2,4,8,16",
+                   help="windows W compared in --decoder mode")
     p.add_argument("--calib-copy", action="store_true",
                    help="only run a 512 MiB device copy (counter calibration) and exit")
     return p.parse_args()
@@ -133,6 +138,9 @@ def main():
 
     if args.calib_copy:
         _calib_copy()
+        return
+    if args.decoder > 0:
+        decoder_bench(args)
         return
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     base_spec = W.config(args.config)
@@ -281,6 +289,103 @@ def main():
 
     if args.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(spec, pre, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def decoder_bench(args):
+    """Per-token latency of a stack of args.decoder layers (random-weight query, key,
+    value and output projections around each layer's step; the past rows re-embedded
+    and their keys and values overwritten), at every window in --decoder-windows:
+    the analogue of the paper's throughput-versus-window table.  Inputs are drawn on
+    the device from seeded generators; each timed step is replayed from its own HIP
+    graph."""
+    import torch
+
+    import workloads as W
+    from paper_2508_09001_amd.decode import RetroDecoder, layer_kwargs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    base = W.config(args.config)
+    if args.budget_permille is not None:
+        base = base.replace(budget_permille=args.budget_permille)
+    windows = [int(x) for x in args.decoder_windows.split(",")]
+    L = args.decoder
+    warmup = max(args.warmup, max(windows) + 1)   # every past row re-embedded from then on
+    need = warmup + args.steps + 1
+    spec0 = base.replace(steps=max(base.steps, need))
+    dev = torch.device("cuda")
+    td = torch.bfloat16 if spec0.dtype == "bf16" else torch.float32
+    dm = spec0.num_q_heads * spec0.head_dim
+    g = torch.Generator(device=dev).manual_seed(2508)
+
+    def randn(*shape, scale=1.0):
+        return (torch.randn(*shape, generator=g, device=dev) * scale).to(td)
+
+    hq_d, hk_d = spec0.num_q_heads * spec0.head_dim, spec0.num_kv_heads * spec0.head_dim
+    weights = [dict(wq=randn(dm, hq_d, scale=dm ** -0.5), wk=randn(dm, hk_d, scale=dm ** -0.5),
+                    wv=randn(dm, hk_d, scale=dm ** -0.5),
+                    wo=randn(hq_d, dm, scale=(hq_d * L) ** -0.5)) for _ in range(L)]
+    prompts = [[(randn(n, spec0.num_kv_heads, spec0.head_dim),
+                 randn(n, spec0.num_kv_heads, spec0.head_dim)) for n in spec0.prefill]
+               for _ in range(L)]
+    emb = randn(spec0.batch, need + max(windows), dm)
+    ms = {}
+    for w in windows:
+        spec = spec0.replace(window=w)
+        dec = RetroDecoder(weights, **layer_kwargs(spec))
+        for layer in range(L):
+            for b, (k, v) in enumerate(prompts[layer]):
+                dec.prefill(layer, b, k, v)
+        off = max(windows)
+        wins = [emb[:, off + t - w:off + t + 1].contiguous() for t in range(need)]
+        for t in range(warmup):
+            dec.step(t, wins[t])
+        torch.cuda.synchronize()
+        graphs = []
+        for t in range(warmup, warmup + args.steps):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                dec.step(t, wins[t])
+            graphs.append(gr)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for gr in graphs:
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms[w] = e0.elapsed_time(e1) / args.steps
+        print(f"[decoder] W={w}: {ms[w]:.4f} ms/token over {L} layers", file=sys.stderr,
+              flush=True)
+        del graphs, dec, wins
+        torch.cuda.empty_cache()
+    w_main = max(windows)
+    base_ms = ms.get(0)
+    result = {
+        "metric": "decode_ms_per_token",
+        "value": round(ms[w_main], 4),
+        "unit": "ms/token",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms[w_main], 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec0.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{spec0.name} x {L} layers with projections",
+                   "batch": spec0.batch, "context": int(spec0.prefill[0]), "layers": L,
+                   "d_model": dm, "budget_tokens": spec0.budget,
+                   "budget_permille": spec0.budget_permille, "window": w_main,
+                   "launch": "hip-graph per token"},
+        "ms_per_token_by_window": {str(w): round(v, 4) for w, v in ms.items()},
+        "tokens_per_s_by_window": {str(w): round(spec0.batch * 1000.0 / v, 1)
+                                   for w, v in ms.items()},
+    }
+    if base_ms:
+        result["overhead_vs_w0_pct"] = {str(w): round(100.0 * (v / base_ms - 1.0), 2)
+                                        for w, v in ms.items() if w != 0}
     print(json.dumps(result), flush=True)
 
 

@@ -1,0 +1,113 @@
+"""Multi-layer decode with retrospective re-embedding (Sec. 3.3, "Influences on
+deeper layers"; Alg. 1 in every layer).
+
+At step t every layer sees the W+1 window rows t-W .. t.  The newest row is
+embedded for the first time; the W past rows carry the layer below's updated
+outputs, so their queries, keys and values are computed again: UpdateKV
+(``retro_update_kv``) overwrites the stored keys and values of the decoded past
+rows, and the layer's step (``retro_step``) appends the newest token and attends
+all W+1 queries.  Layers are joined by a residual stream kept in fp32:
+``H(l+1) = H(l) + O(l) Wo``.
+
+The projections are plain dense products over (W+1) * batch rows, the case the
+paper's linear-layer analysis (Appendix, linear layer overhead) prices; they run
+as library GEMMs (torch.matmul on the device, bf16 in, fp32 accumulation, bf16
+out).  Every attention-side step runs in the gfx950 library.  Feed-forward blocks
+and normalisation are left out: they do not touch the KV cache.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import torch
+
+from .layer import RetroLayer
+
+
+class RetroDecoder:
+    """``len(weights)`` RetroLayers joined by query/key/value and output projections.
+
+    ``weights``: per layer a dict of ``wq [d_model][h_q*d]``, ``wk``, ``wv
+    [d_model][h_k*d]`` and ``wo [h_q*d][d_model]`` (host arrays or device tensors);
+    ``d_model = h_q * d``.  ``layer_kw`` are the RetroLayer arguments shared by all
+    layers (batch, num_kv_heads, group, head_dim, page_size, budget, window,
+    max_pages, dtype, budget_permille, ...).
+    """
+
+    def __init__(self, weights: Sequence[dict], device: str = "cuda", **layer_kw):
+        self.device = torch.device(device)
+        self.layers: List[RetroLayer] = [RetroLayer(device=device, **layer_kw)
+                                         for _ in weights]
+        lay = self.layers[0]
+        self.dtype = lay.dtype
+        self.W, self.batch, self.hq, self.hk, self.d = lay.W, lay.batch, lay.hq, lay.hk, lay.d
+        self.d_model = self.hq * self.d
+        self.weights = []
+        for w in weights:
+            dw = {}
+            for name in ("wq", "wk", "wv", "wo"):
+                x = w[name]
+                if not isinstance(x, torch.Tensor):
+                    x = torch.from_numpy(x)
+                dw[name] = x.to(device=self.device, dtype=self.dtype).contiguous()
+            if dw["wq"].shape != (self.d_model, self.hq * self.d) or \
+               dw["wk"].shape != (self.d_model, self.hk * self.d) or \
+               dw["wv"].shape != (self.d_model, self.hk * self.d) or \
+               dw["wo"].shape != (self.hq * self.d, self.d_model):
+                raise ValueError("projection shapes do not match the layer geometry")
+            self.weights.append(dw)
+        self.decoded = 0  # decode steps run so far
+
+    def prefill(self, layer: int, seq: int, k, v, stream=None) -> None:
+        """Prompt keys and values [n][h_k][d] of one sequence in one layer."""
+        self.layers[layer].prefill(seq, k, v, stream)
+
+    def n_update(self) -> int:
+        """Past rows re-embedded this step: the decoded ones among the W."""
+        return min(self.W, self.decoded)
+
+    def step(self, t: int, emb_window: torch.Tensor, trace: Optional[list] = None
+             ) -> torch.Tensor:
+        """One decode step of the whole stack on the current stream.
+
+        emb_window: [batch][W+1][d_model] device tensor, the embeddings of the
+        window's tokens (row W the newest; zero rows before the first decode step).
+        Returns the residual stream after the last layer, [batch][W+1][d_model]
+        fp32.  ``trace`` (a list) receives per layer the tensors the layer saw and
+        produced (for tests).
+        """
+        b, rows, W = self.batch, self.W + 1, self.W
+        if tuple(emb_window.shape) != (b, rows, self.d_model):
+            raise ValueError("emb_window must be [batch][W+1][d_model]")
+        n_upd = self.n_update()
+        h = emb_window.to(device=self.device, dtype=torch.float32)
+        for lay, w in zip(self.layers, self.weights):
+            x = h.to(self.dtype)
+            q = torch.matmul(x, w["wq"]).view(b, rows, self.hq, self.d)
+            k = torch.matmul(x, w["wk"]).view(b, rows, self.hk, self.d)
+            v = torch.matmul(x, w["wv"]).view(b, rows, self.hk, self.d)
+            if n_upd > 0:
+                lay.update_kv(k[:, W - n_upd:W], v[:, W - n_upd:W])
+            lay.step(t, q, k[:, W], v[:, W])
+            y = torch.matmul(lay.o_out.to(self.dtype).view(b, rows, self.d_model), w["wo"])
+            if trace is not None:
+                trace.append(dict(x=x.clone(), q=q.clone(), k=k.clone(), v=v.clone(),
+                                  o_out=lay.o_out.clone(), lse_out=lay.lse_out.clone(),
+                                  selected=lay.selected.clone(), mask=lay.mask.clone(),
+                                  num_selected=lay.num_selected.clone(), y=y.clone()))
+            h = h + y.float()
+        self.decoded += 1
+        return h
+
+
+def layer_kwargs(spec, **over) -> dict:
+    """RetroLayer arguments of a workload Spec (shared by every layer)."""
+    kw = dict(batch=spec.batch, num_kv_heads=spec.num_kv_heads, group=spec.group,
+              head_dim=spec.head_dim, page_size=spec.page_size, budget=spec.budget,
+              window=spec.window, max_pages=spec.max_pages, dtype=spec.dtype,
+              budget_permille=spec.budget_permille)
+    kw.update(over)
+    return kw
+
+
+__all__ = ["RetroDecoder", "layer_kwargs"]

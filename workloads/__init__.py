@@ -24,8 +24,8 @@ from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
 
-__all__ = ["Spec", "Generator", "QueryWindow", "CONFIGS", "config", "round_bf16",
-           "config4_combos"]
+__all__ = ["Spec", "Generator", "QueryWindow", "DecoderInputs", "CONFIGS", "config",
+           "round_bf16", "config4_combos"]
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
@@ -228,3 +228,56 @@ class QueryWindow:
             self.q[:, :-1] = self.q[:, 1:]
         self.q[:, -1] = q
         return self.q
+
+
+class DecoderInputs:
+    """Seeded inputs of a multi-layer synthetic decode with re-embedding.
+
+    ``num_layers`` attention layers of the Spec's shape with model width
+    ``d_model = h_q * d`` (the Llama layout: 32 query heads of 128 = 4096):
+
+    * ``weights()``: per layer the query, key, value and output projections
+      ``wq [d_model][h_q*d]``, ``wk``, ``wv [d_model][h_k*d]``, ``wo [h_q*d][d_model]``,
+      Gaussian with variance 1/fan_in (the output projection further scaled by
+      1/sqrt(num_layers), which keeps the residual stream's size bounded over depth);
+    * ``prefill(layer)``: that layer's prompt keys and values, as ``Generator.prefill``
+      (an independent stream per layer);
+    * ``embedding(t)``: the embedding ``[batch][d_model]`` of the token decoded at step
+      ``t`` (unit Gaussian).
+
+    Trained weights do not exist here; these random ones stand in for them.  Values
+    are rounded to bf16 for bf16 Specs, like every other input of this module.
+    """
+
+    def __init__(self, spec: Spec, num_layers: int, seed: Optional[int] = None):
+        self.spec = spec
+        self.num_layers = num_layers
+        self.seed = spec.seed if seed is None else seed
+        self.d_model = spec.num_q_heads * spec.head_dim
+        self._bf16 = spec.dtype == "bf16"
+
+    def _q(self, x: np.ndarray) -> np.ndarray:
+        return round_bf16(x) if self._bf16 else np.ascontiguousarray(x, np.float32)
+
+    def weights(self) -> List[dict]:
+        s, dm = self.spec, self.d_model
+        hq_d, hk_d = s.num_q_heads * s.head_dim, s.num_kv_heads * s.head_dim
+        out = []
+        for layer in range(self.num_layers):
+            rng = np.random.default_rng(np.random.SeedSequence([self.seed, 10, layer]))
+
+            def draw(rows, cols, scale):
+                w = rng.standard_normal((rows, cols), dtype=np.float32)
+                return self._q(w * np.float32(scale))
+
+            out.append(dict(wq=draw(dm, hq_d, dm ** -0.5), wk=draw(dm, hk_d, dm ** -0.5),
+                            wv=draw(dm, hk_d, dm ** -0.5),
+                            wo=draw(hq_d, dm, (hq_d * self.num_layers) ** -0.5)))
+        return out
+
+    def prefill(self, layer: int) -> List[Tuple[np.ndarray, np.ndarray]]:
+        return Generator(self.spec, seed=self.seed * 1000 + 11 + layer).prefill()
+
+    def embedding(self, t: int) -> np.ndarray:
+        rng = np.random.default_rng(np.random.SeedSequence([self.seed, 12, t]))
+        return self._q(rng.standard_normal((self.spec.batch, self.d_model), dtype=np.float32))
