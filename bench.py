@@ -60,6 +60,8 @@ def _args():
                         "re-embedding, timed per token at each --decoder-windows value")
     p.add_argument("--decoder-windows", default="0,2,4,8,16",
                    help="windows W compared in --decoder mode")
+    p.add_argument("--decoder-torch-proj", action="store_true",
+                   help="in --decoder mode, run the projections on torch.matmul instead")
     p.add_argument("--calib-copy", action="store_true",
                    help="only run a 512 MiB device copy (counter calibration) and exit")
     return p.parse_args()
@@ -332,7 +334,8 @@ def decoder_bench(args):
     ms = {}
     for w in windows:
         spec = spec0.replace(window=w)
-        dec = RetroDecoder(weights, **layer_kwargs(spec))
+        dec = RetroDecoder(weights, library_projections=not args.decoder_torch_proj,
+                           **layer_kwargs(spec))
         for layer in range(L):
             for b, (k, v) in enumerate(prompts[layer]):
                 dec.prefill(layer, b, k, v)
@@ -378,7 +381,8 @@ def decoder_bench(args):
                    "batch": spec0.batch, "context": int(spec0.prefill[0]), "layers": L,
                    "d_model": dm, "budget_tokens": spec0.budget,
                    "budget_permille": spec0.budget_permille, "window": w_main,
-                   "launch": "hip-graph per token"},
+                   "launch": "hip-graph per token",
+                   "projections": "torch.matmul" if args.decoder_torch_proj else "library"},
         "ms_per_token_by_window": {str(w): round(v, 4) for w, v in ms.items()},
         "tokens_per_s_by_window": {str(w): round(spec0.batch * 1000.0 / v, 1)
                                    for w, v in ms.items()},

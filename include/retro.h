@@ -278,6 +278,42 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
                         float* o_out, float* lse_out, void* workspace, size_t ws_bytes,
                         void* stream);
 
+/* ---- Projections of the multi-layer decode with re-embedding (Sec. 3.3) --------
+ * Every layer projects the W+1 window rows of every sequence (rows = batch*(W+1),
+ * at most 48) to queries, keys and values, and its merged outputs back to the
+ * model width; the past rows are re-embedded from the layer below's updated
+ * outputs, their new keys and values then go to retro_update_kv.  With so few
+ * rows the products are bound by reading the weights, which are therefore kept
+ * pre-tiled for the matrix cores.  bf16 weights and inputs, fp32 accumulation,
+ * bf16 results rounded to nearest even.  Every pointer is a device address,
+ * 16-byte aligned; the caller owns every buffer. */
+
+/* Tiles a weight w [k][n] bf16 (row-major, y = x . w) into w_packed (k*n bf16, a
+ * separate buffer): element (i, j) goes to [j/16][i/32][(i%32)/8][j%16][i%8].
+ * Weights that share an input (query, key and value) are packed as one [k][n]
+ * matrix with their columns side by side.  k % 32 == 0 and n % 16 == 0, else
+ * RETRO_EUNSUPPORTED. */
+retro_status retro_pack_weight(const void* w, int32_t k, int32_t n, void* w_packed,
+                               void* stream);
+
+/* q = x . Wq, k_out = x . Wk, v = x . Wv for x [rows][k] bf16 and a packed
+ * [k][n_q + 2 n_kv] weight whose columns are Wq's, then Wk's, then Wv's; outputs
+ * bf16 [rows][n_q], [rows][n_kv], [rows][n_kv] (for the window rows of a
+ * decoder: [batch][W+1][h_q][d] and [batch][W+1][h_k][d]).  Supported: 1 <= rows
+ * <= 48, k % 1024 == 0, n_q % 16 == n_kv % 16 == 0 (else RETRO_EUNSUPPORTED);
+ * rows == 0 does nothing. */
+retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const void* w_packed,
+                               int32_t n_q, int32_t n_kv, void* q, void* k_out, void* v,
+                               void* stream);
+
+/* The output projection and the residual add: y = bf16(o) . Wo for o [rows][k]
+ * fp32 (a decoder's merged outputs o_out, k = h_q * d) and a packed [k][n]
+ * weight, rounded to bf16; then h[r][j] += y[r][j] in fp32 (h [rows][n], the
+ * residual stream, updated in place) and x_next = bf16(h) [rows][n] (the next
+ * layer's input).  Supported shapes as for retro_project_qkv. */
+retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const void* w_packed,
+                               int32_t n, float* h, void* x_next, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

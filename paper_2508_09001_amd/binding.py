@@ -22,7 +22,8 @@ EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_worksp
             "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
             "retro_decode_attend",
             "retro_decode_attend_partials", "retro_step_attend_partials",
-            "retro_merge_output_cache", "retro_step")
+            "retro_merge_output_cache", "retro_step", "retro_pack_weight", "retro_project_qkv",
+            "retro_project_out")
 
 
 class RetroError(RuntimeError):
@@ -89,6 +90,9 @@ def load_library(path: str = LIB_PATH):
         "retro_merge_output_cache": ([D, i32, P, P, C.POINTER(OutputCache), P, P, P], C.c_int),
         "retro_step": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
                         C.POINTER(OutputCache), P, P, P, C.c_size_t, P], C.c_int),
+        "retro_pack_weight": ([P, i32, i32, P, P], C.c_int),
+        "retro_project_qkv": ([P, i32, i32, P, i32, i32, P, P, P, P], C.c_int),
+        "retro_project_out": ([P, i32, i32, P, i32, P, P, P], C.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -203,3 +207,20 @@ def retro_step(dims: Dims, step: int, q_window, k_new, v_new, cache: KVCache, se
                                      C.byref(cache), C.byref(sel), C.byref(ocache), _ptr(o_out),
                                      _ptr(lse_out), _ptr(workspace), ws_bytes, _stream(stream)),
            "retro_step")
+
+
+def retro_pack_weight(w, k: int, n: int, w_packed, stream=None) -> None:
+    _check(load_library().retro_pack_weight(_ptr(w), k, n, _ptr(w_packed), _stream(stream)),
+           "retro_pack_weight")
+
+
+def retro_project_qkv(x, rows: int, k: int, w_packed, n_q: int, n_kv: int, q, k_out, v,
+                      stream=None) -> None:
+    _check(load_library().retro_project_qkv(_ptr(x), rows, k, _ptr(w_packed), n_q, n_kv, _ptr(q),
+                                            _ptr(k_out), _ptr(v), _stream(stream)),
+           "retro_project_qkv")
+
+
+def retro_project_out(o, rows: int, k: int, w_packed, n: int, h, x_next, stream=None) -> None:
+    _check(load_library().retro_project_out(_ptr(o), rows, k, _ptr(w_packed), n, _ptr(h),
+                                            _ptr(x_next), _stream(stream)), "retro_project_out")

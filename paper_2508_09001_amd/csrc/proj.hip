@@ -1,0 +1,247 @@
+// Dense projections of the multi-layer decode with re-embedding (Sec. 3.3): the
+// W+1 window rows of every sequence, a few dozen at most, times a weight matrix.
+// With so few rows the product is bound by reading the weight once from HBM
+// (the paper's appendix on linear layers makes the same point), so each weight is
+// stored pre-tiled for the MFMA operand layout: one wavefront load of 1 KB per
+// 16 columns x 32 reduction elements, contiguous in memory.
+//
+// Packed layout of a [K][N] weight (y = x . w): [N/16][K/32][4][16][8] bf16;
+// element (k, n) sits at tile n/16, step k/32, group (k%32)/8, column n%16,
+// position k%8.  Lane l = 16 * group + column of a wavefront then holds exactly
+// the B operand of v_mfma_f32_16x16x32_bf16 for its column.
+//
+// A workgroup owns 16 output columns; its PJ_WAVES wavefronts split the
+// reduction, each accumulating all row tiles (16 rows each) of its share with
+// MFMA, and the shares are summed in a fixed order through LDS.  Sixteen
+// wavefronts of 512 reduction elements each load their whole share of a
+// 4096-deep weight in one pass: the launch is a single round trip to HBM per
+// wavefront, which is what a few-row product costs.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace retro {
+namespace {
+
+constexpr int PJ_WAVES = 16;         // wavefronts per workgroup, each a slice of the reduction
+constexpr int PJ_MIN_STEPS = 2;      // 32-element reduction steps per wavefront (at least)
+constexpr int PJ_MAX_ROW_TILES = 3;  // up to 48 rows
+
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+__device__ __forceinline__ bf16x8 bits_to_bf16x8(uint4 u) {
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+// A operand: row `row` of x, elements [k, k + 8); zero past the last row.
+// x is bf16 [rows][K], or f32 [rows][K] rounded to bf16 here.
+template <bool F32IN>
+__device__ __forceinline__ bf16x8 load_a(const void* x, int rows, int K, int row, int k) {
+  if (row >= rows) return bits_to_bf16x8(make_uint4(0, 0, 0, 0));
+  if constexpr (F32IN) {
+    const float* p = static_cast<const float*>(x) + (int64_t)row * K + k;
+    const float4 lo = *reinterpret_cast<const float4*>(p);
+    const float4 hi = *reinterpret_cast<const float4*>(p + 4);
+    uint4 u;
+    u.x = bf16_rne(lo.x) | (uint32_t(bf16_rne(lo.y)) << 16);
+    u.y = bf16_rne(lo.z) | (uint32_t(bf16_rne(lo.w)) << 16);
+    u.z = bf16_rne(hi.x) | (uint32_t(bf16_rne(hi.y)) << 16);
+    u.w = bf16_rne(hi.z) | (uint32_t(bf16_rne(hi.w)) << 16);
+    return bits_to_bf16x8(u);
+  } else {
+    const bf16_t* p = static_cast<const bf16_t*>(x) + (int64_t)row * K + k;
+    return bits_to_bf16x8(*reinterpret_cast<const uint4*>(p));
+  }
+}
+
+struct ProjArgs {
+  const void* x;          // [rows][K]: bf16 (QKV) or f32 (output projection)
+  const uint4* w;         // packed weight, N columns
+  int rows, K, N;
+  // QKV: columns [0, nq) -> q, [nq, nq + nkv) -> k, the rest -> v (bf16 [rows][n])
+  int nq, nkv;
+  bf16_t *q, *k, *v;
+  // output projection: h [rows][N] f32 += bf16(y); x_next = bf16(h)
+  float* h;
+  bf16_t* x_next;
+};
+
+template <int MT, bool OUT, int U>
+__global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
+  __shared__ float red[PJ_WAVES][MT][4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ln16 = lane & 15, g4 = lane >> 4;
+  const int tile = blockIdx.x;
+  const int steps = a.K / 32, per_wave = steps / PJ_WAVES;
+  const int s0 = wave * per_wave;
+  const uint4* wp = a.w + ((int64_t)tile * steps + s0) * 64 + lane;
+  f32x4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // U steps per pass, every load of the pass issued before its MFMAs
+  for (int s = 0; s < per_wave; s += U) {
+    bf16x8 b[U], av[U][MT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      b[u] = bits_to_bf16x8(wp[(int64_t)(s + u) * 64]);
+      const int k = (s0 + s + u) * 32 + 8 * g4;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) av[u][mt] = load_a<OUT>(a.x, a.rows, a.K, mt * 16 + ln16, k);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt], b[u], acc[mt], 0, 0, 0);
+  }
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][mt][i][lane] = acc[mt][i];
+  __syncthreads();
+  // output (mt, i, l): row mt*16 + 4*(l/16) + i, column tile*16 + l%16
+  for (int o = threadIdx.x; o < MT * 256; o += blockDim.x) {
+    const int mt = o >> 8, i = (o >> 6) & 3, l = o & 63;
+    const int row = mt * 16 + 4 * (l >> 4) + i;
+    if (row >= a.rows) continue;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < PJ_WAVES; ++w) sum += red[w][mt][i][l];
+    const int col = tile * 16 + (l & 15);
+    const uint16_t y = bf16_rne(sum);
+    if constexpr (OUT) {
+      const int64_t e = (int64_t)row * a.N + col;
+      const float hv = a.h[e] + __uint_as_float(uint32_t(y) << 16);
+      a.h[e] = hv;
+      a.x_next[e].bits = bf16_rne(hv);
+    } else {
+      if (col < a.nq)
+        a.q[(int64_t)row * a.nq + col].bits = y;
+      else if (col < a.nq + a.nkv)
+        a.k[(int64_t)row * a.nkv + (col - a.nq)].bits = y;
+      else
+        a.v[(int64_t)row * a.nkv + (col - a.nq - a.nkv)].bits = y;
+    }
+  }
+}
+
+template <int MT, bool OUT>
+void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
+  // as many reduction steps per pass as the wavefront's share allows (up to 8;
+  // 4 for three row tiles, whose operands would not fit the registers), so that
+  // a share takes as few dependent round trips to memory as possible
+  const int per_wave = a.K / 32 / PJ_WAVES;
+  const dim3 grid(a.N / 16), block(64 * PJ_WAVES);
+  if (MT <= 2 && per_wave % 8 == 0)
+    proj_kernel<MT, OUT, (MT <= 2 ? 8 : 4)><<<grid, block, 0, s>>>(a);
+  else if (per_wave % 4 == 0)
+    proj_kernel<MT, OUT, 4><<<grid, block, 0, s>>>(a);
+  else
+    proj_kernel<MT, OUT, 2><<<grid, block, 0, s>>>(a);
+}
+
+template <bool OUT>
+hipError_t launch_proj(const ProjArgs& a, hipStream_t s) {
+  const int mt = (a.rows + 15) / 16;
+  if (mt == 1)
+    launch_proj_mt<1, OUT>(a, s);
+  else if (mt == 2)
+    launch_proj_mt<2, OUT>(a, s);
+  else
+    launch_proj_mt<3, OUT>(a, s);
+  return hipGetLastError();
+}
+
+// [K][N] row-major -> packed tiles; one thread per 8-element group.
+__global__ void pack_kernel(const bf16_t* __restrict__ w, int K, int N, uint4* __restrict__ out) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)K * N / 8;
+  if (idx >= total) return;
+  const int lane = (int)(idx & 63);
+  const int64_t ts = idx >> 6;           // tile * steps + step
+  const int steps = K / 32;
+  const int tile = (int)(ts / steps), step = (int)(ts % steps);
+  const int col = tile * 16 + (lane & 15);
+  const int k0 = step * 32 + 8 * (lane >> 4);
+  uint32_t h[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) h[j] = w[(int64_t)(k0 + j) * N + col].bits;
+  out[idx] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                        h[6] | (h[7] << 16));
+}
+
+retro_status status_of(hipError_t e) { return e == hipSuccess ? RETRO_OK : RETRO_EHIP; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool proj_shape_ok(int rows, int K, int N) {
+  return rows >= 1 && rows <= 16 * PJ_MAX_ROW_TILES && K > 0 &&
+         K % (32 * PJ_WAVES * PJ_MIN_STEPS) == 0 &&
+         N > 0 && N % 16 == 0;
+}
+
+}  // namespace
+}  // namespace retro
+
+extern "C" {
+
+retro_status retro_pack_weight(const void* w, int32_t k, int32_t n, void* w_packed,
+                               void* stream) {
+  if (!w || !w_packed || k <= 0 || n <= 0) return RETRO_EINVAL;
+  if (!retro::aligned16(w_packed)) return RETRO_EINVAL;
+  if (k % 32 != 0 || n % 16 != 0) return RETRO_EUNSUPPORTED;
+  const int64_t groups = (int64_t)k * n / 8;
+  const int threads = 256;
+  const int64_t blocks = (groups + threads - 1) / threads;
+  if (blocks > 0x7fffffff) return RETRO_EUNSUPPORTED;
+  retro::pack_kernel<<<(unsigned)blocks, threads, 0, (hipStream_t)stream>>>(
+      static_cast<const retro::bf16_t*>(w), k, n, static_cast<uint4*>(w_packed));
+  return retro::status_of(hipGetLastError());
+}
+
+retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const void* w_packed,
+                               int32_t n_q, int32_t n_kv, void* q, void* k_out, void* v,
+                               void* stream) {
+  if (!x || !w_packed || !q || !k_out || !v || rows < 0 || k <= 0 || n_q <= 0 || n_kv <= 0)
+    return RETRO_EINVAL;
+  if (rows == 0) return RETRO_OK;
+  if (!retro::aligned16(x) || !retro::aligned16(w_packed)) return RETRO_EINVAL;
+  const int n = n_q + 2 * n_kv;
+  if (!retro::proj_shape_ok(rows, k, n) || n_q % 16 != 0 || n_kv % 16 != 0)
+    return RETRO_EUNSUPPORTED;
+  retro::ProjArgs a{};
+  a.x = x;
+  a.w = static_cast<const uint4*>(w_packed);
+  a.rows = rows;
+  a.K = k;
+  a.N = n;
+  a.nq = n_q;
+  a.nkv = n_kv;
+  a.q = static_cast<retro::bf16_t*>(q);
+  a.k = static_cast<retro::bf16_t*>(k_out);
+  a.v = static_cast<retro::bf16_t*>(v);
+  return retro::status_of(retro::launch_proj<false>(a, (hipStream_t)stream));
+}
+
+retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const void* w_packed,
+                               int32_t n, float* h, void* x_next, void* stream) {
+  if (!o || !w_packed || !h || !x_next || rows < 0 || k <= 0 || n <= 0) return RETRO_EINVAL;
+  if (rows == 0) return RETRO_OK;
+  if (!retro::aligned16(o) || !retro::aligned16(w_packed)) return RETRO_EINVAL;
+  if (!retro::proj_shape_ok(rows, k, n)) return RETRO_EUNSUPPORTED;
+  retro::ProjArgs a{};
+  a.x = o;
+  a.w = static_cast<const uint4*>(w_packed);
+  a.rows = rows;
+  a.K = k;
+  a.N = n;
+  a.h = h;
+  a.x_next = static_cast<retro::bf16_t*>(x_next);
+  return retro::status_of(retro::launch_proj<true>(a, (hipStream_t)stream));
+}
+
+}  // extern "C"

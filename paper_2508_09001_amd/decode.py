@@ -9,11 +9,15 @@ rows, and the layer's step (``retro_step``) appends the newest token and attends
 all W+1 queries.  Layers are joined by a residual stream kept in fp32:
 ``H(l+1) = H(l) + O(l) Wo``.
 
-The projections are plain dense products over (W+1) * batch rows, the case the
-paper's linear-layer analysis (Appendix, linear layer overhead) prices; they run
-as library GEMMs (torch.matmul on the device, bf16 in, fp32 accumulation, bf16
-out).  Every attention-side step runs in the gfx950 library.  Feed-forward blocks
-and normalisation are left out: they do not touch the KV cache.
+The projections are dense products over (W+1) * batch rows, the case the paper's
+linear-layer analysis (Appendix, linear layer overhead) prices: bound by reading
+the weights.  In bf16 they run in the library too (``retro_project_qkv``: one
+launch for the query, key and value projections of a layer, weights pre-tiled by
+``retro_pack_weight``; ``retro_project_out``: the output projection fused with the
+residual add and the next layer's bf16 input), both bf16 in, fp32 accumulation,
+bf16 out.  fp32 stacks (small test shapes) use torch.matmul for the products.
+Feed-forward blocks and normalisation are left out: they do not touch the KV
+cache.
 """
 from __future__ import annotations
 
@@ -21,6 +25,7 @@ from typing import List, Optional, Sequence
 
 import torch
 
+from . import binding as B
 from .layer import RetroLayer
 
 
@@ -31,10 +36,12 @@ class RetroDecoder:
     [d_model][h_k*d]`` and ``wo [h_q*d][d_model]`` (host arrays or device tensors);
     ``d_model = h_q * d``.  ``layer_kw`` are the RetroLayer arguments shared by all
     layers (batch, num_kv_heads, group, head_dim, page_size, budget, window,
-    max_pages, dtype, budget_permille, ...).
+    max_pages, dtype, budget_permille, ...).  ``library_projections=False`` keeps
+    the products on torch.matmul (for comparison).
     """
 
-    def __init__(self, weights: Sequence[dict], device: str = "cuda", **layer_kw):
+    def __init__(self, weights: Sequence[dict], device: str = "cuda",
+                 library_projections: bool = True, **layer_kw):
         self.device = torch.device(device)
         self.layers: List[RetroLayer] = [RetroLayer(device=device, **layer_kw)
                                          for _ in weights]
@@ -57,6 +64,30 @@ class RetroDecoder:
                 raise ValueError("projection shapes do not match the layer geometry")
             self.weights.append(dw)
         self.decoded = 0  # decode steps run so far
+        # bf16: library projections (weights pre-tiled; the first needs k % 1024 == 0
+        # and at most 48 rows)
+        rows = self.batch * (self.W + 1)
+        self.fused = (library_projections and self.dtype == torch.bfloat16 and
+                      self.d_model % 1024 == 0 and
+                      (self.hq * self.d) % 1024 == 0 and rows <= 48)
+        if self.fused:
+            nq, nkv = self.hq * self.d, self.hk * self.d
+            self.packed = []
+            for dw in self.weights:
+                wqkv = torch.cat([dw["wq"], dw["wk"], dw["wv"]], dim=1).contiguous()
+                pq = torch.empty_like(wqkv)
+                po = torch.empty_like(dw["wo"])
+                B.retro_pack_weight(wqkv, self.d_model, nq + 2 * nkv, pq)
+                B.retro_pack_weight(dw["wo"], nq, self.d_model, po)
+                self.packed.append((pq, po))
+            torch.cuda.synchronize(self.device)
+            dev, td = self.device, self.dtype
+            self.h = torch.zeros(self.batch, self.W + 1, self.d_model, dtype=torch.float32,
+                                 device=dev)
+            self.x = torch.zeros(self.batch, self.W + 1, self.d_model, dtype=td, device=dev)
+            self.q = torch.zeros(self.batch, self.W + 1, self.hq, self.d, dtype=td, device=dev)
+            self.k = torch.zeros(self.batch, self.W + 1, self.hk, self.d, dtype=td, device=dev)
+            self.v = torch.zeros_like(self.k)
 
     def prefill(self, layer: int, seq: int, k, v, stream=None) -> None:
         """Prompt keys and values [n][h_k][d] of one sequence in one layer."""
@@ -73,13 +104,16 @@ class RetroDecoder:
         emb_window: [batch][W+1][d_model] device tensor, the embeddings of the
         window's tokens (row W the newest; zero rows before the first decode step).
         Returns the residual stream after the last layer, [batch][W+1][d_model]
-        fp32.  ``trace`` (a list) receives per layer the tensors the layer saw and
-        produced (for tests).
+        fp32 (with the library projections, a buffer of the decoder that the next
+        step overwrites).  ``trace`` (a list) receives per layer the tensors the
+        layer saw and produced (for tests).
         """
         b, rows, W = self.batch, self.W + 1, self.W
         if tuple(emb_window.shape) != (b, rows, self.d_model):
             raise ValueError("emb_window must be [batch][W+1][d_model]")
         n_upd = self.n_update()
+        if self.fused:
+            return self._step_fused(t, emb_window, n_upd, trace)
         h = emb_window.to(device=self.device, dtype=torch.float32)
         for lay, w in zip(self.layers, self.weights):
             x = h.to(self.dtype)
@@ -98,6 +132,30 @@ class RetroDecoder:
             h = h + y.float()
         self.decoded += 1
         return h
+
+    def _step_fused(self, t, emb_window, n_upd, trace):
+        b, rows, W = self.batch, self.W + 1, self.W
+        nq, nkv = self.hq * self.d, self.hk * self.d
+        self.h.copy_(emb_window)
+        self.x.copy_(emb_window)
+        for lay, (pq, po) in zip(self.layers, self.packed):
+            h_in = self.h.clone() if trace is not None else None
+            x_in = self.x.clone() if trace is not None else None
+            B.retro_project_qkv(self.x, b * rows, self.d_model, pq, nq, nkv, self.q, self.k,
+                                self.v)
+            if n_upd > 0:
+                lay.update_kv(self.k[:, W - n_upd:W], self.v[:, W - n_upd:W])
+            lay.step(t, self.q, self.k[:, W], self.v[:, W])
+            B.retro_project_out(lay.o_out, b * rows, nq, po, self.d_model, self.h, self.x)
+            if trace is not None:
+                trace.append(dict(x=x_in, q=self.q.clone(), k=self.k.clone(), v=self.v.clone(),
+                                  o_out=lay.o_out.clone(), lse_out=lay.lse_out.clone(),
+                                  selected=lay.selected.clone(), mask=lay.mask.clone(),
+                                  num_selected=lay.num_selected.clone(), h_in=h_in,
+                                  h_out=self.h.clone(), x_next=self.x.clone(),
+                                  y=self.h - h_in))
+        self.decoded += 1
+        return self.h
 
 
 def layer_kwargs(spec, **over) -> dict:

@@ -17,6 +17,7 @@ import numpy as np
 import pytest
 
 import workloads as W
+from oracle.decoder import round_to
 
 pytestmark = pytest.mark.gpu
 
@@ -123,5 +124,80 @@ def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_perm
             ey = np.abs(_np(g["y"]) - y_ref)
             assert np.all(ey <= 2.0 ** -7 * np.abs(y_ref) + 1e-3), f"t={t} l={layer}: o-proj"
             worst["y"] = max(worst["y"], float(ey.max()))
+            if "x_next" in g:   # library projections: the next input is bf16(h)
+                np.testing.assert_array_equal(_np(g["x_next"]), round_to(_np(g["h_out"]), "bf16"))
         orc.decoded += 1
     print(f"[decoder] {spec.name}: ok, worst {worst}", flush=True)
+
+
+def _proj_case(rows, K, nq, nkv, seed):
+    import torch
+    from paper_2508_09001_amd import binding as B
+    rng = np.random.default_rng(seed)
+    n = nq + 2 * nkv
+    x = W.round_bf16(rng.standard_normal((rows, K), dtype=np.float32))
+    w = W.round_bf16(rng.standard_normal((K, n), dtype=np.float32) * np.float32(K ** -0.5))
+    xd = torch.from_numpy(x).cuda().to(torch.bfloat16)
+    wd = torch.from_numpy(w).cuda().to(torch.bfloat16)
+    wp = torch.empty_like(wd)
+    B.retro_pack_weight(wd, K, n, wp)
+    q = torch.empty(rows, nq, dtype=torch.bfloat16, device="cuda")
+    k = torch.empty(rows, nkv, dtype=torch.bfloat16, device="cuda")
+    v = torch.empty(rows, nkv, dtype=torch.bfloat16, device="cuda")
+    B.retro_project_qkv(xd, rows, K, wp, nq, nkv, q, k, v)
+    torch.cuda.synchronize()
+    ref = x.astype(np.float64) @ w.astype(np.float64)
+    got = np.concatenate([q.float().cpu().numpy(), k.float().cpu().numpy(),
+                          v.float().cpu().numpy()], axis=1)
+    return got, ref, round_to(ref, "bf16")
+
+
+@pytest.mark.parametrize("rows,K,nq,nkv", [(1, 1024, 256, 64), (5, 2048, 512, 128),
+                                           (17, 4096, 4096, 1024), (34, 1024, 128, 32),
+                                           (48, 3072, 64, 16), (20, 1024, 16, 16)])
+def test_project_qkv_matches_fp64_products(rows, K, nq, nkv):
+    print(f"[proj] qkv rows={rows} K={K} nq={nq} nkv={nkv}", flush=True)
+    got, ref, ref_b = _proj_case(rows, K, nq, nkv, seed=rows * 7 + K)
+    # fp32 accumulation, then one rounding to bf16: within one bf16 step of the
+    # fp64 product, and equal to its rounding for almost every element
+    assert np.all(np.abs(got - ref) <= 2.0 ** -7 * np.abs(ref) + 1e-6)
+    assert np.mean(got == ref_b) > 0.98
+
+
+@pytest.mark.parametrize("rows,K,n", [(1, 1024, 512), (17, 4096, 4096), (40, 2048, 256),
+                                      (18, 1024, 48)])
+def test_project_out_adds_the_residual(rows, K, n):
+    import torch
+    from paper_2508_09001_amd import binding as B
+    print(f"[proj] out rows={rows} K={K} n={n}", flush=True)
+    rng = np.random.default_rng(rows + K + n)
+    o = rng.standard_normal((rows, K)).astype(np.float32)
+    w = W.round_bf16(rng.standard_normal((K, n), dtype=np.float32) * np.float32(K ** -0.5))
+    h0 = rng.standard_normal((rows, n)).astype(np.float32)
+    wd = torch.from_numpy(w).cuda().to(torch.bfloat16)
+    wp = torch.empty_like(wd)
+    B.retro_pack_weight(wd, K, n, wp)
+    h = torch.from_numpy(h0).cuda()
+    xn = torch.empty(rows, n, dtype=torch.bfloat16, device="cuda")
+    B.retro_project_out(torch.from_numpy(o).cuda(), rows, K, wp, n, h, xn)
+    torch.cuda.synchronize()
+    y_ref = round_to(round_to(o, "bf16").astype(np.float64) @ w.astype(np.float64), "bf16")
+    hn = h.cpu().numpy()
+    err = np.abs(hn.astype(np.float64) - (h0.astype(np.float64) + y_ref))
+    assert np.all(err <= 2.0 ** -7 * np.abs(y_ref) + 1e-6 * (1 + np.abs(h0)))
+    np.testing.assert_array_equal(xn.float().cpu().numpy(), round_to(hn, "bf16"))
+
+
+def test_projection_shape_errors_are_reported_before_any_launch():
+    import torch
+    from paper_2508_09001_amd import binding as B
+    x = torch.zeros(4, 1024, dtype=torch.bfloat16, device="cuda")
+    wp = torch.zeros(1024, 96, dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros(4, 64, dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros(4, 16, dtype=torch.bfloat16, device="cuda")
+    for rows, K in [(49, 1024), (4, 512), (4, 1000)]:
+        with pytest.raises(RuntimeError):
+            B.retro_project_qkv(x, rows, K, wp, 64, 16, q, kv, kv)
+    B.retro_project_qkv(x, 0, 1024, wp, 64, 16, q, kv, kv)   # no rows: nothing to do
+    with pytest.raises(RuntimeError):
+        B.retro_pack_weight(wp, 1000, 96, wp)
