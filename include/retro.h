@@ -306,6 +306,22 @@ retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const voi
                                int32_t n_q, int32_t n_kv, void* q, void* k_out, void* v,
                                void* stream);
 
+/* retro_project_qkv for the window rows of one decoder layer (rows = batch *
+ * (W+1), x [batch][W+1][k] bf16, a packed [k][(h_q + 2 h_k) d] weight) with the
+ * layer's UpdateKV folded in (Alg. 1; Sec. 3.3): q [batch][W+1][h_q][d] receives
+ * every row's query; k_new, v_new [batch][h_k][d] the newest row's key and value
+ * (for retro_step, which appends them); the keys and values of the n_update rows
+ * before the newest overwrite the sequence's last n_update stored tokens, as
+ * retro_update_kv would (positions seq_lens[b] - n_update .. seq_lens[b] - 1,
+ * those below 0 skipped), and the digests of the pages they touch are
+ * recomputed.  Call it before the step, whose append advances seq_lens.  bf16
+ * dims only; 0 <= n_update <= W; rows <= 48, k % 1024 == 0, batch <= 48 (else
+ * RETRO_EUNSUPPORTED). */
+retro_status retro_project_qkv_update(const retro_dims* dims, const retro_kv_cache* cache,
+                                      const void* x, int32_t k, const void* w_packed,
+                                      int32_t n_update, void* q, void* k_new, void* v_new,
+                                      void* stream);
+
 /* The output projection and the residual add: y = bf16(o) . Wo for o [rows][k]
  * fp32 (a decoder's merged outputs o_out, k = h_q * d) and a packed [k][n]
  * weight, rounded to bf16; then h[r][j] += y[r][j] in fp32 (h [rows][n], the

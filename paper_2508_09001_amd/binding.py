@@ -23,7 +23,7 @@ EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_worksp
             "retro_decode_attend",
             "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_merge_output_cache", "retro_step", "retro_pack_weight", "retro_project_qkv",
-            "retro_project_out")
+            "retro_project_qkv_update", "retro_project_out")
 
 
 class RetroError(RuntimeError):
@@ -93,6 +93,8 @@ def load_library(path: str = LIB_PATH):
         "retro_pack_weight": ([P, i32, i32, P, P], C.c_int),
         "retro_project_qkv": ([P, i32, i32, P, i32, i32, P, P, P, P], C.c_int),
         "retro_project_out": ([P, i32, i32, P, i32, P, P, P], C.c_int),
+        "retro_project_qkv_update": ([D, C.POINTER(KVCache), P, i32, P, i32, P, P, P, P],
+                                     C.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -224,3 +226,11 @@ def retro_project_qkv(x, rows: int, k: int, w_packed, n_q: int, n_kv: int, q, k_
 def retro_project_out(o, rows: int, k: int, w_packed, n: int, h, x_next, stream=None) -> None:
     _check(load_library().retro_project_out(_ptr(o), rows, k, _ptr(w_packed), n, _ptr(h),
                                             _ptr(x_next), _stream(stream)), "retro_project_out")
+
+
+def retro_project_qkv_update(dims: Dims, cache: KVCache, x, k: int, w_packed, n_update: int, q,
+                             k_new, v_new, stream=None) -> None:
+    _check(load_library().retro_project_qkv_update(C.byref(dims), C.byref(cache), _ptr(x), k,
+                                                   _ptr(w_packed), n_update, _ptr(q),
+                                                   _ptr(k_new), _ptr(v_new), _stream(stream)),
+           "retro_project_qkv_update")

@@ -212,6 +212,23 @@ retro_status retro_update_kv(const retro_dims* dims, const retro_kv_cache* cache
   return from_hip(retro::launch_update_kv(g, *cache, n_tokens, k_upd, v_upd, (hipStream_t)stream));
 }
 
+retro_status retro_project_qkv_update(const retro_dims* dims, const retro_kv_cache* cache,
+                                      const void* x, int32_t k, const void* w_packed,
+                                      int32_t n_update, void* q, void* k_new, void* v_new,
+                                      void* stream) {
+  Geometry g;
+  retro_status st = make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  if (!cache_ok(cache) || !x || !w_packed || !q || !k_new || !v_new || k <= 0 ||
+      n_update < 0 || n_update > g.W)
+    return RETRO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(x) & 15u) || (reinterpret_cast<uintptr_t>(w_packed) & 15u))
+    return RETRO_EINVAL;
+  if (!retro::project_qkv_update_supported(g, k)) return RETRO_EUNSUPPORTED;
+  return from_hip(retro::launch_project_qkv_update(g, *cache, x, k, w_packed, n_update, q, k_new,
+                                                   v_new, (hipStream_t)stream));
+}
+
 retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void* q_cur,
                                 const retro_kv_cache* cache, const retro_selection* sel,
                                 void* workspace, size_t ws_bytes, void* stream) {

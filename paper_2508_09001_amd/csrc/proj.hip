@@ -68,11 +68,27 @@ struct ProjArgs {
   // output projection: h [rows][N] f32 += bf16(y); x_next = bf16(h)
   float* h;
   bf16_t* x_next;
+  // QKV with UpdateKV (rows = batch * W1 window rows): row W1-1 of every
+  // sequence goes to k / v ([batch][nkv]), the n_upd rows before it overwrite the
+  // sequence's last n_upd stored tokens, whose pages' digests are recomputed
+  int W1, n_upd, P, D, hk, max_pages, num_phys;
+  bf16_t *kc, *vc, *dg;
+  const int32_t* pt;
+  const int32_t* seq_lens;
 };
 
-template <int MT, bool OUT, int U>
+constexpr int PJ_MAX_BATCH = 48;
+
+template <int MT, bool OUT, int U, bool UPD = false>
 __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
   __shared__ float red[PJ_WAVES][MT][4][64];
+  __shared__ int s_len[UPD ? PJ_MAX_BATCH : 1];
+  __shared__ uint16_t s_val[UPD ? MT * 16 : 1][16];
+  if constexpr (UPD) {
+    // sequence lengths before the step's append, loaded under the weight stream
+    const int nb = a.rows / a.W1;
+    if ((int)threadIdx.x < nb) s_len[threadIdx.x] = a.seq_lens[threadIdx.x];
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ln16 = lane & 15, g4 = lane >> 4;
   const int tile = blockIdx.x;
@@ -118,6 +134,32 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
       const float hv = a.h[e] + __uint_as_float(uint32_t(y) << 16);
       a.h[e] = hv;
       a.x_next[e].bits = bf16_rne(hv);
+    } else if constexpr (UPD) {
+      s_val[row][l & 15] = y;
+      if (col < a.nq) {
+        a.q[(int64_t)row * a.nq + col].bits = y;
+        continue;
+      }
+      const bool is_k = col < a.nq + a.nkv;
+      const int c = is_k ? col - a.nq : col - a.nq - a.nkv;
+      const int b = row / a.W1, j = row % a.W1;
+      if (j == a.W1 - 1) {  // the step's token: appended by the step itself
+        (is_k ? a.k : a.v)[(int64_t)b * a.nkv + c].bits = y;
+        continue;
+      }
+      const int len = s_len[b];
+      const int pos = len - (a.W1 - 1) + j;  // row j of the window is token t-W+j
+      if (j < a.W1 - 1 - a.n_upd || pos < 0) continue;
+      const int lp = pos / a.P, slot = pos % a.P;
+      if (lp >= a.max_pages) continue;
+      const int phys = a.pt[(int64_t)b * a.max_pages + lp];
+      if (phys < 0 || phys >= a.num_phys) continue;
+      const int h = c / a.D, e = c % a.D;
+      const int64_t ph = (int64_t)phys * a.hk + h;
+      if (is_k)
+        a.kc[(ph * a.P + slot) * a.D + e].bits = y;
+      else
+        a.vc[(ph * a.D + e) * a.P + slot].bits = y;
     } else {
       if (col < a.nq)
         a.q[(int64_t)row * a.nq + col].bits = y;
@@ -125,6 +167,48 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
         a.k[(int64_t)row * a.nkv + (col - a.nq)].bits = y;
       else
         a.v[(int64_t)row * a.nkv + (col - a.nq - a.nkv)].bits = y;
+    }
+  }
+  if constexpr (UPD) {
+    // digests of the pages the update touched, for this workgroup's 16 key
+    // columns: element-wise min / max over every stored key of the page, the
+    // updated ones taken from s_val (a min / max cannot be narrowed in place)
+    const int col0 = tile * 16;
+    if (col0 < a.nq || col0 >= a.nq + a.nkv || a.n_upd == 0) return;
+    __syncthreads();
+    const int c0 = col0 - a.nq, h = c0 / a.D;
+    const int nb = a.rows / a.W1;
+    const int span = (a.n_upd + a.P - 1) / a.P + 1;  // pages a run of n_upd can touch
+    for (int o = threadIdx.x; o < nb * span * 16; o += blockDim.x) {
+      const int cl = o & 15, pi = (o >> 4) % span, b = (o >> 4) / span;
+      const int e = c0 % a.D + cl;
+      const int len = s_len[b];
+      const int start = max(len - a.n_upd, 0);
+      const int lp = start / a.P + pi;
+      if (lp >= a.max_pages || lp * a.P >= len) continue;
+      const int phys = a.pt[(int64_t)b * a.max_pages + lp];
+      if (phys < 0 || phys >= a.num_phys) continue;
+      const int filled = min(a.P, len - lp * a.P);
+      const int64_t ph = (int64_t)phys * a.hk + h;
+      float lo = 0.f, hi = 0.f;
+      for (int sl = 0; sl < filled; ++sl) {
+        const int pos = lp * a.P + sl;
+        float f;
+        if (pos >= start)
+          f = to_f32(bf16_t{s_val[b * a.W1 + (pos - len + a.W1 - 1)][cl]});
+        else
+          f = to_f32(a.kc[(ph * a.P + sl) * a.D + e]);
+        if (sl == 0) {
+          lo = f;
+          hi = f;
+        } else {
+          if (f < lo) lo = f;
+          if (hi < f) hi = f;
+        }
+      }
+      bf16_t* drow = a.dg + (((int64_t)b * a.hk + h) * a.max_pages + lp) * 2 * a.D;
+      drow[e].bits = static_cast<uint16_t>(__float_as_uint(lo) >> 16);
+      drow[a.D + e].bits = static_cast<uint16_t>(__float_as_uint(hi) >> 16);
     }
   }
 }
@@ -142,6 +226,18 @@ void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
     proj_kernel<MT, OUT, 4><<<grid, block, 0, s>>>(a);
   else
     proj_kernel<MT, OUT, 2><<<grid, block, 0, s>>>(a);
+}
+
+template <int MT>
+void launch_proj_upd_mt(const ProjArgs& a, hipStream_t s) {
+  const int per_wave = a.K / 32 / PJ_WAVES;
+  const dim3 grid(a.N / 16), block(64 * PJ_WAVES);
+  if (MT <= 2 && per_wave % 8 == 0)
+    proj_kernel<MT, false, (MT <= 2 ? 8 : 4), true><<<grid, block, 0, s>>>(a);
+  else if (per_wave % 4 == 0)
+    proj_kernel<MT, false, 4, true><<<grid, block, 0, s>>>(a);
+  else
+    proj_kernel<MT, false, 2, true><<<grid, block, 0, s>>>(a);
 }
 
 template <bool OUT>
@@ -185,6 +281,48 @@ bool proj_shape_ok(int rows, int K, int N) {
 }
 
 }  // namespace
+
+hipError_t launch_project_qkv_update(const Geometry& g, const retro_kv_cache& c, const void* x,
+                                     int k, const void* w_packed, int n_upd, void* q,
+                                     void* k_new, void* v_new, hipStream_t s) {
+  ProjArgs a{};
+  a.x = x;
+  a.w = static_cast<const uint4*>(w_packed);
+  a.W1 = g.W + 1;
+  a.rows = g.batch * a.W1;
+  a.K = k;
+  a.nq = g.hq * g.D;
+  a.nkv = g.hk * g.D;
+  a.N = a.nq + 2 * a.nkv;
+  a.q = static_cast<bf16_t*>(q);
+  a.k = static_cast<bf16_t*>(k_new);
+  a.v = static_cast<bf16_t*>(v_new);
+  a.n_upd = n_upd;
+  a.P = g.P;
+  a.D = g.D;
+  a.hk = g.hk;
+  a.max_pages = g.max_pages;
+  a.num_phys = g.num_phys;
+  a.kc = static_cast<bf16_t*>(c.k_cache);
+  a.vc = static_cast<bf16_t*>(c.v_cache);
+  a.dg = static_cast<bf16_t*>(c.digest);
+  a.pt = c.page_table;
+  a.seq_lens = c.seq_lens;
+  const int mt = (a.rows + 15) / 16;
+  if (mt == 1)
+    launch_proj_upd_mt<1>(a, s);
+  else if (mt == 2)
+    launch_proj_upd_mt<2>(a, s);
+  else
+    launch_proj_upd_mt<3>(a, s);
+  return hipGetLastError();
+}
+
+bool project_qkv_update_supported(const Geometry& g, int k) {
+  return g.dtype == RETRO_BF16 && proj_shape_ok(g.batch * (g.W + 1), k, (g.hq + 2 * g.hk) * g.D) &&
+         g.batch <= PJ_MAX_BATCH && g.D % 16 == 0;
+}
+
 }  // namespace retro
 
 extern "C" {

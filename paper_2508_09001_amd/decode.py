@@ -37,11 +37,13 @@ class RetroDecoder:
     ``d_model = h_q * d``.  ``layer_kw`` are the RetroLayer arguments shared by all
     layers (batch, num_kv_heads, group, head_dim, page_size, budget, window,
     max_pages, dtype, budget_permille, ...).  ``library_projections=False`` keeps
-    the products on torch.matmul (for comparison).
+    the products on torch.matmul (for comparison); with the library projections,
+    ``fuse_update`` folds UpdateKV into the query / key / value launch
+    (``retro_project_qkv_update``) instead of a ``retro_update_kv`` of its own.
     """
 
     def __init__(self, weights: Sequence[dict], device: str = "cuda",
-                 library_projections: bool = True, **layer_kw):
+                 library_projections: bool = True, fuse_update: bool = True, **layer_kw):
         self.device = torch.device(device)
         self.layers: List[RetroLayer] = [RetroLayer(device=device, **layer_kw)
                                          for _ in weights]
@@ -88,6 +90,9 @@ class RetroDecoder:
             self.q = torch.zeros(self.batch, self.W + 1, self.hq, self.d, dtype=td, device=dev)
             self.k = torch.zeros(self.batch, self.W + 1, self.hk, self.d, dtype=td, device=dev)
             self.v = torch.zeros_like(self.k)
+            self.k_new = torch.zeros(self.batch, self.hk, self.d, dtype=td, device=dev)
+            self.v_new = torch.zeros_like(self.k_new)
+        self.fuse_update = self.fused and fuse_update
 
     def prefill(self, layer: int, seq: int, k, v, stream=None) -> None:
         """Prompt keys and values [n][h_k][d] of one sequence in one layer."""
@@ -141,14 +146,22 @@ class RetroDecoder:
         for lay, (pq, po) in zip(self.layers, self.packed):
             h_in = self.h.clone() if trace is not None else None
             x_in = self.x.clone() if trace is not None else None
-            B.retro_project_qkv(self.x, b * rows, self.d_model, pq, nq, nkv, self.q, self.k,
-                                self.v)
-            if n_upd > 0:
-                lay.update_kv(self.k[:, W - n_upd:W], self.v[:, W - n_upd:W])
-            lay.step(t, self.q, self.k[:, W], self.v[:, W])
+            if self.fuse_update:
+                B.retro_project_qkv_update(lay.dims, lay.cache, self.x, self.d_model, pq, n_upd,
+                                           self.q, self.k_new, self.v_new)
+                k_new, v_new = self.k_new, self.v_new
+            else:
+                B.retro_project_qkv(self.x, b * rows, self.d_model, pq, nq, nkv, self.q, self.k,
+                                    self.v)
+                if n_upd > 0:
+                    lay.update_kv(self.k[:, W - n_upd:W], self.v[:, W - n_upd:W])
+                k_new, v_new = self.k[:, W], self.v[:, W]
+            lay.step(t, self.q, k_new, v_new)
             B.retro_project_out(lay.o_out, b * rows, nq, po, self.d_model, self.h, self.x)
             if trace is not None:
-                trace.append(dict(x=x_in, q=self.q.clone(), k=self.k.clone(), v=self.v.clone(),
+                kv = (dict(k_new=self.k_new.clone(), v_new=self.v_new.clone())
+                      if self.fuse_update else dict(k=self.k.clone(), v=self.v.clone()))
+                trace.append(dict(x=x_in, q=self.q.clone(), **kv,
                                   o_out=lay.o_out.clone(), lse_out=lay.lse_out.clone(),
                                   selected=lay.selected.clone(), mask=lay.mask.clone(),
                                   num_selected=lay.num_selected.clone(), h_in=h_in,

@@ -8,8 +8,10 @@
 * bf16, layer by layer: each layer's projections are checked against the
   oracle's fp64 products of the same bf16 inputs (within one bf16 rounding), then
   the GPU's own bf16 queries, keys and values are handed to the oracle layer, so
-  that selection, mask and A compare bit for bit and the merged outputs within
-  2e-3, as for a single layer.
+  that selection, mask, A and every page digest compare bit for bit and the
+  merged outputs within 2e-3, as for a single layer.  With UpdateKV folded into
+  the projection launch the past rows' keys and values are read back from the
+  GPU cache.
 """
 from __future__ import annotations
 
@@ -27,12 +29,12 @@ def _inputs(spec, layers):
     return inp, inp.weights()
 
 
-def _build(spec, layers):
+def _build(spec, layers, fuse_update=True):
     import torch
     from oracle.decoder import OracleDecoder
     from paper_2508_09001_amd.decode import RetroDecoder, layer_kwargs
     inp, weights = _inputs(spec, layers)
-    dec = RetroDecoder(weights, **layer_kwargs(spec))
+    dec = RetroDecoder(weights, fuse_update=fuse_update, **layer_kwargs(spec))
     orc = OracleDecoder(spec, weights)
     for layer in range(layers):
         for b, (k, v) in enumerate(inp.prefill(layer)):
@@ -84,16 +86,31 @@ def test_decoder_fp32_free_running_matches_oracle():
     print(f"[decoder] {spec.name}: ok, worst abs error {worst:.3g}", flush=True)
 
 
-@pytest.mark.parametrize("window,budget_permille", [(4, 0), (8, 150), (0, 0)])
-def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_permille):
+def _cache_rows(lay, b, positions):
+    """Keys and values [n][h_k][d] of sequence b at the given positions, read back
+    from the layer's paged cache."""
+    pt = lay.page_table.cpu().numpy()
+    kc, vc = lay.k_cache.float().cpu().numpy(), lay.v_cache.float().cpu().numpy()
+    P = lay.P
+    k = np.stack([kc[pt[b, p // P], :, p % P, :] for p in positions])
+    v = np.stack([vc[pt[b, p // P], :, :, p % P] for p in positions])
+    return k, v
+
+
+@pytest.mark.parametrize("window,budget_permille,fuse", [(4, 0, True), (8, 150, True),
+                                                         (0, 0, True), (4, 0, False),
+                                                         (16, 0, True)])
+def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_permille, fuse):
+    """fuse: UpdateKV inside the projection launch (the past rows' keys and values
+    are then read back from the cache and the digests compared exactly)."""
     import torch
     spec = W.Spec(name="dec-bf16-llama-heads", batch=2, num_kv_heads=8, group=4, head_dim=128,
-                  page_size=16, budget=256, window=window, steps=7, dtype="bf16",
-                  prefill=(1500, 2047), budget_permille=budget_permille)
+                  page_size=16, budget=256, window=window, steps=7 if window < 16 else 20,
+                  dtype="bf16", prefill=(1500, 2047), budget_permille=budget_permille)
     layers = 2
-    print(f"[decoder] {spec.name}: W={window} permille={budget_permille} layers={layers}",
-          flush=True)
-    inp, dec, orc = _build(spec, layers)
+    print(f"[decoder] {spec.name}: W={window} permille={budget_permille} fuse={fuse} "
+          f"layers={layers}", flush=True)
+    inp, dec, orc = _build(spec, layers, fuse_update=fuse)
     emb = np.zeros((spec.batch, spec.window + 1, inp.d_model), np.float32)
     worst = {"proj": 0.0, "o": 0.0, "y": 0.0}
     for t in range(spec.steps):
@@ -108,14 +125,41 @@ def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_perm
             x = _np(g["x"])
             if layer == 0:
                 np.testing.assert_array_equal(x, W.round_bf16(emb))
-            q, k, v = (_np(g[n]) for n in ("q", "k", "v"))
-            for got, ref in zip((q, k, v), orc.project(layer, x)):
+            q = _np(g["q"])
+            refs = orc.project(layer, x)
+            if fuse:
+                # rows W-n .. W-1 went straight to the cache, row W to k_new / v_new
+                k = np.zeros_like(refs[1])
+                v = np.zeros_like(refs[2])
+                k[:, -1], v[:, -1] = _np(g["k_new"]), _np(g["v_new"])
+                for b in range(spec.batch):
+                    L = int(orc.layers[layer].seq_lens[b])
+                    pos = list(range(L - n_upd, L))
+                    if pos:
+                        kb, vb = _cache_rows(dec.layers[layer], b, pos)
+                        k[b, spec.window - n_upd:spec.window] = kb
+                        v[b, spec.window - n_upd:spec.window] = vb
+                rows = list(range(spec.window - n_upd, spec.window + 1))
+                checks = ((q, refs[0]), (k[:, rows], refs[1][:, rows]),
+                          (v[:, rows], refs[2][:, rows]))
+            else:
+                k, v = _np(g["k"]), _np(g["v"])
+                checks = zip((q, k, v), refs)
+            for got, ref in checks:
                 err = np.abs(got - ref)
                 assert np.all(err <= 2.0 ** -7 * np.abs(ref) + 1e-3), f"t={t} l={layer}: proj"
                 worst["proj"] = max(worst["proj"], float(err.max()))
             r = orc.attend_layer(layer, t, q, k, v, n_upd)
             _same_selection(t, layer, g, r, _np(dec.layers[layer].last_loaded),
                             orc.layers[layer].A)
+            # digests of every stored page (the re-embedded ones recomputed)
+            dg = _np(dec.layers[layer].digest).reshape(spec.batch, spec.num_kv_heads,
+                                                       spec.max_pages, 2, spec.head_dim)
+            ol = orc.layers[layer]
+            for b in range(spec.batch):
+                npg = -(-int(ol.seq_lens[b]) // spec.page_size)
+                np.testing.assert_array_equal(dg[b, :, :npg, 0], ol.kmin[b, :, :npg])
+                np.testing.assert_array_equal(dg[b, :, :npg, 1], ol.kmax[b, :, :npg])
             o = _np(g["o_out"])
             eo = float(np.max(np.abs(o - r["o_out"])))
             assert eo <= 2e-3, f"t={t} l={layer}: max |O - O_ref| = {eo:.3g}"
