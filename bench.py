@@ -60,6 +60,9 @@ def _args():
                         "re-embedding, timed per token at each --decoder-windows value")
     p.add_argument("--decoder-windows", default="0,2,4,8,16",
                    help="windows W compared in --decoder mode")
+    p.add_argument("--decoder-batch", type=int, default=None,
+                   help="in --decoder mode, sequences decoded together (all at the workload's "
+                        "first context length)")
     p.add_argument("--decoder-torch-proj", action="store_true",
                    help="in --decoder mode, run the projections on torch.matmul instead")
     p.add_argument("--calib-copy", action="store_true",
@@ -310,6 +313,9 @@ def decoder_bench(args):
     base = W.config(args.config)
     if args.budget_permille is not None:
         base = base.replace(budget_permille=args.budget_permille)
+    if args.decoder_batch is not None:
+        base = base.replace(batch=args.decoder_batch,
+                            prefill=(base.prefill[0],) * args.decoder_batch)
     windows = [int(x) for x in args.decoder_windows.split(",")]
     L = args.decoder
     warmup = max(args.warmup, max(windows) + 1)   # every past row re-embedded from then on
@@ -331,7 +337,7 @@ def decoder_bench(args):
                  randn(n, spec0.num_kv_heads, spec0.head_dim)) for n in spec0.prefill]
                for _ in range(L)]
     emb = randn(spec0.batch, need + max(windows), dm)
-    ms = {}
+    ms, lib_proj = {}, {}
     for w in windows:
         spec = spec0.replace(window=w)
         dec = RetroDecoder(weights, library_projections=not args.decoder_torch_proj,
@@ -358,8 +364,10 @@ def decoder_bench(args):
         e1.record()
         torch.cuda.synchronize()
         ms[w] = e0.elapsed_time(e1) / args.steps
-        print(f"[decoder] W={w}: {ms[w]:.4f} ms/token over {L} layers", file=sys.stderr,
+        print(f"[decoder] W={w}: {ms[w]:.4f} ms/token over {L} layers, batch {spec.batch}, "
+              f"projections {'library' if dec.fused else 'torch.matmul'}", file=sys.stderr,
               flush=True)
+        lib_proj[w] = bool(dec.fused)
         del graphs, dec, wins
         torch.cuda.empty_cache()
     w_main = max(windows)
@@ -382,7 +390,8 @@ def decoder_bench(args):
                    "d_model": dm, "budget_tokens": spec0.budget,
                    "budget_permille": spec0.budget_permille, "window": w_main,
                    "launch": "hip-graph per token",
-                   "projections": "torch.matmul" if args.decoder_torch_proj else "library"},
+                   "projections": {str(w): "library" if v else "torch.matmul"
+                                   for w, v in lib_proj.items()}},
         "ms_per_token_by_window": {str(w): round(v, 4) for w, v in ms.items()},
         "tokens_per_s_by_window": {str(w): round(spec0.batch * 1000.0 / v, 1)
                                    for w, v in ms.items()},

@@ -280,7 +280,7 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
 
 /* ---- Projections of the multi-layer decode with re-embedding (Sec. 3.3) --------
  * Every layer projects the W+1 window rows of every sequence (rows = batch*(W+1),
- * at most 48) to queries, keys and values, and its merged outputs back to the
+ * at most 112) to queries, keys and values, and its merged outputs back to the
  * model width; the past rows are re-embedded from the layer below's updated
  * outputs, their new keys and values then go to retro_update_kv.  With so few
  * rows the products are bound by reading the weights, which are therefore kept
@@ -300,7 +300,7 @@ retro_status retro_pack_weight(const void* w, int32_t k, int32_t n, void* w_pack
  * [k][n_q + 2 n_kv] weight whose columns are Wq's, then Wk's, then Wv's; outputs
  * bf16 [rows][n_q], [rows][n_kv], [rows][n_kv] (for the window rows of a
  * decoder: [batch][W+1][h_q][d] and [batch][W+1][h_k][d]).  Supported: 1 <= rows
- * <= 48, k % 1024 == 0, n_q % 16 == n_kv % 16 == 0 (else RETRO_EUNSUPPORTED);
+ * <= 112, k % 1024 == 0, n_q % 16 == n_kv % 16 == 0 (else RETRO_EUNSUPPORTED);
  * rows == 0 does nothing. */
 retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const void* w_packed,
                                int32_t n_q, int32_t n_kv, void* q, void* k_out, void* v,
@@ -315,7 +315,7 @@ retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const voi
  * retro_update_kv would (positions seq_lens[b] - n_update .. seq_lens[b] - 1,
  * those below 0 skipped), and the digests of the pages they touch are
  * recomputed.  Call it before the step, whose append advances seq_lens.  bf16
- * dims only; 0 <= n_update <= W; rows <= 48, k % 1024 == 0, batch <= 48 (else
+ * dims only; 0 <= n_update <= W; rows <= 112, k % 1024 == 0 (else
  * RETRO_EUNSUPPORTED). */
 retro_status retro_project_qkv_update(const retro_dims* dims, const retro_kv_cache* cache,
                                       const void* x, int32_t k, const void* w_packed,

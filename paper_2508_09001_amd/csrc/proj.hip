@@ -25,7 +25,7 @@ namespace {
 
 constexpr int PJ_WAVES = 16;         // wavefronts per workgroup, each a slice of the reduction
 constexpr int PJ_MIN_STEPS = 2;      // 32-element reduction steps per wavefront (at least)
-constexpr int PJ_MAX_ROW_TILES = 3;  // up to 48 rows
+constexpr int PJ_MAX_ROW_TILES = 7;  // up to 112 rows (more would spill registers)
 
 __device__ __forceinline__ uint16_t bf16_rne(float x) {
   const uint32_t u = __float_as_uint(x);
@@ -77,11 +77,11 @@ struct ProjArgs {
   const int32_t* seq_lens;
 };
 
-constexpr int PJ_MAX_BATCH = 48;
+constexpr int PJ_MAX_BATCH = 16 * PJ_MAX_ROW_TILES;
 
 template <int MT, bool OUT, int U, bool UPD = false>
 __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
-  __shared__ float red[PJ_WAVES][MT][4][64];
+  __shared__ float red[PJ_WAVES][4][64];
   __shared__ int s_len[UPD ? PJ_MAX_BATCH : 1];
   __shared__ uint16_t s_val[UPD ? MT * 16 : 1][16];
   if constexpr (UPD) {
@@ -114,19 +114,22 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
       for (int mt = 0; mt < MT; ++mt)
         acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt], b[u], acc[mt], 0, 0, 0);
   }
+  // row tile by row tile through one LDS buffer: output (i, l) of tile mt is
+  // row mt*16 + 4*(l/16) + i, column tile*16 + l%16
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MT; ++mt) {
+    if (mt > 0) __syncthreads();  // the previous tile's sums are read
 #pragma unroll
-    for (int i = 0; i < 4; ++i) red[wave][mt][i][lane] = acc[mt][i];
-  __syncthreads();
-  // output (mt, i, l): row mt*16 + 4*(l/16) + i, column tile*16 + l%16
-  for (int o = threadIdx.x; o < MT * 256; o += blockDim.x) {
-    const int mt = o >> 8, i = (o >> 6) & 3, l = o & 63;
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[mt][i];
+    __syncthreads();
+    const int o = threadIdx.x;
+    if (o >= 256) continue;
+    const int i = o >> 6, l = o & 63;
     const int row = mt * 16 + 4 * (l >> 4) + i;
     if (row >= a.rows) continue;
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < PJ_WAVES; ++w) sum += red[w][mt][i][l];
+    for (int w = 0; w < PJ_WAVES; ++w) sum += red[w][i][l];
     const int col = tile * 16 + (l & 15);
     const uint16_t y = bf16_rne(sum);
     if constexpr (OUT) {
@@ -213,42 +216,37 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
   }
 }
 
-template <int MT, bool OUT>
+// The most reduction steps per pass whose operands fit the registers: 8 for
+// one or two row tiles, 4 for three or four, 2 beyond.
+constexpr int max_unroll(int mt) { return mt <= 2 ? 8 : mt <= 4 ? 4 : 2; }
+
+template <int MT, bool OUT, bool UPD>
 void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
-  // as many reduction steps per pass as the wavefront's share allows (up to 8;
-  // 4 for three row tiles, whose operands would not fit the registers), so that
-  // a share takes as few dependent round trips to memory as possible
+  // as many reduction steps per pass as the wavefront's share and the registers
+  // allow, so that a share takes as few dependent round trips to memory as
+  // possible (the share, K / 512 steps, is even)
+  constexpr int UM = max_unroll(MT);
   const int per_wave = a.K / 32 / PJ_WAVES;
   const dim3 grid(a.N / 16), block(64 * PJ_WAVES);
-  if (MT <= 2 && per_wave % 8 == 0)
-    proj_kernel<MT, OUT, (MT <= 2 ? 8 : 4)><<<grid, block, 0, s>>>(a);
-  else if (per_wave % 4 == 0)
-    proj_kernel<MT, OUT, 4><<<grid, block, 0, s>>>(a);
+  if (per_wave % UM == 0)
+    proj_kernel<MT, OUT, UM, UPD><<<grid, block, 0, s>>>(a);
+  else if (UM > 4 && per_wave % 4 == 0)
+    proj_kernel<MT, OUT, (UM > 4 ? 4 : 2), UPD><<<grid, block, 0, s>>>(a);
   else
-    proj_kernel<MT, OUT, 2><<<grid, block, 0, s>>>(a);
+    proj_kernel<MT, OUT, 2, UPD><<<grid, block, 0, s>>>(a);
 }
 
-template <int MT>
-void launch_proj_upd_mt(const ProjArgs& a, hipStream_t s) {
-  const int per_wave = a.K / 32 / PJ_WAVES;
-  const dim3 grid(a.N / 16), block(64 * PJ_WAVES);
-  if (MT <= 2 && per_wave % 8 == 0)
-    proj_kernel<MT, false, (MT <= 2 ? 8 : 4), true><<<grid, block, 0, s>>>(a);
-  else if (per_wave % 4 == 0)
-    proj_kernel<MT, false, 4, true><<<grid, block, 0, s>>>(a);
-  else
-    proj_kernel<MT, false, 2, true><<<grid, block, 0, s>>>(a);
-}
-
-template <bool OUT>
+template <bool OUT, bool UPD>
 hipError_t launch_proj(const ProjArgs& a, hipStream_t s) {
-  const int mt = (a.rows + 15) / 16;
-  if (mt == 1)
-    launch_proj_mt<1, OUT>(a, s);
-  else if (mt == 2)
-    launch_proj_mt<2, OUT>(a, s);
-  else
-    launch_proj_mt<3, OUT>(a, s);
+  switch ((a.rows + 15) / 16) {
+    case 1: launch_proj_mt<1, OUT, UPD>(a, s); break;
+    case 2: launch_proj_mt<2, OUT, UPD>(a, s); break;
+    case 3: launch_proj_mt<3, OUT, UPD>(a, s); break;
+    case 4: launch_proj_mt<4, OUT, UPD>(a, s); break;
+    case 5: launch_proj_mt<5, OUT, UPD>(a, s); break;
+    case 6: launch_proj_mt<6, OUT, UPD>(a, s); break;
+    default: launch_proj_mt<7, OUT, UPD>(a, s); break;
+  }
   return hipGetLastError();
 }
 
@@ -308,14 +306,7 @@ hipError_t launch_project_qkv_update(const Geometry& g, const retro_kv_cache& c,
   a.dg = static_cast<bf16_t*>(c.digest);
   a.pt = c.page_table;
   a.seq_lens = c.seq_lens;
-  const int mt = (a.rows + 15) / 16;
-  if (mt == 1)
-    launch_proj_upd_mt<1>(a, s);
-  else if (mt == 2)
-    launch_proj_upd_mt<2>(a, s);
-  else
-    launch_proj_upd_mt<3>(a, s);
-  return hipGetLastError();
+  return launch_proj<false, true>(a, s);
 }
 
 bool project_qkv_update_supported(const Geometry& g, int k) {
@@ -362,7 +353,7 @@ retro_status retro_project_qkv(const void* x, int32_t rows, int32_t k, const voi
   a.q = static_cast<retro::bf16_t*>(q);
   a.k = static_cast<retro::bf16_t*>(k_out);
   a.v = static_cast<retro::bf16_t*>(v);
-  return retro::status_of(retro::launch_proj<false>(a, (hipStream_t)stream));
+  return retro::status_of(retro::launch_proj<false, false>(a, (hipStream_t)stream));
 }
 
 retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const void* w_packed,
@@ -379,7 +370,7 @@ retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const vo
   a.N = n;
   a.h = h;
   a.x_next = static_cast<retro::bf16_t*>(x_next);
-  return retro::status_of(retro::launch_proj<true>(a, (hipStream_t)stream));
+  return retro::status_of(retro::launch_proj<true, false>(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -66,12 +66,12 @@ class RetroDecoder:
                 raise ValueError("projection shapes do not match the layer geometry")
             self.weights.append(dw)
         self.decoded = 0  # decode steps run so far
-        # bf16: library projections (weights pre-tiled; the first needs k % 1024 == 0
-        # and at most 48 rows)
+        # bf16: library projections (weights pre-tiled; they need k % 1024 == 0 and
+        # at most 112 rows)
         rows = self.batch * (self.W + 1)
         self.fused = (library_projections and self.dtype == torch.bfloat16 and
                       self.d_model % 1024 == 0 and
-                      (self.hq * self.d) % 1024 == 0 and rows <= 48)
+                      (self.hq * self.d) % 1024 == 0 and rows <= 112)
         if self.fused:
             nq, nkv = self.hq * self.d, self.hk * self.d
             self.packed = []

@@ -97,19 +97,20 @@ def _cache_rows(lay, b, positions):
     return k, v
 
 
-@pytest.mark.parametrize("window,budget_permille,fuse", [(4, 0, True), (8, 150, True),
-                                                         (0, 0, True), (4, 0, False),
-                                                         (16, 0, True)])
-def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_permille, fuse):
+@pytest.mark.parametrize("window,budget_permille,fuse,batch", [(4, 0, True, 2), (8, 150, True, 2),
+                                                               (0, 0, True, 2), (4, 0, False, 2),
+                                                               (16, 0, True, 2), (16, 0, True, 4)])
+def test_decoder_bf16_layers_match_oracle_on_the_same_inputs(window, budget_permille, fuse, batch):
     """fuse: UpdateKV inside the projection launch (the past rows' keys and values
     are then read back from the cache and the digests compared exactly)."""
     import torch
-    spec = W.Spec(name="dec-bf16-llama-heads", batch=2, num_kv_heads=8, group=4, head_dim=128,
-                  page_size=16, budget=256, window=window, steps=7 if window < 16 else 20,
-                  dtype="bf16", prefill=(1500, 2047), budget_permille=budget_permille)
+    spec = W.Spec(name="dec-bf16-llama-heads", batch=batch, num_kv_heads=8, group=4,
+                  head_dim=128, page_size=16, budget=256, window=window,
+                  steps=7 if window < 16 else 20, dtype="bf16",
+                  prefill=(1500, 2047, 777, 1024)[:batch], budget_permille=budget_permille)
     layers = 2
     print(f"[decoder] {spec.name}: W={window} permille={budget_permille} fuse={fuse} "
-          f"layers={layers}", flush=True)
+          f"batch={batch} layers={layers}", flush=True)
     inp, dec, orc = _build(spec, layers, fuse_update=fuse)
     emb = np.zeros((spec.batch, spec.window + 1, inp.d_model), np.float32)
     worst = {"proj": 0.0, "o": 0.0, "y": 0.0}
@@ -198,7 +199,8 @@ def _proj_case(rows, K, nq, nkv, seed):
 
 @pytest.mark.parametrize("rows,K,nq,nkv", [(1, 1024, 256, 64), (5, 2048, 512, 128),
                                            (17, 4096, 4096, 1024), (34, 1024, 128, 32),
-                                           (48, 3072, 64, 16), (20, 1024, 16, 16)])
+                                           (48, 3072, 64, 16), (20, 1024, 16, 16),
+                                           (72, 2048, 256, 64), (112, 1024, 64, 16)])
 def test_project_qkv_matches_fp64_products(rows, K, nq, nkv):
     print(f"[proj] qkv rows={rows} K={K} nq={nq} nkv={nkv}", flush=True)
     got, ref, ref_b = _proj_case(rows, K, nq, nkv, seed=rows * 7 + K)
@@ -209,7 +211,7 @@ def test_project_qkv_matches_fp64_products(rows, K, nq, nkv):
 
 
 @pytest.mark.parametrize("rows,K,n", [(1, 1024, 512), (17, 4096, 4096), (40, 2048, 256),
-                                      (18, 1024, 48)])
+                                      (18, 1024, 48), (72, 4096, 1024), (100, 1024, 256)])
 def test_project_out_adds_the_residual(rows, K, n):
     import torch
     from paper_2508_09001_amd import binding as B
@@ -239,7 +241,7 @@ def test_projection_shape_errors_are_reported_before_any_launch():
     wp = torch.zeros(1024, 96, dtype=torch.bfloat16, device="cuda")
     q = torch.zeros(4, 64, dtype=torch.bfloat16, device="cuda")
     kv = torch.zeros(4, 16, dtype=torch.bfloat16, device="cuda")
-    for rows, K in [(49, 1024), (4, 512), (4, 1000)]:
+    for rows, K in [(113, 1024), (4, 512), (4, 1000)]:
         with pytest.raises(RuntimeError):
             B.retro_project_qkv(x, rows, K, wp, 64, 16, q, kv, kv)
     B.retro_project_qkv(x, 0, 1024, wp, 64, 16, q, kv, kv)   # no rows: nothing to do
