@@ -79,11 +79,11 @@ struct ProjArgs {
 
 constexpr int PJ_MAX_BATCH = 16 * PJ_MAX_ROW_TILES;
 
-template <int MT, bool OUT, int U, bool UPD = false>
+template <int MT, bool OUT, int U, bool UPD = false, int CT = 1>
 __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
   __shared__ float red[PJ_WAVES][4][64];
   __shared__ int s_len[UPD ? PJ_MAX_BATCH : 1];
-  __shared__ uint16_t s_val[UPD ? MT * 16 : 1][16];
+  __shared__ uint16_t s_val[UPD ? CT : 1][UPD ? MT * 16 : 1][16];
   if constexpr (UPD) {
     // sequence lengths before the step's append, loaded under the weight stream
     const int nb = a.rows / a.W1;
@@ -91,19 +91,22 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ln16 = lane & 15, g4 = lane >> 4;
-  const int tile = blockIdx.x;
+  const int tile0 = blockIdx.x * CT;  // CT column tiles share each load of the rows
   const int steps = a.K / 32, per_wave = steps / PJ_WAVES;
   const int s0 = wave * per_wave;
-  const uint4* wp = a.w + ((int64_t)tile * steps + s0) * 64 + lane;
-  f32x4 acc[MT];
+  const uint4* wp = a.w + ((int64_t)tile0 * steps + s0) * 64 + lane;
+  f32x4 acc[CT][MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < CT; ++c)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[c][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   // U steps per pass, every load of the pass issued before its MFMAs
   for (int s = 0; s < per_wave; s += U) {
-    bf16x8 b[U], av[U][MT];
+    bf16x8 b[U][CT], av[U][MT];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      b[u] = bits_to_bf16x8(wp[(int64_t)(s + u) * 64]);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) b[u][c] = bits_to_bf16x8(wp[((int64_t)c * steps + s + u) * 64]);
       const int k = (s0 + s + u) * 32 + 8 * g4;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) av[u][mt] = load_a<OUT>(a.x, a.rows, a.K, mt * 16 + ln16, k);
@@ -111,16 +114,20 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt], b[u], acc[mt], 0, 0, 0);
+      for (int c = 0; c < CT; ++c)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[c][mt] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][mt], b[u][c], acc[c][mt], 0, 0, 0);
   }
-  // row tile by row tile through one LDS buffer: output (i, l) of tile mt is
-  // row mt*16 + 4*(l/16) + i, column tile*16 + l%16
+  // tile by tile through one LDS buffer: output (i, l) of column tile c and row
+  // tile mt is row mt*16 + 4*(l/16) + i, column (tile0 + c)*16 + l%16
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    if (mt > 0) __syncthreads();  // the previous tile's sums are read
+  for (int pass = 0; pass < CT * MT; ++pass) {
+    const int c = pass / MT, mt = pass % MT;
+    if (pass > 0) __syncthreads();  // the previous tile's sums are read
 #pragma unroll
-    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[mt][i];
+    for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc[c][mt][i];
     __syncthreads();
     const int o = threadIdx.x;
     if (o >= 256) continue;
@@ -130,7 +137,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
     float sum = 0.f;
 #pragma unroll
     for (int w = 0; w < PJ_WAVES; ++w) sum += red[w][i][l];
-    const int col = tile * 16 + (l & 15);
+    const int col = (tile0 + c) * 16 + (l & 15);
     const uint16_t y = bf16_rne(sum);
     if constexpr (OUT) {
       const int64_t e = (int64_t)row * a.N + col;
@@ -138,7 +145,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
       a.h[e] = hv;
       a.x_next[e].bits = bf16_rne(hv);
     } else if constexpr (UPD) {
-      s_val[row][l & 15] = y;
+      s_val[c][row][l & 15] = y;
       if (col < a.nq) {
         a.q[(int64_t)row * a.nq + col].bits = y;
         continue;
@@ -176,12 +183,15 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
     // digests of the pages the update touched, for this workgroup's 16 key
     // columns: element-wise min / max over every stored key of the page, the
     // updated ones taken from s_val (a min / max cannot be narrowed in place)
-    const int col0 = tile * 16;
-    if (col0 < a.nq || col0 >= a.nq + a.nkv || a.n_upd == 0) return;
+    if (a.n_upd == 0) return;
     __syncthreads();
-    const int c0 = col0 - a.nq, h = c0 / a.D;
     const int nb = a.rows / a.W1;
     const int span = (a.n_upd + a.P - 1) / a.P + 1;  // pages a run of n_upd can touch
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+    const int col0 = (tile0 + c) * 16;
+    if (col0 < a.nq || col0 >= a.nq + a.nkv) continue;
+    const int c0 = col0 - a.nq, h = c0 / a.D;
     for (int o = threadIdx.x; o < nb * span * 16; o += blockDim.x) {
       const int cl = o & 15, pi = (o >> 4) % span, b = (o >> 4) / span;
       const int e = c0 % a.D + cl;
@@ -198,7 +208,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
         const int pos = lp * a.P + sl;
         float f;
         if (pos >= start)
-          f = to_f32(bf16_t{s_val[b * a.W1 + (pos - len + a.W1 - 1)][cl]});
+          f = to_f32(bf16_t{s_val[c][b * a.W1 + (pos - len + a.W1 - 1)][cl]});
         else
           f = to_f32(a.kc[(ph * a.P + sl) * a.D + e]);
         if (sl == 0) {
@@ -213,6 +223,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
       drow[e].bits = static_cast<uint16_t>(__float_as_uint(lo) >> 16);
       drow[a.D + e].bits = static_cast<uint16_t>(__float_as_uint(hi) >> 16);
     }
+    }
   }
 }
 
@@ -225,9 +236,22 @@ void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
   // as many reduction steps per pass as the wavefront's share and the registers
   // allow, so that a share takes as few dependent round trips to memory as
   // possible (the share, K / 512 steps, is even)
+  // three to five row tiles: two column tiles per workgroup where N allows,
+  // halving the re-reads of the rows (every workgroup reads all of them)
   constexpr int UM = max_unroll(MT);
+  constexpr int CT = (MT >= 3 && MT <= 5) ? 2 : 1;
   const int per_wave = a.K / 32 / PJ_WAVES;
-  const dim3 grid(a.N / 16), block(64 * PJ_WAVES);
+  const dim3 block(64 * PJ_WAVES);
+  if (CT == 2 && a.N % 32 == 0) {
+    const dim3 grid(a.N / 32);
+    constexpr int UC = MT >= 4 ? 2 : UM;  // four or five row tiles: 4 steps would spill
+    if (per_wave % UC == 0)
+      proj_kernel<MT, OUT, UC, UPD, CT><<<grid, block, 0, s>>>(a);
+    else
+      proj_kernel<MT, OUT, 2, UPD, CT><<<grid, block, 0, s>>>(a);
+    return;
+  }
+  const dim3 grid(a.N / 16);
   if (per_wave % UM == 0)
     proj_kernel<MT, OUT, UM, UPD><<<grid, block, 0, s>>>(a);
   else if (UM > 4 && per_wave % 4 == 0)
