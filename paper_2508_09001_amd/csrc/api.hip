@@ -4,6 +4,7 @@
 #include <math.h>
 
 #include "internal.h"
+#include "proj.h"
 
 namespace retro {
 

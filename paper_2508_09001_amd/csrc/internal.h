@@ -98,12 +98,6 @@ hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, i
 // values (k_upd, v_upd: [batch][n][h_k][d]); their pages' digests are recomputed.
 hipError_t launch_update_kv(const Geometry& g, const retro_kv_cache& c, int n, const void* k_upd,
                             const void* v_upd, hipStream_t s);
-// The query / key / value projections of a decoder layer's window rows with
-// UpdateKV of the n_upd past rows folded in (proj.hip); bf16 only.
-hipError_t launch_project_qkv_update(const Geometry& g, const retro_kv_cache& c, const void* x,
-                                     int k, const void* w_packed, int n_upd, void* q,
-                                     void* k_new, void* v_new, hipStream_t s);
-bool project_qkv_update_supported(const Geometry& g, int k);
 // With g.token_pending, the score launch also appends the step's token
 // (k_new, v_new: [batch][h_k][d]) as AppendKV does, without advancing seq_lens.
 // With a selection, counters ([batch * h_k] ints of the workspace, zero

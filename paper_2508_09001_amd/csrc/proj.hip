@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "proj.h"
 
 namespace retro {
 namespace {
