@@ -237,10 +237,12 @@ void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
   // as many reduction steps per pass as the wavefront's share and the registers
   // allow, so that a share takes as few dependent round trips to memory as
   // possible (the share, K / 512 steps, is even)
-  // three to five row tiles: two column tiles per workgroup where N allows,
-  // halving the re-reads of the rows (every workgroup reads all of them)
+  // query / key / value with three to five row tiles: two column tiles per
+  // workgroup where N allows, halving the re-reads of the rows (every workgroup
+  // reads all of them); not for the output projection, whose 4096 columns would
+  // then leave half the compute units without a workgroup
   constexpr int UM = max_unroll(MT);
-  constexpr int CT = (MT >= 3 && MT <= 5) ? 2 : 1;
+  constexpr int CT = (!OUT && MT >= 3 && MT <= 5) ? 2 : 1;
   const int per_wave = a.K / 32 / PJ_WAVES;
   const dim3 block(64 * PJ_WAVES);
   if (CT == 2 && a.N % 32 == 0) {
