@@ -80,9 +80,9 @@ struct ProjArgs {
 
 constexpr int PJ_MAX_BATCH = 16 * PJ_MAX_ROW_TILES;
 
-template <int MT, bool OUT, int U, bool UPD = false, int CT = 1>
-__global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
-  __shared__ float red[PJ_WAVES][4][64];
+template <int MT, bool OUT, int U, bool UPD = false, int CT = 1, int NW = PJ_WAVES>
+__global__ void __launch_bounds__(64 * NW) proj_kernel(ProjArgs a) {
+  __shared__ float red[NW][4][64];
   __shared__ int s_len[UPD ? PJ_MAX_BATCH : 1];
   __shared__ uint16_t s_val[UPD ? CT : 1][UPD ? MT * 16 : 1][16];
   if constexpr (UPD) {
@@ -93,7 +93,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ln16 = lane & 15, g4 = lane >> 4;
   const int tile0 = blockIdx.x * CT;  // CT column tiles share each load of the rows
-  const int steps = a.K / 32, per_wave = steps / PJ_WAVES;
+  const int steps = a.K / 32, per_wave = steps / NW;
   const int s0 = wave * per_wave;
   const uint4* wp = a.w + ((int64_t)tile0 * steps + s0) * 64 + lane;
   f32x4 acc[CT][MT];
@@ -137,7 +137,7 @@ __global__ void __launch_bounds__(64 * PJ_WAVES) proj_kernel(ProjArgs a) {
     if (row >= a.rows) continue;
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < PJ_WAVES; ++w) sum += red[w][i][l];
+    for (int w = 0; w < NW; ++w) sum += red[w][i][l];
     const int col = (tile0 + c) * 16 + (l & 15);
     const uint16_t y = bf16_rne(sum);
     if constexpr (OUT) {
@@ -255,6 +255,15 @@ void launch_proj_mt(const ProjArgs& a, hipStream_t s) {
     return;
   }
   const dim3 grid(a.N / 16);
+  if constexpr (MT == 1) {
+    if ((int)grid.x > compute_units() && (a.K / 32 / 8) % 8 == 0) {
+      // one row tile and more column tiles than compute units: eight wavefronts
+      // per workgroup (two passes of eight steps), so that every workgroup of
+      // the launch is resident at once instead of a second, half-empty round
+      proj_kernel<MT, OUT, 8, UPD, 1, 8><<<grid, dim3(64 * 8), 0, s>>>(a);
+      return;
+    }
+  }
   if (per_wave % UM == 0)
     proj_kernel<MT, OUT, UM, UPD><<<grid, block, 0, s>>>(a);
   else if (UM > 4 && per_wave % 4 == 0)
