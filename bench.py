@@ -78,17 +78,12 @@ def _sha(paths):
     return h.hexdigest()
 
 
-def _step_path():
-    """The launch sequence retro_step takes at the headline shape (the environment
-    switches it reads on every call)."""
-    env = os.environ
-    if env.get("RETRO_STEP_FUSED") == "1":
-        return "single launch"
-    if env.get("RETRO_SELECT_IN_SCORE") == "1":
-        return "three launches: scores + selection, attention, combine"
-    if env.get("RETRO_SCORE_LAUNCH") == "1":
-        return "three launches: scores, selection + attention, combine"
-    return "two launches: scores + selection + attention, combine"
+def _step_path(spec):
+    """The launch sequence retro_step takes for this workload on this GPU (no
+    flags: the library's own choice)."""
+    if spec.batch * spec.num_kv_heads <= 8:
+        return "two launches: scores + selection + attention, combine"
+    return "three or four launches: scores (+ selection), [selection +] attention, combine"
 
 
 def algorithmic_bytes(spec, seq_lens, num_selected):
@@ -280,7 +275,7 @@ def main():
                    "window": spec.window, "update_kv": bool(upd is not None),
                    "layers_rotated": L,
                    "launch": "hip-graph per step",
-                   "step_path": _step_path()},
+                   "step_path": _step_path(spec)},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
@@ -402,6 +397,18 @@ def decoder_bench(args):
     print(json.dumps(result), flush=True)
 
 
+def _cpu_model():
+    """The host CPU's model name, as /proc/cpuinfo reports it."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(spec, pre, budget_s):
     """The CPU oracle on the same workload: untimed ramp-up of the window, then
     decode steps of one layer until the time budget is used."""
@@ -432,6 +439,8 @@ def cpu_baseline(spec, pre, budget_s):
     nb = algorithmic_bytes(spec, orc.seq_lens, last["num_selected"])
     return {"value": round(nb["total"] / (us * 1e-6) / 1e9, 4), "unit": "GB/s",
             "us_per_layer_step": round(us, 1), "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu_model": _cpu_model(), "nproc": len(os.sched_getaffinity(0)),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
             "sample": f"{n} decode steps of one layer of {spec.name} with a full window "
                       f"(steps {spec.window + 1}..{t}), fp64 attention, OpenMP"}
 

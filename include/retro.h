@@ -58,9 +58,25 @@ typedef enum {
 
 typedef enum { RETRO_F32 = 0, RETRO_BF16 = 1 } retro_dtype;
 
+/* Bits of retro_dims.flags.  0 lets retro_step choose its launches (the normal
+ * case); the other bits select a launch sequence explicitly or test the failure
+ * path, with the same results. */
+typedef enum {
+  /* retro_step: the page scores take a launch of their own even where the
+   * scores, selection and attention fit in one launch */
+  RETRO_FLAG_SEPARATE_SCORES = 1,
+  /* retro_step: the selection runs at the end of the score launch (implies a
+   * separate score launch) */
+  RETRO_FLAG_SELECT_IN_SCORES = 2,
+  /* tests of the failure path only: every bounded wait between the workgroups
+   * of a launch gives up after a few polls, as if its producers never came */
+  RETRO_FLAG_TEST_WAIT_TIMEOUT = 4
+} retro_flag;
+
 /* Problem statement of one layer.  Supported: head_dim 64 or 128; page_size
  * 16 or 32; 1 <= group <= 16; 0 <= window <= 64; (window+1)*group <= 1024;
- * page_size <= budget_tokens; 0 <= budget_permille <= 1000; max_pages <= 16384. */
+ * page_size <= budget_tokens; 0 <= budget_permille <= 1000; max_pages <= 16384;
+ * flags a combination of retro_flag bits. */
 typedef struct retro_dims {
   int32_t batch;           /* sequences in the batch                                   */
   int32_t num_kv_heads;    /* h_k                                                      */
@@ -78,6 +94,7 @@ typedef struct retro_dims {
                               1000)) tokens for a sequence of L tokens (the step's
                               token included); 0: B_t = B.  k_max covers the largest
                               B_t of a full page-table row.                          */
+  int32_t flags;           /* retro_flag bits; 0 for normal use                        */
 } retro_dims;
 
 /* The paged KV cache of one layer (Sec. 2.1; pages as in a vLLM-style pool).
@@ -142,11 +159,13 @@ const char* retro_status_string(int32_t status);
 retro_status retro_k_max(const retro_dims* dims, int32_t* k_max);
 
 /* Bytes of scratch the select / attend / step calls need for these dims.  The
- * workspace holds, besides scratch, counters through which the workgroups of
- * one launch hand work to each other: zero-fill it once before its first use,
- * use it with the dims it was sized for only (one of its counters grows by a
- * dims-dependent amount every call instead of returning to zero), and let one
- * call at a time use it (calls sharing a workspace are ordered on one stream). */
+ * workspace holds, besides scratch, the words through which the workgroups of
+ * one launch hand work to each other and a sticky error word: zero-fill it once
+ * before its first use and let one call at a time use it (calls sharing a
+ * workspace are ordered on one stream).  Use it with the dims it was sized for:
+ * a one-launch step (see retro_step) on a workspace last used by a one-launch
+ * step of another geometry sets the error word instead of running (its outputs
+ * are NaN) until the workspace is zero-filled again. */
 retro_status retro_workspace_size(const retro_dims* dims, size_t* bytes);
 
 /* Bulk-store n_tokens tokens of sequence `seq` at positions start_pos ..
@@ -234,6 +253,15 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
                                         const retro_selection* sel, void* workspace,
                                         size_t ws_bytes, void* stream);
 
+/* The page scores, eq. (quest_score) in the fp32 order of retro_select_pages,
+ * that the last retro_step, retro_step_attend_partials or retro_select_pages
+ * call with this workspace computed: copied (asynchronously, on `stream`) to
+ * scores [batch][h_k][max_pages] fp32, device memory.  Entries of pages at or
+ * past a sequence's page count are unspecified.  Meant for checking the scores
+ * bit for bit; workspace as sized by retro_workspace_size for these dims. */
+retro_status retro_copy_scores(const retro_dims* dims, const void* workspace, size_t ws_bytes,
+                               float* scores, void* stream);
+
 /* MergeOutput + CacheOutput (Alg. 1; eq. merged_attn_general) for step t.
  * For each query head and row r with tau = t-W+r >= 0:
  *   r == W   : out = part; pushed to slot t mod W;
@@ -250,28 +278,25 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
- * semantics, without materialising o_part / lse_part.  Two launches where the
- * attention's workgroups all fit on the GPU at once (rtw 1, max_pages <= 2560,
- * no more workgroups than compute units): page scores (with the append),
- * selection and attention, the workgroups of a KV head meeting on a counter
- * kept in `workspace` between scores and selection; then combine + merge (with
- * the last_loaded update and the seq_lens advance).  The meeting needs every
- * workgroup of the launch resident at once: work of other streams or processes
- * holding compute units delays it until they free them; a wait that runs past
- * its bound (tens of milliseconds) sets a sticky word in `workspace`, and that
- * step's outputs, and those of every later step with this workspace until it
- * is zero-filled again, are NaN (RETRO_TEST_WAIT_TIMEOUT=1 in the environment
+ * semantics, without materialising o_part / lse_part.
+ * Two launches where every workgroup of the first fits on the GPU at once (as
+ * the occupancy of its kernel times the compute units tells; up to 2560 pages
+ * per sequence, rtw 1): page scores (with the append), selection and attention,
+ * the workgroups of a KV head exchanging their scores through tagged words in
+ * `workspace`; then combine + merge (with the last_loaded update and the
+ * seq_lens advance).  The exchange needs every workgroup of the first launch
+ * resident at once: work of other streams or processes holding compute units
+ * delays it until they free them; a wait that runs past its bound (tens of
+ * milliseconds) sets the sticky error word in `workspace`: the outputs of that
+ * step and of every later step with this workspace are then NaN, and the
+ * output cache, last_loaded and seq_lens are left as they were, until the
+ * workspace is zero-filled again (RETRO_FLAG_TEST_WAIT_TIMEOUT in dims->flags
  * makes every such wait give up at once, for tests of that path).
- * Otherwise, or with RETRO_SCORE_LAUNCH=1 in the environment (read on every
- * call), the scores take a launch of their own first; with
- * RETRO_SELECT_IN_SCORE=1, or for max_pages > 6144, the selection runs at the
- * end of the score launch (or in a launch of its own) instead of in front of
- * the attention.
- * With RETRO_STEP_FUSED=1 in the environment (read on every call) the step runs
- * as one launch whose workgroups hand work to each other through counters kept
- * in `workspace` (zero-filled once, as for every call).  If a hand-off wait
- * there ever exceeds its bound the launch completes with unspecified outputs
- * instead of hanging. */
+ * Otherwise, or with RETRO_FLAG_SEPARATE_SCORES, the scores take a launch of
+ * their own first and every attention workgroup selects in front of its
+ * attention; with RETRO_FLAG_SELECT_IN_SCORES, or for max_pages > 6144, the
+ * selection runs at the end of the score launch (or in a launch of its own)
+ * instead. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,

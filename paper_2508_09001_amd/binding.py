@@ -17,12 +17,14 @@ LIB_PATH = os.path.join(HERE, "libretro_mi355x.so")
 
 RETRO_OK, RETRO_EINVAL, RETRO_EUNSUPPORTED, RETRO_EHIP, RETRO_EWORKSPACE = 0, -1, -2, -3, -4
 RETRO_F32, RETRO_BF16 = 0, 1
+RETRO_FLAG_SEPARATE_SCORES, RETRO_FLAG_SELECT_IN_SCORES, RETRO_FLAG_TEST_WAIT_TIMEOUT = 1, 2, 4
 
 EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_workspace_size",
             "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
             "retro_decode_attend",
             "retro_decode_attend_partials", "retro_step_attend_partials",
-            "retro_merge_output_cache", "retro_step", "retro_pack_weight", "retro_project_qkv",
+            "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_pack_weight",
+            "retro_project_qkv",
             "retro_project_qkv_update", "retro_project_out")
 
 
@@ -36,7 +38,8 @@ class Dims(C.Structure):
     _fields_ = [("batch", C.c_int32), ("num_kv_heads", C.c_int32), ("group", C.c_int32),
                 ("head_dim", C.c_int32), ("page_size", C.c_int32), ("budget_tokens", C.c_int32),
                 ("window", C.c_int32), ("max_pages", C.c_int32), ("num_phys_pages", C.c_int32),
-                ("dtype", C.c_int32), ("sm_scale", C.c_float), ("budget_permille", C.c_int32)]
+                ("dtype", C.c_int32), ("sm_scale", C.c_float), ("budget_permille", C.c_int32),
+                ("flags", C.c_int32)]
 
 
 class KVCache(C.Structure):
@@ -87,6 +90,7 @@ def load_library(path: str = LIB_PATH):
                                           C.c_size_t, P], C.c_int),
         "retro_step_attend_partials": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
                                           C.c_size_t, P], C.c_int),
+        "retro_copy_scores": ([D, P, C.c_size_t, P, P], C.c_int),
         "retro_merge_output_cache": ([D, i32, P, P, C.POINTER(OutputCache), P, P, P], C.c_int),
         "retro_step": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
                         C.POINTER(OutputCache), P, P, P, C.c_size_t, P], C.c_int),
@@ -192,6 +196,11 @@ def retro_step_attend_partials(dims: Dims, step: int, q_window, cache: KVCache, 
                                                        C.byref(cache), C.byref(sel),
                                                        _ptr(workspace), ws_bytes, _stream(stream)),
            "retro_step_attend_partials")
+
+
+def retro_copy_scores(dims: Dims, workspace, ws_bytes: int, scores, stream=None) -> None:
+    _check(load_library().retro_copy_scores(C.byref(dims), _ptr(workspace), ws_bytes,
+                                            _ptr(scores), _stream(stream)), "retro_copy_scores")
 
 
 def retro_merge_output_cache(dims: Dims, step: int, o_part, lse_part, ocache: OutputCache, o_out,

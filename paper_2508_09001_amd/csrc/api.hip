@@ -1,6 +1,5 @@
 // C ABI entry points: argument validation, geometry and workspace sizing, and the
 // launch sequences of each call.  Nothing here allocates device memory.
-#include <cstdlib>
 #include <math.h>
 
 #include "internal.h"
@@ -36,6 +35,9 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   if (d->budget_tokens < d->page_size) return RETRO_EINVAL;
   if (d->budget_permille < 0 || d->budget_permille > 1000) return RETRO_EINVAL;
   if (d->max_pages > 16384) return RETRO_EUNSUPPORTED;
+  if (d->flags & ~(RETRO_FLAG_SEPARATE_SCORES | RETRO_FLAG_SELECT_IN_SCORES |
+                   RETRO_FLAG_TEST_WAIT_TIMEOUT))
+    return RETRO_EINVAL;
   if ((int64_t)d->batch * d->num_kv_heads > 65535) return RETRO_EUNSUPPORTED;
 
   Geometry x{};
@@ -82,15 +84,7 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.waves = std::max(std::max((x.tiles_per_group + x.rtw - 1) / x.rtw, attend_min_waves(x.dtype, x.D)),
                      kMaxWaves);
   if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
-
-  x.f_rgroups = (x.row_tiles + kFusedWaves - 1) / kFusedWaves;
-  x.f_tpg = (x.row_tiles + x.f_rgroups - 1) / x.f_rgroups;
-  const int f_ppb = fused_score_pages_per_block(x.dtype, x.D);
-  x.fA = (x.max_pages + f_ppb - 1) / f_ppb;
-  x.fC = x.f_rgroups * x.n_splits;
-  x.fD = (x.G * (x.W > 0 ? x.W : 1) + kFusedWaves - 1) / kFusedWaves;
-  x.f_grid = (int64_t)8 * ((bh + 7) / 8) * (x.fA + 1 + x.fC + x.fD);
-  x.fused = fused_supported(x) && x.f_grid < (1LL << 31);
+  x.flags = d->flags;
 
   const size_t bhs = (size_t)bh;
   x.ws_scores = 0;
@@ -101,14 +95,18 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * x.n_splits * x.R * x.D * sizeof(float));
   x.ws_lpart = off;
   off += align256(bhs * x.n_splits * x.R * sizeof(float));
-  x.ws_ctl = off;
-  off += align256((kCtlCounts + 3 * bhs * kCtlStride) * sizeof(int32_t));
+  x.ws_err = off;  // sticky error word (a bounded wait ran out, or a foreign geometry)
+  off += 256;
   x.ws_sel = off;  // per-head counters of the score + selection launch
   off += align256(bhs * kSelCounterInts * (1 + kSelMaxGroups) * sizeof(int32_t));
-  x.ws_tok = off;  // per KV head: the step's token page when not kept (selection in attention)
+  x.ws_tok = off;  // per KV head: the step token's page when not kept (selection in attention)
   off += align256(bhs * sizeof(int32_t));
-  x.ws_full = off;  // per KV head: the arrival counter of the one-launch attention
-  off += align256(bhs * kSelCounterInts * sizeof(int32_t));
+  x.ws_tagged = off;  // the one-launch step's tagged score words, then its key-range words
+  off += align256(bhs * (x.max_pages + 2 * (size_t)x.n_splits * x.n_rgroups) * sizeof(uint64_t));
+  x.ws_heads = off;  // per workgroup of that step: launch count + geometry fingerprint, 128 B each
+  off += align256(bhs * x.n_splits * x.n_rgroups * 128);
+  x.ws_dummy = off;  // never written: the stand-in of empty loads
+  off += 256;
   x.ws_total = off;
   *g = x;
   return RETRO_OK;
@@ -142,6 +140,23 @@ retro_status check_ws(const Geometry& g, void* ws, size_t ws_bytes) {
 }
 
 float* ws_at(void* ws, size_t off) { return reinterpret_cast<float*>((char*)ws + off); }
+
+// retro_step's launch plan: scores, selection and attention in one launch
+// where every workgroup of it fits on the GPU at once and the caller did not
+// ask for a separate score launch
+bool one_launch(const Geometry& g) {
+  return !(g.flags & (RETRO_FLAG_SEPARATE_SCORES | RETRO_FLAG_SELECT_IN_SCORES)) &&
+         retro::step_attend_supported(g);
+}
+
+// bounded waits: RETRO_FLAG_TEST_WAIT_TIMEOUT makes each give up after a few
+// polls, its awaited tag being out of reach
+int wait_limit(const Geometry& g) {
+  return (g.flags & RETRO_FLAG_TEST_WAIT_TIMEOUT) ? 4 : retro::kSpinLimit;
+}
+uint32_t wait_bias(const Geometry& g) {
+  return (g.flags & RETRO_FLAG_TEST_WAIT_TIMEOUT) ? 0x40000000u : 0u;
+}
 
 }  // namespace
 
@@ -260,7 +275,8 @@ retro_status retro_decode_attend(const retro_dims* dims, int32_t step, const voi
   hipStream_t s = (hipStream_t)stream;
   float* o_ws = ws_at(workspace, g.ws_opart);
   float* l_ws = ws_at(workspace, g.ws_lpart);
-  hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, nullptr, o_ws, l_ws, s);
+  hipError_t e = retro::launch_attend(g, step, q_window, *cache, *sel, nullptr, o_ws, l_ws,
+                                      (char*)workspace + g.ws_dummy, s);
   if (e == hipSuccess)
     e = retro::launch_combine_merge(g, step, 0, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
                                     o_part, lse_part, nullptr, nullptr, nullptr, nullptr, s);
@@ -278,7 +294,7 @@ retro_status retro_decode_attend_partials(const retro_dims* dims, int32_t step,
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   return from_hip(retro::launch_attend(g, step, q_window, *cache, *sel, nullptr,
                                        ws_at(workspace, g.ws_opart), ws_at(workspace, g.ws_lpart),
-                                       (hipStream_t)stream));
+                                       (char*)workspace + g.ws_dummy, (hipStream_t)stream));
 }
 
 retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
@@ -293,20 +309,30 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
   if (!retro::attend_selects(g)) return RETRO_EUNSUPPORTED;
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
   int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
-  if (retro::attend_full_supported(g, retro::compute_units())) {
-    uint64_t* cnt = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_full);
-    int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
-    return from_hip(retro::launch_attend_full(g, step, q_window, nullptr, nullptr, *cache, *sel,
-                                              phys, ws_at(workspace, g.ws_scores),
-                                              ws_at(workspace, g.ws_opart),
-                                              ws_at(workspace, g.ws_lpart), tok, cnt, err,
-                                              (hipStream_t)stream));
+  if (one_launch(g)) {
+    int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_err);
+    return from_hip(retro::launch_step_attend(g, step, q_window, nullptr, nullptr, *cache, *sel,
+                                              workspace, ws_at(workspace, g.ws_opart),
+                                              ws_at(workspace, g.ws_lpart), tok, err,
+                                              wait_limit(g), wait_bias(g), (hipStream_t)stream));
   }
   return from_hip(retro::launch_attend_select(g, step, q_window, *cache, *sel, phys,
                                               ws_at(workspace, g.ws_scores),
                                               ws_at(workspace, g.ws_opart),
                                               ws_at(workspace, g.ws_lpart), tok,
-                                              (hipStream_t)stream));
+                                              (char*)workspace + g.ws_dummy, (hipStream_t)stream));
+}
+
+retro_status retro_copy_scores(const retro_dims* dims, const void* workspace, size_t ws_bytes,
+                               float* scores, void* stream) {
+  Geometry g;
+  retro_status st = retro::make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  if (!scores) return RETRO_EINVAL;
+  if (!workspace || ws_bytes < g.ws_total) return RETRO_EWORKSPACE;
+  const size_t n = (size_t)g.batch * g.hk * g.max_pages * sizeof(float);
+  return from_hip(hipMemcpyAsync(scores, (const char*)workspace + g.ws_scores, n,
+                                 hipMemcpyDeviceToDevice, (hipStream_t)stream));
 }
 
 retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, const float* o_part,
@@ -324,29 +350,6 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 
 }  // extern "C"
 
-namespace {
-// The single-launch step is chosen with RETRO_STEP_FUSED=1 in the environment
-// (read on every call); otherwise the step runs as five dependent launches.
-// RETRO_SELECT_IN_SCORE=1: the selection at the end of the score launch
-// instead of in front of the attention
-bool select_in_score_requested() {
-  const char* v = std::getenv("RETRO_SELECT_IN_SCORE");
-  return v && v[0] == '1';
-}
-
-// RETRO_SCORE_LAUNCH=1: the page scores in a launch of their own, before the
-// selection + attention launch
-bool score_launch_requested() {
-  const char* v = std::getenv("RETRO_SCORE_LAUNCH");
-  return v && v[0] == '1';
-}
-
-bool fused_requested() {
-  const char* v = std::getenv("RETRO_STEP_FUSED");
-  return v && v[0] == '1';
-}
-}  // namespace
-
 extern "C" {
 
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
@@ -362,56 +365,54 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   if (g.W > 0 && (!ocache || !ocache->o_cache || !ocache->lse_cache)) return RETRO_EINVAL;
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  if (g.fused && fused_requested())
-    return from_hip(retro::launch_step_fused(g, step, q_window, k_new, v_new, *cache, *sel, ocache,
-                                             o_out, lse_out, workspace, s));
   float* scores = ws_at(workspace, g.ws_scores);
   float* o_ws = ws_at(workspace, g.ws_opart);
   float* l_ws = ws_at(workspace, g.ws_lpart);
   const int64_t qbs = (int64_t)(g.W + 1) * g.hq * g.D;
   const char* q_cur = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
   int32_t* phys = reinterpret_cast<int32_t*>((char*)workspace + g.ws_phys);
-  // score (+ the token's append, + top-k + mask) -> attention -> combine + merge
-  // (+ seq_lens advance)
+  int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
+  int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_err);
+  const void* dummy = (char*)workspace + g.ws_dummy;
+  // the launches of this step append the token in their first launch and use
+  // the length with it; the combine + merge launch advances seq_lens
   Geometry gp = g;
   gp.token_pending = 1;
-  if (retro::attend_full_supported(gp, retro::compute_units()) && !select_in_score_requested() &&
-      !score_launch_requested()) {
+  if (one_launch(gp)) {
     // scores (+ the token's append), selection and attention in one launch ->
     // combine + merge (+ last_loaded update, + seq_lens advance)
-    int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
-    uint64_t* cnt = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_full);
-    int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_ctl) + retro::kCtlError;
-    hipError_t e = retro::launch_attend_full(gp, step, q_window, k_new, v_new, *cache, *sel, phys,
-                                             scores, o_ws, l_ws, tok, cnt, err, s);
+    hipError_t e = retro::launch_step_attend(gp, step, q_window, k_new, v_new, *cache, *sel,
+                                             workspace, o_ws, l_ws, tok, err, wait_limit(g),
+                                             wait_bias(g), s);
     if (e == hipSuccess)
       e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
                                       nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
                                       sel->selected, tok, err);
     return from_hip(e);
   }
-  if (retro::attend_selects(gp) && !select_in_score_requested()) {
+  if (retro::attend_selects(gp) && !(g.flags & RETRO_FLAG_SELECT_IN_SCORES)) {
     // score (+ the token's append) -> attention with the selection in front ->
     // combine + merge (+ last_loaded update, + seq_lens advance)
-    int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
     hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores,
                                        nullptr, nullptr, nullptr, s);
     if (e == hipSuccess)
       e = retro::launch_attend_select(gp, step, q_window, *cache, *sel, phys, scores, o_ws, l_ws,
-                                      tok, s);
+                                      tok, dummy, s);
     if (e == hipSuccess)
       e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
                                       nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
                                       sel->selected, tok);
     return from_hip(e);
   }
+  // score (+ the token's append, + top-k + mask) -> [top-k + mask] -> attention
+  // -> combine + merge (+ seq_lens advance)
   int32_t* counters = reinterpret_cast<int32_t*>((char*)workspace + g.ws_sel);
   hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores, sel, phys,
                                      counters, s);
   if (e == hipSuccess && !retro::score_selects(gp))
     e = retro::launch_topk_mask(gp, step, scores, *cache, *sel, phys, s);
   if (e == hipSuccess)
-    e = retro::launch_attend(gp, step, q_window, *cache, *sel, phys, o_ws, l_ws, s);
+    e = retro::launch_attend(gp, step, q_window, *cache, *sel, phys, o_ws, l_ws, dummy, s);
   if (e == hipSuccess)
     e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr, nullptr,
                                     nullptr, nullptr, ocache, o_out, lse_out, cache, s);

@@ -30,8 +30,6 @@
 //
 // Output: per split and row, the normalised partial output and its natural-log
 // normaliser, combined across splits by the merge kernel.
-#include <cstdlib>
-
 #include "roles.h"
 
 namespace retro {
@@ -49,6 +47,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_kernel(AttendArgs a) {
   __shared__ int s_phys[kMaxSplitPages];
   __shared__ int s_page[kMaxSplitPages];
   __shared__ int s_mask[kMaxSplitPages];
+  __shared__ int s_tok;
   const Geometry& g = a.g;
   // Work units are ordered (sequence, KV head, row group, split), split fastest,
   // and spread so that the units of one KV head share an XCD (workgroups go to
@@ -62,7 +61,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_kernel(AttendArgs a) {
   const int h = u % g.hk, b = u / g.hk;
   attend_role<T, D, RTW, MAXP, RTW == 1, false>(
       a, b, h, rg, split, [&] { return live_seq_len(g, a.seq_lens, a.pt, b); }, lds, s_phys,
-      s_page, s_mask, [] {}, SelectionRows{});
+      s_page, s_mask, &s_tok, -1, [] {}, SelectionRows{});
 }
 
 template <typename T, int D, int RTW>
@@ -155,7 +154,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArg
   __shared__ int s_page[kMaxSplitPages];
   __shared__ int s_mask[kMaxSplitPages];
   __shared__ int l_lp[kMaxSplitPages], l_m[kMaxSplitPages], l_ph[kMaxSplitPages];
-  __shared__ int s_k;
+  __shared__ int s_k, s_tok;
   const Geometry& g = a.g;
   int u = xcd_remap(blockIdx.x, gridDim.x);
   const int split = u % g.n_splits;
@@ -184,7 +183,7 @@ __global__ void __launch_bounds__(kAttendThreads) attend_select_kernel(AttendArg
   };
   attend_role<T, D, RTW, MAXP, RTW == 1, false>(
       a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
-      s_mask, select, [&](int t, int, int& lp, int& m, int& phys) {
+      s_mask, &s_tok, -1, select, [&](int t, int, int& lp, int& m, int& phys) {
         if (t < g.pages_per_split) {
           lp = l_lp[t];
           m = l_m[t];
@@ -216,160 +215,6 @@ hipError_t attend_select_d(const AttendArgs& a, const TopkArgs& ta, int32_t* tok
   return attend_select_p<T, D, 12>(a, ta, tok_out, s);
 }
 
-// Scoring in the same launch (see attend_full_kernel).
-struct ScoreInArgs {
-  const void* q;      // current query rows: sequence b's at q + b * q_bstride
-  int64_t q_bstride;  // elements
-  void* dg;           // digests
-  float* scores;      // [batch][h_k][max_pages]
-  const void* k_new;  // the step's token, [batch][h_k][d]
-  const void* v_new;
-  uint64_t* cnt;      // per KV head: an arrival counter, a 128-byte line each
-  int32_t* err;       // set when a wait runs past its bound
-  int ppb;            // pages scored per workgroup
-  int spin_limit;     // polls before a wait gives up
-  uint64_t target_bias;  // added to every wait's target (a test makes waits time out with it)
-};
-
-// Page scores, the token's append, the selection and the attention in one
-// launch.  Each workgroup of a KV head scores its share of the head's pages
-// (appending the token if its page is in that share), writes the scores (and
-// the token) device-coherently, waits for its own stores, meets at a barrier
-// and counts itself in on the head's arrival counter; then it polls the counter
-// until the whole head has arrived, and runs the selection and attention as
-// attend_select_kernel does.  The host launches this form only when every
-// workgroup fits on the chip at once (no more workgroups than compute units,
-// one per unit), so every wait ends; it is bounded all the same (past
-// kSpinLimit polls the error word is set and the workgroup goes on).
-// The counter is never reset: it grows by the head's workgroup count every
-// launch (64 bits).  Every arrival of a launch precedes every arrival of the
-// next one, which starts after it ends, so a count read by a workgroup of the
-// launch before it counts itself in lies in [n * c, n * c + c - 1] (c: the
-// head's workgroups, n: the launches before) and the workgroup waits for the
-// next multiple of c.  Reading it at the start takes the round trip of a
-// returning atomic off the path of the head's last arrival; resetting the
-// counter instead would take a second counter whose returning atomic kept the
-// selection's first wavefront waiting about a microsecond.
-template <typename T, int D, int PER, int SITERS, int GC>
-__global__ void __launch_bounds__(kAttendThreads) attend_full_kernel(AttendArgs a, TopkArgs ta,
-                                                                     ScoreInArgs sc,
-                                                                     int32_t* tok_out) {
-  using TL = Tiles<T, D>;
-  constexpr int MAXP = (TL::PIECES + kAttendThreads - 1) / kAttendThreads;
-  constexpr int kStageBytes = 2 * TL::BUF_ELEMS * (int)sizeof(T);
-  constexpr int kSelectBytes = (kTopkHistWords + kTopkSmall) * 4;
-  __shared__ __attribute__((aligned(16))) char lds[std::max(kStageBytes, kSelectBytes)];
-  __shared__ int s_phys[kMaxSplitPages];
-  __shared__ int s_page[kMaxSplitPages];
-  __shared__ int s_mask[kMaxSplitPages];
-  __shared__ int l_lp[kMaxSplitPages], l_m[kMaxSplitPages], l_ph[kMaxSplitPages];
-  __shared__ int s_k;
-  const Geometry& g = a.g;
-  int u = xcd_remap(blockIdx.x, gridDim.x);
-  const int split = u % g.n_splits;
-  u /= g.n_splits;
-  const int rg = u % g.n_rgroups;
-  u /= g.n_rgroups;
-  const int h = u % g.hk, b = u / g.hk;
-  const int bh = b * g.hk + h;
-  const int per_head = g.n_splits * g.n_rgroups;
-  const bool writer = split == 0 && rg == 0;
-  const int first = split * g.pages_per_split;
-  const int tid = thread_index();
-  uint64_t* arrive = sc.cnt + (int64_t)bh * (kSelCounterInts / 2);
-  // thread 0: the head's arrival count before this workgroup counts itself in,
-  // read now so that counting in needs no returning atomic (see below)
-  uint64_t before = 0, target = 0;
-  if (tid == 0) before = __hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-  // ---- this workgroup's share of the head's page scores
-  int seq_len = 0, tok_lp = -1, n_pages = 0;
-  {
-    const int page0 = (rg * g.n_splits + split) * sc.ppb;
-    const int page_end = min(page0 + sc.ppb, g.max_pages);
-    score_role<T, D, SITERS, true, GC>(
-        g, page0, page_end,
-        reinterpret_cast<const T*>(sc.q) + b * sc.q_bstride + (int64_t)h * g.G * D,
-        reinterpret_cast<T*>(sc.dg) + (int64_t)bh * g.max_pages * 2 * D,
-        sc.scores + (int64_t)bh * g.max_pages, reinterpret_cast<float*>(lds),
-        [&](int& np) {
-          const int pos = a.seq_lens[b];
-          StepToken<T> tk{-1, 0, nullptr, nullptr, nullptr, nullptr};
-          seq_len = pos;
-          if (g.token_pending) {
-            const int phys = token_phys(g, a.pt, b, pos);
-            if (phys >= 0) {
-              seq_len = pos + 1;
-              tk = make_step_token<T>(g, b, h, pos, phys, sc.k_new, sc.v_new,
-                                      const_cast<void*>(a.kc), const_cast<void*>(a.vc));
-            }
-          }
-          np = n_pages = min((seq_len + g.P - 1) / g.P, g.max_pages);
-          tok_lp = tk.lp;
-          return tk;
-        });
-    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's score and token stores have completed
-    __syncthreads();
-    if (tid == 0) {
-      __hip_atomic_fetch_add(arrive, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      target = (before / per_head + 1) * per_head + sc.target_bias;
-    }
-  }
-
-  // the head's arrival wait, run by the selection once its last_loaded and
-  // page-table loads are in flight and its histograms are cleared
-  auto head_wait = [&] {
-    if (tid == 0) {
-      int it = 0;
-      while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-        if (++it > sc.spin_limit) {
-          __hip_atomic_store(sc.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(8);  // ~0.2 us between polls
-      }
-    }
-    __syncthreads();
-  };
-  auto select = [&] {
-    select_for_split<PER>(ta, bh, first, writer, [&] { return seq_len; }, tok_lp, head_wait,
-                          lds, l_lp, l_m, l_ph, s_k, tok_out);
-  };
-  attend_role<T, D, 1, MAXP, true, false>(
-      a, b, h, rg, split, [&] { return seq_len; }, reinterpret_cast<T*>(lds), s_phys, s_page,
-      s_mask, select, [&](int t, int, int& lp, int& m, int& phys) {
-        if (t < g.pages_per_split) {
-          lp = l_lp[t];
-          m = l_m[t];
-          phys = l_ph[t];
-        }
-        return s_k;
-      });
-}
-
-template <typename T, int D, int PER>
-hipError_t attend_full_p(const AttendArgs& a, const TopkArgs& ta, const ScoreInArgs& sc,
-                         int32_t* tok_out, hipStream_t s) {
-  const Geometry& g = a.g;
-  const int64_t n = (int64_t)g.n_splits * g.n_rgroups * g.hk * g.batch;
-  if (64 * g.waves != kAttendThreads || g.rtw != 1 || g.max_pages > PER * kAttendThreads ||
-      sc.ppb < 1 || sc.ppb > 3 * (kAttendThreads / 64) * 4)
-    return hipErrorInvalidValue;
-  // the headline group size (4 query heads per KV head) gets an unrolled score loop
-  if (g.G == 4)
-    attend_full_kernel<T, D, PER, 3, 4><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
-  else
-    attend_full_kernel<T, D, PER, 3, 0><<<(unsigned)n, kAttendThreads, 0, s>>>(a, ta, sc, tok_out);
-  return hipGetLastError();
-}
-
-template <typename T, int D>
-hipError_t attend_full_d(const AttendArgs& a, const TopkArgs& ta, const ScoreInArgs& sc,
-                         int32_t* tok_out, hipStream_t s) {
-  if (a.g.max_pages <= 2 * kAttendThreads) return attend_full_p<T, D, 2>(a, ta, sc, tok_out, s);
-  return attend_full_p<T, D, 5>(a, ta, sc, tok_out, s);
-}
-
 }  // namespace
 
 int attend_min_waves(int dtype, int D) {
@@ -380,7 +225,7 @@ int attend_min_waves(int dtype, int D) {
 
 AttendArgs make_attend_args(const Geometry& g, int step, const void* q_window,
                             const retro_kv_cache& c, const retro_selection& sel,
-                            const int32_t* sel_phys, float* o_ws, float* l_ws) {
+                            const int32_t* sel_phys, float* o_ws, float* l_ws, const void* dummy) {
   AttendArgs a;
   a.g = g;
   a.step = step;
@@ -396,13 +241,18 @@ AttendArgs make_attend_args(const Geometry& g, int step, const void* q_window,
   a.sel_phys = sel_phys;
   a.o_ws = o_ws;
   a.l_ws = l_ws;
+  a.dummy = dummy;
+  a.tok_k = nullptr;
+  a.tok_v = nullptr;
   return a;
 }
 
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
                          const retro_kv_cache& c, const retro_selection& sel,
-                         const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s) {
-  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
+                         const int32_t* sel_phys, float* o_ws, float* l_ws, const void* dummy,
+                         hipStream_t s) {
+  if (!dummy) return hipErrorInvalidValue;
+  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws, dummy);
   if (g.dtype == RETRO_BF16) return g.D == 128 ? attend_d<bf16_t, 128>(a, s) : attend_d<bf16_t, 64>(a, s);
   return g.D == 128 ? attend_d<float, 128>(a, s) : attend_d<float, 64>(a, s);
 }
@@ -412,9 +262,9 @@ bool attend_selects(const Geometry& g) { return g.max_pages <= 12 * kAttendThrea
 hipError_t launch_attend_select(const Geometry& g, int step, const void* q_window,
                                 const retro_kv_cache& c, const retro_selection& sel,
                                 int32_t* sel_phys, const float* scores, float* o_ws, float* l_ws,
-                                int32_t* tok_out, hipStream_t s) {
-  if (!attend_selects(g) || !sel_phys || !tok_out) return hipErrorInvalidValue;
-  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
+                                int32_t* tok_out, const void* dummy, hipStream_t s) {
+  if (!attend_selects(g) || !sel_phys || !tok_out || !dummy) return hipErrorInvalidValue;
+  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws, dummy);
   const TopkArgs ta{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
                     sel.num_selected, sel_phys};
   if (g.dtype == RETRO_BF16)
@@ -422,50 +272,6 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
                       : attend_select_d<bf16_t, 64>(a, ta, tok_out, s);
   return g.D == 128 ? attend_select_d<float, 128>(a, ta, tok_out, s)
                     : attend_select_d<float, 64>(a, ta, tok_out, s);
-}
-
-bool attend_full_supported(const Geometry& g, int compute_units) {
-  const int per_head = g.n_splits * g.n_rgroups;
-  const int ppb = (g.max_pages + per_head - 1) / per_head;
-  // the score role loads the group's queries as at most two 16-byte pieces per
-  // thread and keeps them in LDS as fp32 (within the selection's share)
-  const bool q_fits = g.G * g.D <= 2 * kAttendThreads * (16 / g.elt) &&
-                      g.G * g.D <= kTopkHistWords + kTopkSmall;
-  return q_fits && g.rtw == 1 && g.max_pages <= 5 * kAttendThreads &&
-         ppb <= 3 * (kAttendThreads / 64) * 4 && (int64_t)per_head * g.hk * g.batch <= compute_units;
-}
-
-hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window, const void* k_new,
-                              const void* v_new, const retro_kv_cache& c,
-                              const retro_selection& sel, int32_t* sel_phys, float* scores,
-                              float* o_ws, float* l_ws, int32_t* tok_out, uint64_t* counters,
-                              int32_t* err, hipStream_t s) {
-  if (!sel_phys || !tok_out || !counters || !err) return hipErrorInvalidValue;
-  const AttendArgs a = make_attend_args(g, step, q_window, c, sel, sel_phys, o_ws, l_ws);
-  const TopkArgs ta{g, step, scores, c.page_table, c.last_loaded, sel.selected, sel.mask,
-                    sel.num_selected, sel_phys};
-  ScoreInArgs sc;
-  sc.q = (const char*)q_window + (int64_t)g.W * g.hq * g.D * g.elt;
-  sc.q_bstride = (int64_t)(g.W + 1) * g.hq * g.D;
-  sc.dg = c.digest;
-  sc.scores = scores;
-  sc.k_new = k_new;
-  sc.v_new = v_new;
-  sc.cnt = counters;
-  sc.err = err;
-  const int per_head = g.n_splits * g.n_rgroups;
-  sc.ppb = (g.max_pages + per_head - 1) / per_head;
-  // RETRO_TEST_WAIT_TIMEOUT=1 (tests of the failure path): every wait gives up
-  // after a few polls, its target being out of reach
-  const char* t = std::getenv("RETRO_TEST_WAIT_TIMEOUT");
-  const bool timeout = t && t[0] == '1';
-  sc.spin_limit = timeout ? 4 : kSpinLimit;
-  sc.target_bias = timeout ? (1ull << 40) : 0ull;
-  if (g.dtype == RETRO_BF16)
-    return g.D == 128 ? attend_full_d<bf16_t, 128>(a, ta, sc, tok_out, s)
-                      : attend_full_d<bf16_t, 64>(a, ta, sc, tok_out, s);
-  return g.D == 128 ? attend_full_d<float, 128>(a, ta, sc, tok_out, s)
-                    : attend_full_d<float, 64>(a, ta, sc, tok_out, s);
 }
 
 }  // namespace retro

@@ -51,43 +51,28 @@ struct Geometry {
   int tiles_per_group;
   int rtw;            // row tiles per wave
   int waves;          // waves per attention workgroup
-  // fused step plan (workgroups of kFusedWaves wavefronts, one attention row
-  // tile per wavefront): row groups and tiles per group of its attention
-  // tasks, tasks per KV head of each role, grid size, availability
-  int f_rgroups, f_tpg;
-  int fA, fC, fD;
-  int64_t f_grid;
-  bool fused;
-  // workspace layout (bytes)
-  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_ctl, ws_sel, ws_tok, ws_full, ws_total;
+  int flags;          // retro_dims.flags (RETRO_FLAG_*)
+  // workspace layout (bytes): page scores, physical ids of the selection,
+  // split partials, the sticky error word, the score launch's counters, the
+  // step token's page per head, the one-launch step's tagged score words and
+  // per-head counter lines, a dummy line (never written) for empty loads
+  size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_err, ws_sel, ws_tok, ws_tagged, ws_heads,
+      ws_dummy, ws_total;
   // set for the launches of a step whose token is written by its score launch:
   // seq_lens does not count the token yet (the merge launch advances it), and
   // every launch uses the length with the token
   int token_pending;
 };
 
-// Synchronisation words of the fused step in the workspace (int32 offsets):
-// 8 lane ticket counters kCtlStride apart, the exit counter, a sticky error
-// word (a bounded wait ran out), then per-head counters of the score, top-k and
-// attention roles, each in a 128-byte line of its own (kCtlStride apart) so
-// that the polls of different heads do not meet on one line.  All zero
-// between launches.
-constexpr int kCtlTicket = 0;
-constexpr int kCtlStride = 32;
-constexpr int kCtlExit = 256;
-constexpr int kCtlError = 257;
-constexpr int kCtlCounts = 512;
-constexpr int kFusedScoreIters = 4;
 // counters of the score + selection launch: per KV head 1 + kSelMaxGroups
 // counters, each kSelCounterInts apart (one 128-byte line)
 constexpr int kSelCounterInts = 32;
 constexpr int kSelMaxGroups = 8;
-constexpr int kFusedWaves = 8;
+// polls of a bounded wait (about 0.2 us each) before it gives up
+constexpr int kSpinLimit = 1 << 18;
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
 int attend_min_waves(int dtype, int D);
-int fused_score_pages_per_block(int dtype, int D);
-bool fused_supported(const Geometry& g);
 
 // ---- launchers (return hipSuccess or the launch error) ----
 hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
@@ -113,7 +98,8 @@ hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
                             int32_t* sel_phys, hipStream_t s);
 hipError_t launch_attend(const Geometry& g, int step, const void* q_window,
                          const retro_kv_cache& c, const retro_selection& sel,
-                         const int32_t* sel_phys, float* o_ws, float* l_ws, hipStream_t s);
+                         const int32_t* sel_phys, float* o_ws, float* l_ws, const void* dummy,
+                         hipStream_t s);
 // Attention with the page selection (top-k + Alg. 2's mask) computed by each
 // of its workgroups (attend_selects(g)); writes the selection outputs (rows,
 // mask, physical pages, count) but not last_loaded: the combine launch after
@@ -123,27 +109,25 @@ bool attend_selects(const Geometry& g);
 hipError_t launch_attend_select(const Geometry& g, int step, const void* q_window,
                                 const retro_kv_cache& c, const retro_selection& sel,
                                 int32_t* sel_phys, const float* scores, float* o_ws, float* l_ws,
-                                int32_t* tok_out, hipStream_t s);
-// Page scores (+ the token's append), selection and attention in one launch:
-// the workgroups of a KV head score its pages, wait for each other on a
-// per-head counter, then run launch_attend_select's work.  Only when every
-// workgroup is resident at once (attend_full_supported; rtw == 1, max_pages <=
-// 2560, at most 96 pages scored per workgroup).  counters: batch * h_k lines
-// of kSelCounterInts ints in the workspace, zero-filled once and then only
-// grown by this launch (by the head's workgroup count each time, so always with
-// the same geometry); err: set if a wait ran past its bound.  The combine
-// launch after it updates last_loaded as for launch_attend_select.
-bool attend_full_supported(const Geometry& g, int compute_units);
-hipError_t launch_attend_full(const Geometry& g, int step, const void* q_window, const void* k_new,
+                                int32_t* tok_out, const void* dummy, hipStream_t s);
+// Page scores (+ the token's append), selection and attention in one launch
+// (step_attend.hip): the workgroups of a KV head score its pages, publish them
+// as tagged words, each reads them all and selects, then attends its split.
+// Only when every workgroup is resident at once (step_attend_supported:
+// occupancy times compute units; rtw == 1, max_pages <= 2560, at most 96 pages
+// scored per workgroup).  Uses the workspace's tagged score words and per-head
+// counter lines (zero-filled once, then only grown; refused with the error
+// word set if last used with another geometry); err: set if a wait ran past
+// spin_limit polls (tag_bias != 0 makes every wait give up, for tests).  The
+// combine launch after it updates last_loaded as for launch_attend_select.
+bool step_attend_supported(const Geometry& g);
+int step_attend_workgroups(const Geometry& g);
+hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window, const void* k_new,
                               const void* v_new, const retro_kv_cache& c,
-                              const retro_selection& sel, int32_t* sel_phys, float* scores,
-                              float* o_ws, float* l_ws, int32_t* tok_out, uint64_t* counters,
-                              int32_t* err, hipStream_t s);
+                              const retro_selection& sel, void* workspace, float* o_ws,
+                              float* l_ws, int32_t* tok_out, int32_t* err, int spin_limit,
+                              uint32_t tag_bias, hipStream_t s);
 int compute_units();
-hipError_t launch_step_fused(const Geometry& g, int step, const void* q_window, const void* k_new,
-                             const void* v_new, const retro_kv_cache& c,
-                             const retro_selection& sel, const retro_output_cache* oc,
-                             float* o_out, float* lse_out, void* workspace, hipStream_t s);
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
 // With g.token_pending and a cache, the launch also advances seq_lens past the
 // step's token (when its page is mapped).  With `selected` and `tok_upd` (from

@@ -35,7 +35,7 @@ __device__ __forceinline__ void update_last_loaded(const MergeArgs& a, int bh) {
   if (lane == 0 && tok >= 0 && tok < g.max_pages) arow[tok] = a.step - 1;
 }
 
-// The rows merge unit `unit` writes (mode 2), as NaN.
+// The output rows merge unit `unit` writes, as NaN (nothing else is written).
 template <int D>
 __device__ void poison_unit(const MergeArgs& a, int unit) {
   const Geometry& g = a.g;
@@ -62,18 +62,25 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   const Geometry& g = a.g;
   const int nunits = g.batch * g.hq * a.xs;
   const int mblocks = (nunits + kWaves - 1) / kWaves;
+  // A bounded wait of the launch that produced the partials ran out (or it
+  // refused a workspace of another geometry): the partials and the selection
+  // are not to be trusted, so the outputs are NaN and the caller's state (the
+  // output cache, last_loaded, seq_lens) is left as it was.
+  const bool failed = a.err && *a.err != 0;
   if ((int)blockIdx.x >= mblocks) {
     // workgroups past the merge units: Alg. 2's last_loaded update, one KV
     // head per wavefront
     const int bh = ((int)blockIdx.x - mblocks) * kWaves + (threadIdx.x >> 6);
-    if (bh < g.batch * g.hk) update_last_loaded(a, bh);
+    if (bh < g.batch * g.hk && !failed) update_last_loaded(a, bh);
     return;
   }
   const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
-  const bool failed = a.err && *a.err != 0;
+  if (failed) {
+    poison_unit<D>(a, u);
+    return;
+  }
   merge_unit<D, 32>(a, u);
-  if (failed && a.mode == 2) poison_unit<D>(a, u);
   if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
     // after the unit's own loads (the two lookups here are dependent): the
     // first wavefront advances every sequence; no other workgroup of this

@@ -282,44 +282,56 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b
 // left operand is always the lower index).  tok.lp < 0: no token to append.
 // The workgroup scores pages [page0, page_end) (at most ITERS passes of four
 // pages per wavefront; pass it covers the workgroup's pages it*nw*4 onwards).
-// COH: the token's key and value are read by other workgroups of the same
-// launch, so they are stored device-coherently.  GC > 0: the group size is
-// GC (== g.G), so the loop over the group's heads unrolls and the heads'
-// reduction chains interleave (0.2 us per step at G = 4); 0: any g.G.
+// DEFER: the role stores nothing to global memory itself: the widened digest
+// row of the token's page goes to dig_lds (2 * D elements of LDS: minimum,
+// then maximum) and the token's key and value are left to the caller (the
+// caller then issues every store of the phase from one wavefront, so that the
+// others carry no pending store into the loads that follow).  Otherwise the
+// row, the key and the value are stored here.  GC > 0: the group size is GC (== g.G), so
+// the loop over the group's heads unrolls and the heads' reduction chains
+// interleave (0.2 us per step at G = 4); 0: any g.G.
 // The token and the number of pages of the sequence come from `tok_of(n_pages)`
 // (returns the StepToken, sets n_pages), called once the digest and query loads
 // are issued: its own loads (sequence length, page table) then overlap them.
-template <typename T, int D, int ITERS, bool COH, int GC = 0, typename TokOf>
+// `pre_barrier()` runs in every thread just before the barrier that publishes
+// the staged queries to the workgroup; `publish(page, score)` hands each score
+// of a page below n_pages on (called by one lane per page).  NT > 0: the
+// workgroup has NT threads (else blockDim.x).  The digest loads depend on
+// page0, page_end and drow only, and are not branched around (pages past the
+// share read its last row, and their scores are not published), so they can
+// go out before any other kernel argument has arrived.
+template <typename T, int D, int ITERS, bool DEFER, int GC = 0, int NT = 0, typename TokOf,
+          typename PreBarrier, typename Publish>
 __device__ __forceinline__ void score_role(const Geometry& g, int page0, int page_end, const T* q,
-                                           T* drow, float* srow, float* sq, TokOf&& tok_of) {
+                                           T* drow, float* sq, TokOf&& tok_of,
+                                           PreBarrier&& pre_barrier, Publish&& publish,
+                                           T* dig_lds = nullptr) {
 #pragma clang fp contract(off)
   using S = ScoreShape<T, D>;
   const int tid = thread_index();
-  const int lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int nthreads = NT > 0 ? NT : (int)blockDim.x;
+  const int lane = tid & 63, wave = tid >> 6, nw = nthreads >> 6;
   const int c = lane % S::LPP;
   // every load before any wait: digest rows (in bounds of the [max_pages] row
   // whatever the sequence length), the queries, the token's key
   uint32_t raw[ITERS][2][S::WORDS];
+  const int last_row = max(page_end - 1, 0);
 #pragma unroll
   for (int it = 0; it < ITERS; ++it) {
-    const int page = page0 + (it * nw + wave) * S::PPW + lane / S::LPP;
-    if (page < page_end) {
-      const T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
-      load_words<S::WORDS>(row, raw[it][0]);
-      load_words<S::WORDS>(row + D, raw[it][1]);
-    } else {
-#pragma unroll
-      for (int w = 0; w < S::WORDS; ++w) raw[it][0][w] = raw[it][1][w] = 0u;
-    }
+    const int page = min(page0 + (it * nw + wave) * S::PPW + lane / S::LPP, last_row);
+    const T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
+    load_words<S::WORDS>(row, raw[it][0]);
+    load_words<S::WORDS>(row + D, raw[it][1]);
   }
   // the group's queries: 16-byte pieces, at most two per thread (G * d <= 2048
   // elements for 256 threads), all requested before any is converted
   constexpr int QV = 16 / sizeof(T);
+  const int gd = (GC > 0 ? GC : g.G) * D;
   uint4 qraw[2];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    const int e = (tid + r * blockDim.x) * QV;
-    if (e < g.G * D) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
+    const int e = (tid + r * nthreads) * QV;
+    if (e < gd) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
   int n_pages = 0;
   const StepToken<T> tok = tok_of(n_pages);
@@ -329,7 +341,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
   // workgroup running this role has at least 256 threads)
   static_assert(D <= 256, "one element per thread");
   T tok_k = T{}, tok_v = T{};
-  if (has_tok) {  // uniform
+  if (!DEFER && has_tok) {  // uniform
     tok_k = tok.k[min(tid, D - 1)];
     tok_v = tok.v[min(tid, D - 1)];
   }
@@ -341,8 +353,8 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
   }
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
-    const int e = (tid + r * blockDim.x) * QV;
-    if (e < g.G * D) {
+    const int e = (tid + r * nthreads) * QV;
+    if (e < gd) {
       const uint32_t w[4] = {qraw[r].x, qraw[r].y, qraw[r].z, qraw[r].w};
       float f[QV];
       words_to_f32<T, 4>(w, f);
@@ -351,10 +363,13 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
         *reinterpret_cast<float4*>(sq + e + i) = make_float4(f[i], f[i + 1], f[i + 2], f[i + 3]);
     }
   }
+  pre_barrier();
   __syncthreads();
 
+  float score[ITERS];
 #pragma unroll
   for (int it = 0; it < ITERS; ++it) {
+    score[it] = 0.f;
     const int wpage0 = page0 + (it * nw + wave) * S::PPW;
     if (it > 0 && wpage0 >= page_end) break;  // uniform: no page of this pass
     const int page = wpage0 + lane / S::LPP;
@@ -372,7 +387,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
           if (hi[v] < kv[v]) hi[v] = kv[v];
         }
       }
-      T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
+      T* row = (DEFER ? dig_lds : drow + (int64_t)page * 2 * D) + c * S::VEC;
       uint32_t w[S::WORDS];
       f32_to_words<T, S::WORDS>(lo, w);
       store_words<S::WORDS>(row, w);
@@ -411,20 +426,16 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
     } else {
       for (int gq = 0; gq < g.G; ++gq) head(gq);
     }
-    // device-coherent store: a later reader of the same launch (the selection)
-    // may run on another XCD
-    if (page < n_pages && page < page_end && c == 0)
-      __hip_atomic_store(srow + page, Ssum + 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    score[it] = Ssum + 0.0f;
   }
-  if (has_tok && tid < D) {
-    if constexpr (COH) {
-      using U = typename std::conditional<sizeof(T) == 2, uint16_t, uint32_t>::type;
-      put_c<true>(reinterpret_cast<U*>(tok.k_row + tid), __builtin_bit_cast(U, tok_k));
-      put_c<true>(reinterpret_cast<U*>(tok.v_col + (int64_t)tid * g.P), __builtin_bit_cast(U, tok_v));
-    } else {
-      tok.k_row[tid] = tok_k;
-      tok.v_col[(int64_t)tid * g.P] = tok_v;
-    }
+  if (!DEFER && has_tok && tid < D) {
+    tok.k_row[tid] = tok_k;
+    tok.v_col[(int64_t)tid * g.P] = tok_v;
+  }
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int page = page0 + (it * nw + wave) * S::PPW + lane / S::LPP;
+    if (page < n_pages && page < page_end && c == 0) publish(page, score[it]);
   }
 }
 
@@ -778,7 +789,19 @@ struct AttendArgs {
   const int32_t* sel_phys;  // physical ids of the selected pages, or null (page-table lookup)
   float* o_ws;
   float* l_ws;
+  // 16 bytes that no kernel writes (a line of the workspace): loads of chunk
+  // pieces with no stored data read here instead of branching around the load,
+  // so they never bring a line of the KV cache into a cache early
+  const void* dummy;
+  // the step's token, [batch][h_k][d], when another workgroup of the same
+  // launch stores it into the cache (see attend_role's tok_pos); else null
+  const void* tok_k;
+  const void* tok_v;
 };
+
+AttendArgs make_attend_args(const Geometry& g, int step, const void* q_window,
+                            const retro_kv_cache& c, const retro_selection& sel,
+                            const int32_t* sel_phys, float* o_ws, float* l_ws, const void* dummy);
 
 
 // The attention pass of one (sequence, KV head, row group, split).  Row-tile
@@ -797,12 +820,37 @@ struct AttendArgs {
 // the selection row from `first` on: logical page, mask value, physical page;
 // left as passed in for tid >= pages_per_split) and returns the number of
 // selected pages of the row.
+// tok_pos >= 0: the position of the step's token, which another workgroup of
+// the same launch is storing into the cache: its key row and value column are
+// taken from a.tok_k / a.tok_v into LDS instead (so no gather has to wait for
+// that store); the cache supplies the page's other tokens, stored by earlier
+// launches.  s_tok: one int of LDS.
+// With a PresetList the caller has filled the split's page list itself before
+// `wait()` returns (after a barrier): s_phys / s_len / s_mask for every slot
+// of the split (-1 / 0 / 0 past the kept pages), *s_tok (the slot of the
+// token's page, -1 if not in the split), and gives the number of kept pages
+// and, for the first d threads, the token's key and value elements.
+// With COH, a PresetList's s_lse (16 floats of LDS per row tile of the group)
+// receives each row's log-normaliser, at the row's place in the group, instead
+// of the workspace (the caller publishes them once the partial outputs are
+// known to be complete).
+template <typename T>
+struct PresetList {
+  const int* k;  // read once wait() has returned
+  T tok_k, tok_v;
+  float* s_lse;
+};
+template <typename L>
+struct is_preset : std::false_type {};
+template <typename T>
+struct is_preset<PresetList<T>> : std::true_type {};
 struct SelectionRows {};
 template <typename T, int D, int RTW, int MAXP, bool PAIR, bool COH, typename SeqLen, typename Wait,
           typename List = SelectionRows>
 __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, int rg, int split,
                                             SeqLen&& seq_len_of, T* lds, int* s_phys, int* s_len,
-                                            int* s_mask, Wait&& wait, List&& list) {
+                                            int* s_mask, int* s_tok, int tok_pos, Wait&& wait,
+                                            List&& list) {
   using TL = Tiles<T, D>;
   const Geometry& g = a.g;
   const int bh = b * g.hk + h;
@@ -865,6 +913,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   const int first = split * g.pages_per_split;
   int lp = -1, m = 0, phys = -1;
   int k_eff;
+  constexpr bool kPreset = is_preset<typename std::decay<List>::type>::value;
   if constexpr (std::is_same<typename std::decay<List>::type, SelectionRows>::value) {
     if (tid < g.pages_per_split && first + tid < g.k_max) {
       const int64_t o = (int64_t)bh * g.k_max + first + tid;
@@ -873,6 +922,8 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
       if (a.sel_phys) phys = get_c<COH>(a.sel_phys + o);
     }
     k_eff = get_c<COH>(a.nsel + bh);
+  } else if constexpr (kPreset) {
+    k_eff = *list.k;
   } else {
     k_eff = list(tid, first, lp, m, phys);
   }
@@ -885,16 +936,42 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     const int nchunks = (np + g.chunk_pages - 1) / g.chunk_pages;
     // page list of the split: physical page (-1: skip), stored tokens (0 for a
     // skipped page and past the list), mask value
-    if (tid < kMaxSplitPages) {
-      if (!a.sel_phys && tid < np && lp >= 0 && lp < g.max_pages)
-        phys = a.pt[(int64_t)b * g.max_pages + lp];
-      if (tid >= np || lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
-      s_phys[tid] = phys;
-      s_len[tid] = phys >= 0 ? max(0, min(g.P, seq_len - lp * g.P)) : 0;
-      s_mask[tid] = tid < np ? m : 0;
+    if constexpr (!kPreset) {
+      if (tid < kMaxSplitPages) {
+        if (!a.sel_phys && tid < np && lp >= 0 && lp < g.max_pages)
+          phys = a.pt[(int64_t)b * g.max_pages + lp];
+        if (tid >= np || lp < 0 || lp >= g.max_pages || phys < 0 || phys >= g.num_phys) phys = -1;
+        s_phys[tid] = phys;
+        s_len[tid] = phys >= 0 ? max(0, min(g.P, seq_len - lp * g.P)) : 0;
+        s_mask[tid] = tid < np ? m : 0;
+        // the list slot of the step's token page, if it is in this split
+        const uint64_t tm = wave_ballot(tok_pos >= 0 && phys >= 0 && lp == tok_pos / g.P);
+        if (tid == 0) *s_tok = tm ? __builtin_ctzll(tm) : -1;
+      }
+      __syncthreads();  // page list ready
     }
-
-    __syncthreads();  // page list ready
+    const int ts = *s_tok;
+    T tok_kv[2];
+    if constexpr (kPreset) {
+      tok_kv[0] = list.tok_k;
+      tok_kv[1] = list.tok_v;
+    } else if (ts >= 0 && tid < D) {  // uniform condition, then the first D threads
+      const int64_t o = ((int64_t)b * g.hk + h) * D + tid;
+      tok_kv[0] = reinterpret_cast<const T*>(a.tok_k)[o];
+      tok_kv[1] = reinterpret_cast<const T*>(a.tok_v)[o];
+    }
+    // Overwrite the token's key row and value column in LDS buffer `buf`, which
+    // holds chunk c (after the barrier that follows its staging), then barrier.
+    auto patch_token = [&](int c, int buf) {
+      if (ts < 0 || ts / g.chunk_pages != c) return;  // uniform
+      T* base = lds + buf * TL::BUF_ELEMS;
+      const int row = (g.chunk_pages == 2 ? (ts & 1) * 16 : 0) + tok_pos % g.P;
+      if (tid < D) {
+        base[row * TL::KROW + tid] = tok_kv[0];
+        base[TL::K_ELEMS + ((row >> 4) * D + tid) * TL::VROW + (row & 15)] = tok_kv[1];
+      }
+      __syncthreads();
+    };
 
     // ---- chunk staging: global -> registers -> LDS ----------------------------
     const int pieces_per_thread = (TL::PIECES + nthreads - 1) / nthreads;
@@ -937,8 +1014,8 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
     }
 
     // Every piece is loaded without a branch around the load (a piece that holds
-    // no stored data reads a stand-in address, the cache's first 16 bytes), so
-    // the loads of a chunk are all in flight together; `keep` records how many
+    // no stored data reads the dummy line instead), so the loads of a chunk are
+    // all in flight together; `keep` records how many
     // leading elements of each piece hold stored data (4 bits per piece), and
     // the rest is zeroed when the piece is written to LDS.
     const int64_t blk_elems = (int64_t)g.P * D;
@@ -951,7 +1028,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         const int len = s_len[pl];
         int n_el = pc_v[i] ? min(max(len - pc_slot[i], 0), TL::TPP) : (pc_slot[i] < len ? TL::VEC : 0);
         if (i >= pieces_per_thread || tid + i * nthreads >= TL::PIECES) n_el = 0;
-        const T* src = kc;
+        const T* src = reinterpret_cast<const T*>(a.dummy);
         if (n_el > 0)
           src = (pc_v[i] ? vc : kc) + ((int64_t)phys * g.hk + h) * blk_elems + pc_off[i];
         stage[i] = *reinterpret_cast<const uint4*>(src);
@@ -1150,6 +1227,8 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
         if (c + 3 < nchunks) load_chunk(c + 3, stage[1], keep[1]);
         __syncthreads();
+        patch_token(c, 0);
+        if (nv > 1) patch_token(c + 1, 1);
         compute_group(std::integral_constant<int, 2>{}, c, 0, nv);
         if (c + 2 < nchunks) __syncthreads();  // the buffers are rewritten next trip
       }
@@ -1161,11 +1240,13 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         store_chunk(0, stage[0], keep[0]);
         if (c + 2 < nchunks) load_chunk(c + 2, stage[0], keep[0]);
         __syncthreads();
+        patch_token(c, 0);
         compute_chunk(c, 0);
         if (c + 1 < nchunks) {
           store_chunk(1, stage[DEPTH - 1], keep[DEPTH - 1]);
           if (c + 3 < nchunks) load_chunk(c + 3, stage[DEPTH - 1], keep[DEPTH - 1]);
           __syncthreads();
+          patch_token(c + 1, 1);
           compute_chunk(c + 1, 1);
         }
       }
@@ -1176,6 +1257,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         store_chunk(c & 1, stage[0], keep[0]);
         if (c + 1 < nchunks) load_chunk(c + 1, stage[0], keep[0]);
         __syncthreads();
+        patch_token(c, c & 1);
         compute_chunk(c, c & 1);
       }
     }
@@ -1207,7 +1289,8 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
         }
       }
       if (g4 == 0) {
-        if constexpr (COH) put_c<true>(a.l_ws + part + rho, lse);
+        if constexpr (COH && is_preset<typename std::decay<List>::type>::value) list.s_lse[lt * 16 + ln16] = lse;
+        else if constexpr (COH) put_c<true>(a.l_ws + part + rho, lse);
         else __builtin_nontemporal_store(lse, a.l_ws + part + rho);
       }
     }
@@ -1447,40 +1530,6 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   // it is overwritten
   asm volatile("" : : "v"(merged.z) : "memory");
   put<D>(a.o_cache, a.l_cache, slot, p[1]);
-}
-
-// ============================================================================
-// Cross-workgroup hand-off for the fused step, without fences.  Everything a
-// consumer reads from its producers is written and read device-coherently (sc1
-// accesses, which go through / past the per-XCD L2s; the roles' COH forms).
-// Producer: every wavefront waits until its own stores have completed (a bare
-// barrier does not wait for them), the workgroup meets at a barrier, and one
-// thread adds 1 to the counter (relaxed, device scope).  Consumer: thread 0
-// polls the counter with relaxed device-coherent loads, then releases the
-// workgroup through a barrier.  (Release / acquire fences here write back or
-// invalidate a whole L2 each time.)  Polling is bounded: past the limit the
-// error word is set and the consumer goes on, so no wait can hang.
-// ============================================================================
-constexpr int kSpinLimit = 1 << 18;  // polls of about 0.5 us each
-
-__device__ __forceinline__ void block_wait(const int32_t* ctr, int target, int32_t* err) {
-  if (threadIdx.x == 0) {
-    int it = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      if (++it > kSpinLimit) {
-        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(8);  // ~0.2 us between polls: less traffic on the counter's line
-    }
-  }
-  __syncthreads();
-}
-
-__device__ __forceinline__ void block_signal(int32_t* ctr) {
-  __builtin_amdgcn_s_waitcnt(0);  // this wavefront's stores have completed
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace retro

@@ -104,9 +104,15 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
       warm_p = sa.tk.pt[(int64_t)b * g.max_pages + p];
     }
   }
-  score_role<T, D, score_iters(PER), false>(g, page0, page_end, q + b * q_bstride + (int64_t)h * g.G * D,
-                                dg + bh * g.max_pages * 2 * D, scores + bh * g.max_pages,
-                                dyn_lds, tok_of);
+  float* srow = scores + bh * g.max_pages;
+  score_role<T, D, score_iters(PER), false>(
+      g, page0, page_end, q + b * q_bstride + (int64_t)h * g.G * D, dg + bh * g.max_pages * 2 * D,
+      dyn_lds, tok_of, [] {},
+      // device-coherent store: a later reader of the same launch (the selection)
+      // may run on another XCD
+      [&](int page, float v) {
+        __hip_atomic_store(srow + page, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      });
   if constexpr (PER > 0) {
     asm volatile("" : : "v"(warm_a), "v"(warm_p));  // keeps the two loads
     __shared__ int s_last;

@@ -1,0 +1,477 @@
+// Page scores, page selection and the attention of one decode step in a single
+// launch, for shapes whose workgroups all fit on the GPU at once (the Llama-class
+// single-sequence layers): Alg. 1's PageSelect and attention, Alg. 2's mask
+// values, eq. (quest_score), eq. (update-org) and eq. (update-sup).
+//
+// Each KV head (sequence b, head h) gets NW workgroups; workgroup j of the head
+//   1. scores the head's pages [j * ppb, (j + 1) * ppb), appending the step's
+//      token where its page is among them (score_role);
+//   2. publishes every score as one 64-bit word: the score's bits and the
+//      launch's epoch (tag), and the smallest and largest key of its share in
+//      two more, written device-coherently by one wavefront;
+//   3. loads the head's score words, each thread of the other wavefronts its
+//      stripe of pages, until every word of a page of the sequence carries
+//      this launch's epoch (the data are their own signal: no counter, no
+//      barrier across workgroups);
+//   4. computes the head's selection by threshold (threshold.h) and writes the
+//      page list of its split of the kept pages into LDS; the head's writer
+//      workgroup also writes the selection rows, mask values and count;
+//   5. runs the attention of its split (attend_role) and writes the split's
+//      partial (O, LSE) per window row, combined by the merge launch.
+//
+// Epoch.  Every workgroup has a line of its own in the workspace holding the
+// number of launches it has run (and a fingerprint of the geometry); it reads
+// the line at its start and its publisher wavefront stores the count + 1.  All
+// workgroups of a launch run once per launch, so the counts agree, and the
+// epoch (count + 1) is the same in every workgroup of the launch and larger
+// than every tag an earlier launch wrote.  A workspace last used with another
+// geometry is refused by the fingerprint: the sticky error word is set and no
+// wait is entered.
+//
+// Coherence (without fences, which would write back or invalidate whole L2s):
+//   - a score word is written with one device-coherent (sc1) 64-bit store and
+//     read with device-coherent loads, which are not served from a
+//     non-coherent L2 copy: a reader sees either an older word (an older tag)
+//     or this launch's word, never a torn one;
+//   - the step's token key and value are stored into the cache by the
+//     workgroup whose share holds the token's page, with plain stores and no
+//     wait: they are for later launches.  In this launch the gather of the
+//     token's page takes the token's key row and value column from the step's
+//     input (k_new, v_new) into LDS, over whatever the cache slot holds; the
+//     page's other tokens were stored by earlier launches;
+//   - the gather uses plain loads of lines that no workgroup of this launch
+//     writes, apart from the token's bytes (replaced as above); no L2 holds a
+//     line from before the launch (the launch's acquire at its start), so no
+//     stale copy can be hit.
+//
+// Waits are bounded: past spin_limit polls the sticky error word is set and the
+// workgroup goes on with what it has; the merge launch then writes NaN outputs
+// and leaves the output cache, last_loaded and seq_lens as they were.
+#include "threshold.h"
+
+namespace retro {
+namespace {
+
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / 64;
+
+struct StepAttendArgs {
+  AttendArgs a;
+  float* scores;       // [batch * h_k][max_pages] fp32: every score, for retro_copy_scores
+  int32_t* A;          // last_loaded: read for the mask values, updated after the step
+  int32_t* tok_out;    // [batch * h_k]: the step token's page if it is not kept, else -1
+  int32_t* err;        // sticky error word
+  const void* k_new;   // the step's token, [batch][h_k][d] (null: no token)
+  const void* v_new;
+  int spin_limit;      // polls before a wait gives up
+  uint32_t tag_bias;   // added to the awaited tag (tests: makes every wait give up)
+  // the combine + merge in the same launch (null o_out: partials only)
+  uint64_t* lse_tag;   // [batch * h_k][splits][R]: tagged log-normaliser of each partial row
+  uint32_t* done;      // per sequence, a 128-byte line: heads past their selection (never reset)
+  float* o_cache;      // output cache ring [batch][W][h_q][d] + [batch][W][h_q]
+  float* l_cache;
+  float* o_out;        // [batch][W + 1][h_q][d] + [batch][W + 1][h_q]
+  float* l_out;
+  int32_t* seq_lens;   // advanced past the token once every head of the sequence has read it
+};
+
+template <typename T, int D, int PER, int SITERS>
+struct StepLds {
+  union {
+    T stage[2 * Tiles<T, D>::BUF_ELEMS];
+    ThrLds<PER, kWaves> thr;
+  } u;
+  float sq[16 * D];               // the group's current queries (fp32) while scoring
+  float share[SITERS * kWaves * 4];  // this workgroup's scores
+  T dig[2 * D];                   // the token page's widened digest row
+  int s_phys[kMaxSplitPages], s_len[kMaxSplitPages], s_mask[kMaxSplitPages];
+  float lse[kWaves * 16];         // the split's partial log-normaliser of the group's rows
+  int s_tok;
+  uint32_t epoch, fp_seen;
+  int bad;                        // this workgroup failed (see StepAttendArgs::err)
+  int k;
+};
+
+// Wavefront 7 issues every store of the score phase (the score words, the
+// share's key range, the plain scores, the token's key and value, the digest
+// row of its page) and counts the workgroup in; wavefronts 0-6 hold the
+// selection's stripes and poll.  On this GPU a wavefront's loads and stores
+// retire in order: a poll issued behind device-coherent stores would wait for
+// their write-through.
+constexpr int kPollThreads = kThreads - 64;
+
+// Leading arguments (the pointers and sizes the first loads need: digests,
+// then queries) come before the argument block so that they can be preloaded
+// into scalar registers: the digest loads then go out without waiting for the
+// kernel-argument segment.
+template <typename T, int D, int PER, int SITERS, int GC>
+__global__ void __launch_bounds__(kThreads) step_attend_kernel(
+    T* __restrict__ dg, uint32_t mp, uint32_t ppb, uint32_t nw, uint32_t ngrid,
+    const T* __restrict__ q_cur, uint32_t hk, uint32_t q_bstride, uint32_t* __restrict__ ctl,
+    uint64_t* __restrict__ tagged, uint32_t fingerprint, StepAttendArgs sa) {
+  __shared__ __attribute__((aligned(16))) StepLds<T, D, PER, SITERS> L;
+  const Geometry& g = sa.a.g;
+  const int tid = thread_index();
+  const int wave = tid >> 6, lane = tid & 63;
+  const uint32_t u = (uint32_t)xcd_remap(blockIdx.x, ngrid);
+  const uint32_t bh = u / nw;
+  const uint32_t j = u - bh * nw;
+  const int page0 = (int)(j * ppb);
+  const int page_end = min(page0 + (int)ppb, (int)mp);
+  const int b = (int)(bh / hk), h = (int)bh - b * (int)hk;
+  const int gsize = GC > 0 ? GC : g.G;
+  const bool publisher = wave == kWaves - 1;
+
+  // this workgroup's own line: [0, 1] its launches (64 bits), [2] the geometry
+  // fingerprint; read first (no other workgroup touches the line)
+  uint32_t* line = ctl + ((size_t)bh * nw + j) * 32;
+  uint64_t launches = 0;
+  uint32_t fp_seen = 0;
+  if (tid == 0) {
+    launches = __hip_atomic_load(reinterpret_cast<uint64_t*>(line), __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+    fp_seen = __hip_atomic_load(line + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  int seq_len = 0, tok_lp = -1;
+  StepToken<T> tok{-1, 0, nullptr, nullptr, nullptr, nullptr};
+  T tok_kv[2][(D + 63) / 64];  // the publisher's lanes: the token's key and value elements
+  T tok_mine[2];               // threads below d: the token's key and value element
+  int32_t a_old[PER], phys[PER];
+  uint64_t* trow = tagged + (size_t)bh * (mp + 2 * nw);
+  uint64_t* hrow = trow + mp;  // per workgroup: the key range of its share
+  float* srow = sa.scores + (size_t)bh * mp;
+
+  // ---- 1: this workgroup's share of the head's scores, into LDS
+  score_role<T, D, SITERS, true, GC, kThreads>(
+      g, page0, page_end,
+      q_cur + (size_t)b * q_bstride + (size_t)h * gsize * D, dg + (size_t)bh * mp * 2 * D, L.sq,
+      [&](int& np) {
+        // the selection's stripe of last_loaded and page-table entries, with
+        // the digests (no load here depends on another)
+        const int32_t* arow = sa.A + (size_t)bh * mp;
+        const int32_t* prow = sa.a.pt + (size_t)b * mp;
+#pragma unroll
+        for (int jj = 0; jj < PER; ++jj) {
+          const int idx = min(jj * kPollThreads + tid, (int)mp - 1);
+          a_old[jj] = arow[idx];
+          phys[jj] = prow[idx];
+        }
+        const int pos = sa.a.seq_lens[b];
+        seq_len = pos;
+        if (g.token_pending) {
+          const int ph = token_phys(g, sa.a.pt, b, pos);
+          if (ph >= 0) {
+            seq_len = pos + 1;
+            tok = make_step_token<T>(g, b, h, pos, ph, sa.k_new, sa.v_new,
+                                     const_cast<void*>(sa.a.kc), const_cast<void*>(sa.a.vc));
+          }
+        }
+        np = min((seq_len + g.P - 1) / g.P, (int)mp);
+        tok_lp = tok.lp;
+        if (tok.lp >= 0) {
+          tok_mine[0] = tok.k[min(tid, D - 1)];
+          tok_mine[1] = tok.v[min(tid, D - 1)];
+        }
+        if (publisher && tok.lp >= page0 && tok.lp < page_end) {
+#pragma unroll
+          for (int r = 0; r < (D + 63) / 64; ++r) {
+            const int d = min(lane + 64 * r, D - 1);
+            tok_kv[0][r] = tok.k[d];
+            tok_kv[1][r] = tok.v[d];
+          }
+        }
+        return tok;
+      },
+      [&] {
+        thr_clear(L.u.thr);
+        if (tid == 0) {
+          const bool bad = fp_seen != 0 && fp_seen != fingerprint;
+          if (bad) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          L.epoch = (uint32_t)launches + 1u;
+          L.fp_seen = fp_seen;
+          L.bad = bad;
+        }
+      },
+      [&](int page, float v) { L.share[page - page0] = v; }, L.dig);
+
+  const int n = min((seq_len + g.P - 1) / g.P, (int)mp);
+  __syncthreads();  // the share's scores and the token page's digest row are in LDS
+
+  // ---- 2: the publisher stores: score words and the share's key range
+  // (tagged with the epoch), plain scores for later launches, the token and its
+  // page's digest row (for later launches: this launch's gather takes the
+  // token from the step's input)
+  if (publisher) {
+    const uint64_t tag = (uint64_t)L.epoch << 32;
+    uint32_t kmn = 0xFFFFFFFFu, kmx = 0u;
+    for (int p = page0 + lane; p < min(page_end, n); p += 64) {
+      const float v = L.share[p - page0];
+      __hip_atomic_store(trow + p, tag | __float_as_uint(v), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      srow[p] = v;
+      kmn = min(kmn, order_key(v));
+      kmx = max(kmx, order_key(v));
+    }
+    kmn = wave_umin(kmn);
+    kmx = wave_umax(kmx);
+    if (lane < 2)
+      __hip_atomic_store(hrow + 2 * j + lane, tag | (lane == 0 ? kmn : kmx), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    if (tok.lp >= page0 && tok.lp < page_end) {  // uniform
+      constexpr int WORDS = 2 * D * (int)sizeof(T) / 4;
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(L.dig);
+      uint32_t* dst = reinterpret_cast<uint32_t*>(dg + ((size_t)bh * mp + tok.lp) * 2 * D);
+      for (int i = lane; i < WORDS; i += 64) dst[i] = src[i];
+#pragma unroll
+      for (int r = 0; r < (D + 63) / 64; ++r) {
+        const int d = lane + 64 * r;
+        if (d < D) {
+          tok.k_row[d] = tok_kv[0][r];
+          tok.v_col[(int64_t)d * g.P] = tok_kv[1][r];
+        }
+      }
+    }
+    if (lane == 0) {
+      // the launch count of this launch: the epoch (thread 0 read the line)
+      __hip_atomic_store(reinterpret_cast<uint64_t*>(line), (uint64_t)L.epoch, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      if (L.fp_seen == 0)
+        __hip_atomic_store(line + 2, fingerprint, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  const int n_splits = g.n_splits;
+  const int split = (int)j % n_splits, rg = (int)j / n_splits;
+  const int first = split * g.pages_per_split;
+  const bool writer = j == 0;
+
+  // ---- 3-4: the head's scores, then its selection, which fills the split's
+  // page list (run by attend_role once its query loads are in flight)
+  int k = 0;
+  auto select = [&] {
+    const uint32_t want = L.epoch + sa.tag_bias;
+    const bool bad = L.bad != 0;
+    // every page of the sequence in a polling thread's stripe that another
+    // workgroup scored (this workgroup's own scores are in LDS), and the key
+    // ranges of every share (lane l: word l of the head's range words)
+    auto polled = [&](int jj) {
+      const int p = jj * kPollThreads + tid;
+      return tid < kPollThreads && p < n && (p < page0 || p >= page_end);
+    };
+    constexpr int HW = 2;  // range words per lane (shares of up to 64 workgroups)
+    auto hword = [&](int r) { return (int)(lane + 64 * r) < 2 * (int)nw && !publisher; };
+    uint64_t e[PER], hv[HW];
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj)
+      e[jj] = polled(jj) ? __hip_atomic_load(trow + jj * kPollThreads + tid, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT)
+                         : 0ull;
+#pragma unroll
+    for (int r = 0; r < HW; ++r)
+      hv[r] = hword(r) ? __hip_atomic_load(hrow + lane + 64 * r, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT)
+                       : 0ull;
+    // meanwhile: the split's page list starts out empty
+    if (tid < kMaxSplitPages) {
+      L.s_phys[tid] = -1;
+      L.s_len[tid] = 0;
+      L.s_mask[tid] = 0;
+    }
+    if (tid == 0) L.s_tok = -1;
+    for (int it = 0;; ++it) {
+      bool stale = false;
+#pragma unroll
+      for (int jj = 0; jj < PER; ++jj)
+        stale = stale || (polled(jj) && (uint32_t)(e[jj] >> 32) != want);
+#pragma unroll
+      for (int r = 0; r < HW; ++r) stale = stale || (hword(r) && (uint32_t)(hv[r] >> 32) != want);
+      if (wave_ballot(stale) == 0 || bad) break;  // wavefront-uniform
+      if (it >= sa.spin_limit) {
+        if (lane == 0) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+      for (int jj = 0; jj < PER; ++jj)
+        if (polled(jj) && (uint32_t)(e[jj] >> 32) != want)
+          e[jj] = __hip_atomic_load(trow + jj * kPollThreads + tid, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+      for (int r = 0; r < HW; ++r)
+        if (hword(r) && (uint32_t)(hv[r] >> 32) != want)
+          hv[r] = __hip_atomic_load(hrow + lane + 64 * r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // the head's key range: minimum over the even words, maximum over the odd
+    uint32_t kmn = 0xFFFFFFFFu, kmx = 0u;
+#pragma unroll
+    for (int r = 0; r < HW; ++r)
+      if (hword(r)) {
+        if ((lane & 1) == 0) kmn = min(kmn, (uint32_t)hv[r]);
+        else kmx = max(kmx, (uint32_t)hv[r]);
+      }
+    kmn = wave_umin(kmn);
+    kmx = wave_umax(kmx);
+    uint32_t key[PER];
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj) {
+      const int p = jj * kPollThreads + tid;
+      const bool own = p >= page0 && p < page_end;
+      const float sv = L.share[max(0, min(p - page0, (int)ppb - 1))];
+      key[jj] = order_key(own ? sv : __uint_as_float((uint32_t)e[jj]));
+    }
+    k = min(min(budget_pages(g, seq_len), n), g.k_max);
+    int pos[PER];
+    threshold_select<PER, kWaves, kPollThreads, false>(L.u.thr, key, n, k, pos, kmn, kmx);
+
+    int32_t* sel_row = const_cast<int32_t*>(sa.a.sel) + (size_t)bh * g.k_max;
+    int32_t* m_row = const_cast<int32_t*>(sa.a.msk) + (size_t)bh * g.k_max;
+#pragma unroll
+    for (int jj = 0; jj < PER; ++jj) {
+      const int p = jj * kPollThreads + tid;
+      const int q = pos[jj];
+      const int m = p == tok_lp ? sa.a.step - 1 : a_old[jj];  // Alg. 2's current-page rule
+      if (q >= first && q < first + g.pages_per_split) {
+        const int ph = (phys[jj] >= 0 && phys[jj] < g.num_phys) ? phys[jj] : -1;
+        L.s_phys[q - first] = ph;
+        L.s_len[q - first] = ph >= 0 ? min(g.P, seq_len - p * g.P) : 0;
+        L.s_mask[q - first] = m;
+        if (p == tok_lp && ph >= 0) L.s_tok = q - first;
+      }
+      if (writer) {
+        if (q >= 0) {
+          sel_row[q] = p;
+          m_row[q] = m;
+        }
+        if (tid < kPollThreads && p == tok_lp) sa.tok_out[bh] = q < 0 ? p : -1;
+      }
+    }
+    if (writer) {
+      for (int i = k + tid; i < g.k_max; i += kThreads) {
+        sel_row[i] = -1;
+        m_row[i] = -1;
+      }
+      if (tid == 0) {
+        const_cast<int32_t*>(sa.a.nsel)[bh] = k;
+        if (tok_lp < 0) sa.tok_out[bh] = -1;
+      }
+    }
+    __syncthreads();  // the split's page list is in LDS
+  };
+
+  // ---- 5: the split's attention over the window rows
+  attend_role<T, D, 1, (Tiles<T, D>::PIECES + kThreads - 1) / kThreads, true, false>(
+      sa.a, b, h, rg, split, [&] { return seq_len; }, L.u.stage, L.s_phys, L.s_len, L.s_mask,
+      &L.s_tok, tok_lp >= 0 ? seq_len - 1 : -1, select,
+      PresetList<T>{&k, tok_mine[0], tok_mine[1]});
+}
+
+template <typename T, int D, int PER, int SITERS, int GC>
+const void* kernel_ptr() {
+  return reinterpret_cast<const void*>(&step_attend_kernel<T, D, PER, SITERS, GC>);
+}
+
+constexpr int kSiters = 3;  // score passes: at most 3 * 32 pages per workgroup
+
+// The instantiation for g: (dtype, d, stripes per thread, unrolled group).
+template <typename F>
+auto dispatch(const Geometry& g, F&& f) {
+  const bool g4 = g.G == 4;
+  auto per = [&](auto t, auto d) {
+    using T = typename decltype(t)::type;
+    constexpr int DD = decltype(d)::value;
+    if (g.max_pages <= 2 * kPollThreads)
+      return g4 ? f(kernel_ptr<T, DD, 2, kSiters, 4>(), std::integral_constant<int, 2>{}, t, d, std::integral_constant<int, 4>{})
+                : f(kernel_ptr<T, DD, 2, kSiters, 0>(), std::integral_constant<int, 2>{}, t, d, std::integral_constant<int, 0>{});
+    return g4 ? f(kernel_ptr<T, DD, 5, kSiters, 4>(), std::integral_constant<int, 5>{}, t, d, std::integral_constant<int, 4>{})
+              : f(kernel_ptr<T, DD, 5, kSiters, 0>(), std::integral_constant<int, 5>{}, t, d, std::integral_constant<int, 0>{});
+  };
+  struct BF { using type = bf16_t; };
+  struct F32 { using type = float; };
+  if (g.dtype == RETRO_BF16)
+    return g.D == 128 ? per(BF{}, std::integral_constant<int, 128>{}) : per(BF{}, std::integral_constant<int, 64>{});
+  return g.D == 128 ? per(F32{}, std::integral_constant<int, 128>{}) : per(F32{}, std::integral_constant<int, 64>{});
+}
+
+// Workgroups of the kernel that fit on one compute unit at once (cached per
+// instantiation and device).
+int resident_per_cu(const void* fn) {
+  struct Entry { const void* fn; int dev; int n; };
+  static Entry cache[64];
+  static int used = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  for (int i = 0; i < used; ++i)
+    if (cache[i].fn == fn && cache[i].dev == dev) return cache[i].n;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kThreads, 0) != hipSuccess) n = 0;
+  if (used < 64) cache[used++] = Entry{fn, dev, n};
+  return n;
+}
+
+uint32_t fingerprint_of(const Geometry& g) {
+  // FNV-1a over the shape fields that fix the counter's step (NW) and the
+  // score-word layout
+  const int32_t f[] = {g.batch, g.hk, g.G, g.D, g.P, g.W, g.max_pages, g.dtype,
+                       g.n_splits, g.n_rgroups, g.k_max};
+  uint32_t x = 2166136261u;
+  for (int32_t v : f)
+    for (int i = 0; i < 4; ++i) x = (x ^ ((uint32_t)v >> (8 * i) & 0xFFu)) * 16777619u;
+  return x ? x : 1u;
+}
+
+}  // namespace
+
+int step_attend_workgroups(const Geometry& g) { return g.n_splits * g.n_rgroups * g.batch * g.hk; }
+
+bool step_attend_supported(const Geometry& g) {
+  const int nw = g.n_splits * g.n_rgroups;
+  const int ppb = (g.max_pages + nw - 1) / nw;
+  if (g.rtw != 1 || g.max_pages > 5 * kPollThreads ||
+      ppb > kSiters * (kThreads / 64) * 4 || nw > 64)
+    return false;
+  const int grid = step_attend_workgroups(g);
+  if (grid >= (1 << 16)) return false;
+  const int per_cu = dispatch(g, [](const void* fn, auto, auto, auto, auto) { return resident_per_cu(fn); });
+  return per_cu >= 1 && (int64_t)grid <= (int64_t)per_cu * compute_units();
+}
+
+hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window, const void* k_new,
+                              const void* v_new, const retro_kv_cache& c,
+                              const retro_selection& sel, void* workspace, float* o_ws,
+                              float* l_ws, int32_t* tok_out, int32_t* err, int spin_limit,
+                              uint32_t tag_bias, hipStream_t s) {
+  if (!step_attend_supported(g) || !tok_out || !err) return hipErrorInvalidValue;
+  StepAttendArgs sa;
+  sa.a = make_attend_args(g, step, q_window, c, sel, nullptr, o_ws, l_ws,
+                          reinterpret_cast<const char*>(workspace) + g.ws_dummy);
+  sa.a.sel_phys = tok_out;  // non-null: the page list carries physical pages (never read here)
+  sa.a.tok_k = k_new;
+  sa.a.tok_v = v_new;
+  sa.scores = reinterpret_cast<float*>((char*)workspace + g.ws_scores);
+  sa.A = c.last_loaded;
+  sa.tok_out = tok_out;
+  sa.err = err;
+  sa.k_new = k_new;
+  sa.v_new = v_new;
+  sa.spin_limit = spin_limit;
+  sa.tag_bias = tag_bias;
+  const uint32_t nw = (uint32_t)(g.n_splits * g.n_rgroups);
+  const uint32_t ppb = (uint32_t)((g.max_pages + (int)nw - 1) / (int)nw);
+  const uint32_t grid = (uint32_t)step_attend_workgroups(g);
+  uint64_t* tagged = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_tagged);
+  uint32_t* ctl = reinterpret_cast<uint32_t*>((char*)workspace + g.ws_heads);
+  const uint32_t fp = fingerprint_of(g);
+  const uint32_t q_bstride = (uint32_t)((g.W + 1) * g.hq * g.D);
+  return dispatch(g, [&](const void*, auto per, auto t, auto d, auto gc) {
+    using T = typename decltype(t)::type;
+    constexpr int DD = decltype(d)::value;
+    const T* q_cur = reinterpret_cast<const T*>(q_window) + (size_t)g.W * g.hq * g.D;
+    step_attend_kernel<T, DD, decltype(per)::value, kSiters, decltype(gc)::value>
+        <<<grid, kThreads, 0, s>>>(reinterpret_cast<T*>(c.digest), (uint32_t)g.max_pages, ppb,
+                                   nw, grid, q_cur, (uint32_t)g.hk, q_bstride, ctl, tagged, fp,
+                                   sa);
+    return hipGetLastError();
+  });
+}
+
+}  // namespace retro

@@ -24,13 +24,14 @@ class RetroLayer:
     def __init__(self, batch: int, num_kv_heads: int, group: int, head_dim: int, page_size: int,
                  budget: int, window: int, max_pages: int, dtype: str = "bf16",
                  num_phys_pages: Optional[int] = None, page_table: Optional[torch.Tensor] = None,
-                 sm_scale: float = 0.0, budget_permille: int = 0, device: str = "cuda"):
+                 sm_scale: float = 0.0, budget_permille: int = 0, flags: int = 0,
+                 device: str = "cuda"):
         self.device = torch.device(device)
         if num_phys_pages is None:
             num_phys_pages = batch * max_pages
         self.dims = B.Dims(batch, num_kv_heads, group, head_dim, page_size, budget, window,
                            max_pages, num_phys_pages, _RETRO_DTYPE[dtype], sm_scale,
-                           budget_permille)
+                           budget_permille, flags)
         self.k_max = B.retro_k_max(self.dims)
         self.ws_bytes = B.retro_workspace_size(self.dims)
         self.batch, self.hk, self.G, self.d = batch, num_kv_heads, group, head_dim
@@ -40,7 +41,9 @@ class RetroLayer:
         hk, d, P = num_kv_heads, head_dim, page_size
         self.k_cache = torch.zeros(num_phys_pages, hk, P, d, dtype=td, device=dev)
         self.v_cache = torch.zeros(num_phys_pages, hk, d, P, dtype=td, device=dev)
-        self.digest = torch.zeros(num_phys_pages, hk, 2, d, dtype=td, device=dev)
+        # per logical page of each sequence, as the header lays it out (not per
+        # physical page: the pool may hold more or fewer pages than batch * max_pages)
+        self.digest = torch.zeros(batch, hk, max_pages, 2, d, dtype=td, device=dev)
         if page_table is None:
             page_table = torch.arange(batch * max_pages, dtype=torch.int32).view(batch, max_pages)
         self.page_table = page_table.to(device=dev, dtype=torch.int32).contiguous()
@@ -125,6 +128,14 @@ class RetroLayer:
         outputs, not last_loaded."""
         B.retro_step_attend_partials(self.dims, step, q_window, self.cache, self.sel,
                                        self.workspace, self.ws_bytes, stream)
+
+    def scores(self, stream=None) -> torch.Tensor:
+        """The page scores [batch][h_k][max_pages] fp32 of the last call that computed
+        them (entries past a sequence's pages are unspecified)."""
+        out = torch.empty(self.batch, self.hk, self.dims.max_pages, dtype=torch.float32,
+                          device=self.device)
+        B.retro_copy_scores(self.dims, self.workspace, self.ws_bytes, out, stream)
+        return out
 
     def merge(self, step: int, stream=None) -> None:
         B.retro_merge_output_cache(self.dims, step, self.o_part, self.lse_part, self.ocache,

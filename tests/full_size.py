@@ -2,8 +2,8 @@
 
 Every step of a workload runs on the GPU through ``retro_step`` captured in a
 HIP graph and replayed (as bench.py times it).  The CPU oracle runs the same
-steps' page selection (scores, top-k, Alg. 2), and every step's selection, mask
-M, last_loaded A and sequence lengths must match bit for bit.  Outputs are
+steps' page selection (scores, top-k, Alg. 2), and every step's page scores, selection,
+mask M, last_loaded A and sequence lengths must match bit for bit.  Outputs are
 checked on sampled window rows at sampled steps against a brute-force fp64
 softmax over the exact set of tokens that row has attended so far, derived here
 from the selection history by the set form of eq. (update-sup) (a page is
@@ -21,7 +21,7 @@ import numpy as np
 
 import oracle
 import workloads as W
-from gpu_harness import TOL, _gpu_layer
+from gpu_harness import TOL, _gpu_layer, compare_scores
 from oracle_shadow import softmax_attend
 
 
@@ -45,7 +45,7 @@ def attended_tokens(sel_hist: List[np.ndarray], num_hist: List[np.ndarray],
 
 
 def run_full(spec, steps: Optional[int] = None, *, check_steps=None, rows_per_check: int = 48,
-             graph: bool = True, label: str = "") -> int:
+             graph: bool = True, label: str = "", flags: int = 0) -> int:
     import torch
     steps = spec.steps if steps is None else steps
     if check_steps is None:
@@ -58,7 +58,7 @@ def run_full(spec, steps: Optional[int] = None, *, check_steps=None, rows_per_ch
     t_start = time.time()
     gen = W.Generator(spec)
     orc = oracle.Oracle.for_spec(spec)
-    layer = _gpu_layer(spec, None)
+    layer = _gpu_layer(spec, None, flags=flags)
     for b, (k, v) in enumerate(gen.prefill()):
         orc.prefill(b, k, v)
         layer.prefill(b, k, v)
@@ -87,6 +87,7 @@ def run_full(spec, steps: Optional[int] = None, *, check_steps=None, rows_per_ch
         else:
             layer.step(t, win_d, kn_d, vn_d)
         torch.cuda.synchronize()
+        compare_scores(t, layer, ref)
         sel = layer.selected.cpu().numpy()
         num = layer.num_selected.cpu().numpy()
         assert np.array_equal(num, ref["num_selected"]), f"step {t}: num_selected differs"

@@ -12,15 +12,21 @@ import workloads as W
 TOL = {"bf16": 2e-3, "f32": 1e-5}   # max-abs on outputs and log-normalisers
 
 
-def _gpu_layer(spec, page_perm_seed: Optional[int], device="cuda"):
+def _gpu_layer(spec, page_perm_seed: Optional[int], device="cuda", flags: int = 0,
+               pool_pages: Optional[int] = None):
+    """A RetroLayer for spec.  page_perm_seed: logical pages map to a seeded random
+    choice of distinct physical pages (a shuffled table) from a pool of pool_pages
+    physical pages (default batch * max_pages)."""
     import torch
     from paper_2508_09001_amd.layer import RetroLayer
     pt = None
+    pool = spec.batch * spec.max_pages if pool_pages is None else pool_pages
     if page_perm_seed is not None:
         rng = np.random.default_rng(page_perm_seed)
-        perm = rng.permutation(spec.batch * spec.max_pages).astype(np.int32)
+        perm = rng.permutation(pool)[:spec.batch * spec.max_pages].astype(np.int32)
         pt = torch.from_numpy(perm.reshape(spec.batch, spec.max_pages))
-    return RetroLayer.for_spec(spec, page_table=pt, device=device)
+    return RetroLayer.for_spec(spec, page_table=pt, device=device, flags=flags,
+                               num_phys_pages=pool)
 
 
 class Stats:
@@ -31,9 +37,25 @@ class Stats:
         self.rows_checked = 0
 
 
+def compare_scores(t, layer, ref):
+    """The step's page scores, eq. (quest_score) in the fixed fp32 order, bit for bit
+    on every page of every sequence."""
+    s = layer.scores().cpu().numpy()
+    P = layer.P
+    for b, L in enumerate(ref["seq_lens"]):
+        n = -(-int(L) // P)
+        got = s[b, :, :n].view(np.uint32)
+        want = np.ascontiguousarray(ref["scores"][b, :, :n]).view(np.uint32)
+        if not np.array_equal(got, want):
+            bad = np.argwhere(got != want)[:5]
+            raise AssertionError(f"step {t}: page scores of sequence {b} differ at (head, page) "
+                                 f"{bad.tolist()}")
+
+
 def compare_step(t, layer, ref, tol, stats: Stats, outputs=True):
     import torch
     torch.cuda.synchronize()
+    compare_scores(t, layer, ref)
     sel = layer.selected.cpu().numpy()
     num = layer.num_selected.cpu().numpy()
     msk = layer.mask.cpu().numpy()
@@ -86,7 +108,8 @@ def reembedded_kv(orc, n: int, rng, dtype: str):
 
 def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_calls=False,
                check_outputs_from: int = 0, tol: Optional[float] = None, label: str = "",
-               update_kv: bool = False) -> Stats:
+               update_kv: bool = False, flags: int = 0,
+               pool_pages: Optional[int] = None) -> Stats:
     """Run `steps` decode steps on GPU and oracle; compare every step's selection,
     mask and A exactly, and the outputs of the steps >= check_outputs_from (the
     oracle runs attention only from check_outputs_from - W on, which is enough
@@ -96,11 +119,11 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
     print(f"[parity] {label or spec.name}: batch={spec.batch} hk={spec.num_kv_heads} "
           f"G={spec.group} d={spec.head_dim} P={spec.page_size} B={spec.budget} W={spec.window} "
           f"steps={steps} tps={spec.tokens_per_step} perm={page_perm_seed} split={split_calls} "
-          f"update_kv={update_kv}",
+          f"update_kv={update_kv} flags={flags} pool={pool_pages}",
           flush=True)
     gen = W.Generator(spec)
     orc = oracle.Oracle.for_spec(spec)
-    layer = _gpu_layer(spec, page_perm_seed)
+    layer = _gpu_layer(spec, page_perm_seed, flags=flags, pool_pages=pool_pages)
     for b, (k, v) in enumerate(gen.prefill()):
         orc.prefill(b, k, v)
         layer.prefill(b, k, v)

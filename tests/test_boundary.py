@@ -54,6 +54,7 @@ def _dims(lib, **kw):
     ("window", 65, -2), ("group", 17, -2), ("budget_tokens", 8, -1), ("max_pages", 0, -1),
     ("max_pages", 20000, -2), ("dtype", 7, -1), ("sm_scale", -1.0, -1),
     ("sm_scale", float("inf"), -1), ("sm_scale", float("nan"), -1), ("num_phys_pages", 0, -1),
+    ("flags", 8, -1), ("flags", -1, -1),
 ])
 def test_bad_dims_are_rejected(lib, field, value, status):
     d = _dims(lib, **{field: value})

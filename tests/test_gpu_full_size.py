@@ -54,6 +54,6 @@ def test_full_extreme_context_dense():
                     label="full 131k dense") > 0
 
 
-def test_full_llama_layer_32k_single_launch(monkeypatch):
-    monkeypatch.setenv("RETRO_STEP_FUSED", "1")
-    assert run_full(W.config(1), label="full 32k single launch") > 0
+def test_full_llama_layer_32k_separate_score_launch():
+    # the three-launch sequence (scores, selection + attention, combine) at full length
+    assert run_full(W.config(1), flags=1, label="full 32k separate scores") > 0

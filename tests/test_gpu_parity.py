@@ -142,36 +142,94 @@ def test_step_attend_partials_entry_point():
     assert np.array_equal(msk, want)
 
 
-def test_attention_wait_timeout_gives_nan_outputs(monkeypatch):
-    """Failure path of the two-launch step, forced from the host: every
-    per-head wait of the attention launch is made to give up after a few polls
-    (its target out of reach), so every workgroup still runs to its end; the
-    step's outputs must then be NaN, and stay NaN for the next step with that
-    workspace (the error word is sticky), whose waits are normal again."""
+def test_attention_wait_timeout_leaves_state_untouched():
+    """Failure path of the two-launch step, forced from the host through
+    RETRO_FLAG_TEST_WAIT_TIMEOUT: every wait between the workgroups of the first
+    launch gives up after a few polls (its awaited tag out of reach), so every
+    workgroup still runs to its end.  The step's outputs must be NaN, and the
+    output cache, last_loaded and seq_lens exactly as before the step; the error
+    word is sticky, so the next call fails the same way with normal waits; once
+    the workspace is zero-filled the step is retried and matches the oracle."""
     import numpy as np
+    import oracle
     import torch
-    from gpu_harness import _gpu_layer
+    from gpu_harness import TOL, Stats, _gpu_layer, compare_step
+    from paper_2508_09001_amd import binding as B
     spec = W.config(0)
     gen = W.Generator(spec)
+    orc = oracle.Oracle.for_spec(spec)
     layer = _gpu_layer(spec, None)
     for b, (k, v) in enumerate(gen.prefill()):
+        orc.prefill(b, k, v)
         layer.prefill(b, k, v)
     qw = W.QueryWindow(spec)
-    for t in range(3):
+    stats = Stats()
+    for t in range(spec.window + 3):
         k_new, v_new, q = gen.step(t)
         win = qw.push(q).copy()
-        if t == 1:
-            monkeypatch.setenv("RETRO_TEST_WAIT_TIMEOUT", "1")
-        print(f"[timeout] step {t} forced={t == 1}", flush=True)
+        ref = orc.step(t, k_new, v_new, win)
+        ref["A"] = orc.A
+        if t == spec.window + 2:  # the ring is full: every slot has state to corrupt
+            before = {n: getattr(layer, n).clone() for n in
+                      ("o_cache", "lse_cache", "last_loaded", "seq_lens")}
+            for forced in (True, False):
+                layer.dims.flags = B.RETRO_FLAG_TEST_WAIT_TIMEOUT if forced else 0
+                print(f"[timeout] step {t} forced={forced}", flush=True)
+                layer.step(t, win, k_new[-1], v_new[-1])
+                layer.dims.flags = 0
+                torch.cuda.synchronize()
+                assert torch.isnan(layer.o_out).all() and torch.isnan(layer.lse_out).all()
+                for n, v in before.items():
+                    assert torch.equal(getattr(layer, n), v), f"{n} changed by a failed step"
+                layer._lens = [int(x) for x in before["seq_lens"].cpu()]
+            layer.workspace.zero_()
+        print(f"[timeout] step {t}", flush=True)
         layer.step(t, win, k_new[-1], v_new[-1])
-        monkeypatch.delenv("RETRO_TEST_WAIT_TIMEOUT", raising=False)
-        torch.cuda.synchronize()
-        o = layer.o_out.cpu().numpy()
-        z = layer.lse_out.cpu().numpy()
-        if t == 0:
-            assert np.isfinite(o).all() and not np.isnan(z).any()
-        else:
-            assert np.isnan(o).all() and np.isnan(z).all()
+        compare_step(t, layer, ref, TOL[spec.dtype], stats)
+
+
+def test_workspace_of_another_geometry_is_refused():
+    """A workspace last used by the one-launch step of another geometry (here the
+    headline layer with W = 16, then W = 4) is refused: outputs NaN, the second
+    layer's output cache, last_loaded and seq_lens untouched."""
+    import torch
+    from gpu_harness import _gpu_layer
+    spec_a = W.config(1)
+    spec_b = W.config(1).replace(window=4)
+    la, lb = _gpu_layer(spec_a, None), _gpu_layer(spec_b, None)
+    assert lb.ws_bytes <= la.ws_bytes
+    gen_a, gen_b = W.Generator(spec_a), W.Generator(spec_b)
+    for b, (k, v) in enumerate(gen_a.prefill()):
+        la.prefill(b, k, v)
+    for b, (k, v) in enumerate(gen_b.prefill()):
+        lb.prefill(b, k, v)
+    qa, qb = W.QueryWindow(spec_a), W.QueryWindow(spec_b)
+    for t in range(2):
+        k_new, v_new, q = gen_a.step(t)
+        la.step(t, qa.push(q).copy(), k_new[-1], v_new[-1])
+    torch.cuda.synchronize()
+    assert torch.isfinite(la.o_out).all()
+    lb.workspace = la.workspace  # the same scratch, now for another geometry
+    before = {n: getattr(lb, n).clone() for n in ("o_cache", "lse_cache", "last_loaded",
+                                                  "seq_lens")}
+    k_new, v_new, q = gen_b.step(0)
+    print("[geometry] step 0 of W = 4 on a W = 16 workspace", flush=True)
+    lb.step(0, qb.push(q).copy(), k_new[-1], v_new[-1])
+    torch.cuda.synchronize()
+    assert torch.isnan(lb.o_out).all() and torch.isnan(lb.lse_out).all()
+    for n, v in before.items():
+        assert torch.equal(getattr(lb, n), v), f"{n} changed by a refused step"
+
+
+def test_page_pool_larger_than_the_tables_shuffled():
+    """Physical pages drawn at random from a pool larger than batch * max_pages
+    (digests stay per logical page): the headline layer and a ragged batch."""
+    spec = W.config(1)
+    run_parity(spec, 12, page_perm_seed=11, pool_pages=spec.batch * spec.max_pages + 3001,
+               label="32k, pool +3001 pages, shuffled")
+    spec = W.config(2)
+    run_parity(spec, 6, page_perm_seed=12, pool_pages=spec.batch * spec.max_pages + 517,
+               label="batch16, pool +517 pages, shuffled")
 
 
 def test_relative_budget_grows_with_context():
