@@ -87,8 +87,14 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.flags = d->flags;
 
   const size_t bhs = (size_t)bh;
-  x.ws_scores = 0;
-  size_t off = align256(bhs * x.max_pages * sizeof(float));
+  // per workgroup of the one-launch step: launch count, geometry fingerprint
+  // and failure mark, 128 B each; first in every geometry's layout, so that a
+  // workspace last used with another geometry shows that geometry's
+  // fingerprint in every line
+  x.ws_heads = 0;
+  size_t off = (size_t)kCtlLines * 128;
+  x.ws_scores = off;
+  off += align256(bhs * x.max_pages * sizeof(float));
   x.ws_phys = off;
   off += align256(bhs * x.k_max * sizeof(int32_t));
   x.ws_opart = off;
@@ -103,8 +109,10 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   off += align256(bhs * sizeof(int32_t));
   x.ws_tagged = off;  // the one-launch step's tagged score words, then its key-range words
   off += align256(bhs * (x.max_pages + 2 * (size_t)x.n_splits * x.n_rgroups) * sizeof(uint64_t));
-  x.ws_heads = off;  // per workgroup of that step: launch count + geometry fingerprint, 128 B each
-  off += align256(bhs * x.n_splits * x.n_rgroups * 128);
+  x.ws_lse_tag = off;  // that step's tagged log-normalisers, [b * h_k][R][splits]
+  off += align256(bhs * x.R * x.n_splits * sizeof(uint64_t));
+  x.ws_head_tag = off;  // that step's per-head words (selection done)
+  off += align256(bhs * sizeof(uint64_t));
   x.ws_dummy = off;  // never written: the stand-in of empty loads
   off += 256;
   x.ws_total = off;
@@ -314,7 +322,8 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
     return from_hip(retro::launch_step_attend(g, step, q_window, nullptr, nullptr, *cache, *sel,
                                               workspace, ws_at(workspace, g.ws_opart),
                                               ws_at(workspace, g.ws_lpart), tok, err,
-                                              wait_limit(g), wait_bias(g), (hipStream_t)stream));
+                                              wait_limit(g), wait_bias(g), nullptr, nullptr,
+                                              nullptr, (hipStream_t)stream));
   }
   return from_hip(retro::launch_attend_select(g, step, q_window, *cache, *sel, phys,
                                               ws_at(workspace, g.ws_scores),
@@ -379,16 +388,11 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   Geometry gp = g;
   gp.token_pending = 1;
   if (one_launch(gp)) {
-    // scores (+ the token's append), selection and attention in one launch ->
-    // combine + merge (+ last_loaded update, + seq_lens advance)
-    hipError_t e = retro::launch_step_attend(gp, step, q_window, k_new, v_new, *cache, *sel,
-                                             workspace, o_ws, l_ws, tok, err, wait_limit(g),
-                                             wait_bias(g), s);
-    if (e == hipSuccess)
-      e = retro::launch_combine_merge(gp, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
-                                      nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s,
-                                      sel->selected, tok, err);
-    return from_hip(e);
+    // scores (+ the token's append), selection, attention, combine + merge,
+    // last_loaded update and seq_lens advance in one launch
+    return from_hip(retro::launch_step_attend(gp, step, q_window, k_new, v_new, *cache, *sel,
+                                              workspace, o_ws, l_ws, tok, err, wait_limit(g),
+                                              wait_bias(g), ocache, o_out, lse_out, s));
   }
   if (retro::attend_selects(gp) && !(g.flags & RETRO_FLAG_SELECT_IN_SCORES)) {
     // score (+ the token's append) -> attention with the selection in front ->

@@ -55,9 +55,10 @@ struct Geometry {
   // workspace layout (bytes): page scores, physical ids of the selection,
   // split partials, the sticky error word, the score launch's counters, the
   // step token's page per head, the one-launch step's tagged score words and
-  // per-head counter lines, a dummy line (never written) for empty loads
+  // per-workgroup counter lines, its tagged log-normalisers of the partials and
+  // per-head words, a dummy line (never written) for empty loads
   size_t ws_scores, ws_phys, ws_opart, ws_lpart, ws_err, ws_sel, ws_tok, ws_tagged, ws_heads,
-      ws_dummy, ws_total;
+      ws_lse_tag, ws_head_tag, ws_dummy, ws_total;
   // set for the launches of a step whose token is written by its score launch:
   // seq_lens does not count the token yet (the merge launch advances it), and
   // every launch uses the length with the token
@@ -70,6 +71,8 @@ constexpr int kSelCounterInts = 32;
 constexpr int kSelMaxGroups = 8;
 // polls of a bounded wait (about 0.2 us each) before it gives up
 constexpr int kSpinLimit = 1 << 18;
+// control lines of the one-launch step (its largest grid)
+constexpr int kCtlLines = 1024;
 
 retro_status make_geometry(const retro_dims* d, Geometry* g);
 int attend_min_waves(int dtype, int D);
@@ -110,23 +113,29 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
                                 const retro_kv_cache& c, const retro_selection& sel,
                                 int32_t* sel_phys, const float* scores, float* o_ws, float* l_ws,
                                 int32_t* tok_out, const void* dummy, hipStream_t s);
-// Page scores (+ the token's append), selection and attention in one launch
-// (step_attend.hip): the workgroups of a KV head score its pages, publish them
-// as tagged words, each reads them all and selects, then attends its split.
+// Page scores (+ the token's append), selection, attention and (with o_out)
+// the combine + merge of a step in one launch (step_attend.hip): the
+// workgroups of a KV head score its pages, publish them as tagged words, each
+// reads them all and selects, attends its split, publishes the split's
+// log-normalisers as tagged words, and then combines a share of the head's rows
+// with the output cache; the head's first workgroup applies the last_loaded
+// update, and the sequence's first advances seq_lens (with g.token_pending).
 // Only when every workgroup is resident at once (step_attend_supported:
 // occupancy times compute units; rtw == 1, max_pages <= 2560, at most 96 pages
-// scored per workgroup).  Uses the workspace's tagged score words and per-head
-// counter lines (zero-filled once, then only grown; refused with the error
-// word set if last used with another geometry); err: set if a wait ran past
-// spin_limit polls (tag_bias != 0 makes every wait give up, for tests).  The
-// combine launch after it updates last_loaded as for launch_attend_select.
+// scored per workgroup, at most 64 workgroups per head and 64 KV heads).  Uses
+// the workspace's tagged words and per-workgroup counter lines (zero-filled
+// once, then only grown; refused with the error word set if last used with
+// another geometry); err: set if a wait ran past spin_limit polls (tag_bias != 0
+// makes every wait give up, for tests).  Without o_out, only the partials are
+// written (o_ws, l_ws), with the selection, and last_loaded is left as it is.
 bool step_attend_supported(const Geometry& g);
 int step_attend_workgroups(const Geometry& g);
 hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window, const void* k_new,
                               const void* v_new, const retro_kv_cache& c,
                               const retro_selection& sel, void* workspace, float* o_ws,
                               float* l_ws, int32_t* tok_out, int32_t* err, int spin_limit,
-                              uint32_t tag_bias, hipStream_t s);
+                              uint32_t tag_bias, const retro_output_cache* oc, float* o_out,
+                              float* lse_out, hipStream_t s);
 int compute_units();
 // mode 0: combine splits -> o_part/lse_part; 1: o_part -> output cache; 2: splits -> cache
 // With g.token_pending and a cache, the launch also advances seq_lens past the

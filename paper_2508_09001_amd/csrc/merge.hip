@@ -35,26 +35,6 @@ __device__ __forceinline__ void update_last_loaded(const MergeArgs& a, int bh) {
   if (lane == 0 && tok >= 0 && tok < g.max_pages) arow[tok] = a.step - 1;
 }
 
-// The output rows merge unit `unit` writes, as NaN (nothing else is written).
-template <int D>
-__device__ void poison_unit(const MergeArgs& a, int unit) {
-  const Geometry& g = a.g;
-  int u = unit;
-  const int x = u % a.xs;
-  u /= a.xs;
-  const int gq = u % g.G;
-  u /= g.G;
-  const int h = u % g.hk, b = u / g.hk;
-  const int qh = h * g.G + gq;
-  const int64_t out_row = (int64_t)b * (g.W + 1);
-  Row<D> p;
-#pragma unroll
-  for (int e = 0; e < Row<D>::E; ++e) p.o[e] = __builtin_nanf("");
-  p.z = __builtin_nanf("");
-  put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, p);
-  if (x == 0 && g.W > 0) put<D>(a.o_out, a.l_out, (out_row + g.W) * g.hq + qh, p);
-}
-
 template <int D>
 __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
   // units ordered (sequence, KV head, query head of the group, row slot), spread

@@ -1342,10 +1342,14 @@ struct Row {
 // flight together; groups after the first are folded in relative to the
 // running maximum.
 // COH: the partials and the selection count come from other workgroups of the
-// same launch: device-coherent loads.
-template <int D, int NR, int GS, bool COH>
+// same launch: device-coherent loads.  ZPRE: the log-normalisers are not loaded
+// here: lane s of zl.z[r] holds split s's for row r (at most 64 splits).
+struct ZLanes {
+  float z[2];
+};
+template <int D, int NR, int GS, bool COH, bool ZPRE = false>
 __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const int (&rho)[NR],
-                                               Row<D> (&res)[NR]) {
+                                               Row<D> (&res)[NR], const ZLanes& zl) {
   constexpr int E = Row<D>::E;
   const Geometry& g = a.g;
   const int lane = thread_index() & 63;
@@ -1366,7 +1370,12 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
       const int64_t base = (int64_t)bh * g.n_splits * g.R + rho[r];
-      z[r] = lane < cnt ? get_c<COH>(a.l_ws + base + (int64_t)(s0 + lane) * g.R) : -INFINITY;
+      if constexpr (ZPRE) {
+        const float zs = __shfl(zl.z[r], min(s0 + lane, 63));
+        z[r] = lane < cnt ? zs : -INFINITY;
+      } else {
+        z[r] = lane < cnt ? get_c<COH>(a.l_ws + base + (int64_t)(s0 + lane) * g.R) : -INFINITY;
+      }
 #pragma unroll
       for (int j = 0; j < GS; ++j) {
         const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
@@ -1454,9 +1463,9 @@ __device__ Row<D> get(const float* o, const float* z, int64_t idx) {
 
 // The partial (O, Z) of window rows r[] of query head gq of (b, h): from the
 // split partials, or (mode 1) from the caller's o_part / lse_part.
-template <int D, int NR, int GS, bool COH>
+template <int D, int NR, int GS, bool COH, bool ZPRE = false>
 __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int gq, const int (&r)[NR],
-                                         Row<D> (&res)[NR]) {
+                                         Row<D> (&res)[NR], const ZLanes& zl) {
   const Geometry& g = a.g;
   if (a.mode == 1) {
 #pragma unroll
@@ -1467,15 +1476,16 @@ __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int g
   int rho[NR];
 #pragma unroll
   for (int i = 0; i < NR; ++i) rho[i] = r[i] * g.G + gq;
-  combine_splits<D, NR, GS, COH>(a, b * g.hk + h, rho, res);
+  combine_splits<D, NR, GS, COH, ZPRE>(a, b * g.hk + h, rho, res, zl);
 }
 
 // One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
 // executed by one wavefront; no barriers inside.  The unit of row 0 also
 // handles the current row W, whose cache slot is the one row 0 leaves.  GS:
-// splits whose loads are in flight together (at most 64).
-template <int D, int GS, bool COH = false>
-__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
+// splits whose loads are in flight together (at most 64).  ZPRE: the splits'
+// log-normalisers of the unit's rows (x, then W for x == 0 < W) are in zl.
+template <int D, int GS, bool COH = false, bool ZPRE = false>
+__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const ZLanes& zl = ZLanes{}) {
   const Geometry& g = a.g;
   const int W = g.W;
   int u = unit;
@@ -1489,7 +1499,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
 
   if (a.mode == 0 || x == W) {  // plain combine of row x (W == 0: the current row only)
     Row<D> p[1];
-    partials<D, 1, GS, COH>(a, b, h, gq, {x}, p);
+    partials<D, 1, GS, COH, ZPRE>(a, b, h, gq, {x}, p, zl);
     if (a.mode == 0)
       put<D>(a.o_part_out, a.l_part_out, (out_row + x) * g.hq + qh, p[0]);
     else
@@ -1510,7 +1520,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
     const int64_t ci = ((int64_t)b * W + tau0 % W) * g.hq + qh;
     const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
     Row<D> p[1];
-    partials<D, 1, GS, COH>(a, b, h, gq, {x}, p);
+    partials<D, 1, GS, COH, ZPRE>(a, b, h, gq, {x}, p, zl);
     const Row<D> merged = lse_merge<D>(cached, p[0]);
     put<D>(a.o_cache, a.l_cache, ci, merged);
     put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, merged);
@@ -1522,7 +1532,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   Row<D> cached = zero;
   if (tau0 >= 0) cached = get<D>(a.o_cache, a.l_cache, slot);
   Row<D> p[2];
-  partials<D, 2, GS, COH>(a, b, h, gq, {0, W}, p);
+  partials<D, 2, GS, COH, ZPRE>(a, b, h, gq, {0, W}, p, zl);
   const Row<D> merged = tau0 >= 0 ? lse_merge<D>(cached, p[0]) : zero;
   put<D>(a.o_out, a.l_out, out_row * g.hq + qh, merged);
   put<D>(a.o_out, a.l_out, (out_row + W) * g.hq + qh, p[1]);
@@ -1531,5 +1541,31 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit) {
   asm volatile("" : : "v"(merged.z) : "memory");
   put<D>(a.o_cache, a.l_cache, slot, p[1]);
 }
+
+// The output rows merge unit `unit` writes, as NaN; nothing else is written
+// (the output cache keeps its rows).
+template <int D>
+__device__ void poison_unit(const MergeArgs& a, int unit) {
+  const Geometry& g = a.g;
+  int u = unit;
+  const int x = u % a.xs;
+  u /= a.xs;
+  const int gq = u % g.G;
+  u /= g.G;
+  const int h = u % g.hk, b = u / g.hk;
+  const int qh = h * g.G + gq;
+  const int64_t out_row = (int64_t)b * (g.W + 1);
+  Row<D> p;
+#pragma unroll
+  for (int e = 0; e < Row<D>::E; ++e) p.o[e] = __builtin_nanf("");
+  p.z = __builtin_nanf("");
+  put<D>(a.o_out, a.l_out, (out_row + x) * g.hq + qh, p);
+  if (x == 0 && g.W > 0) put<D>(a.o_out, a.l_out, (out_row + g.W) * g.hq + qh, p);
+}
+
+MergeArgs make_merge_args(const Geometry& g, int step, int mode, const float* o_ws,
+                          const float* l_ws, const int32_t* num_selected, const float* o_part,
+                          const float* l_part, float* o_part_out, float* l_part_out,
+                          const retro_output_cache* oc, float* o_out, float* lse_out);
 
 }  // namespace retro

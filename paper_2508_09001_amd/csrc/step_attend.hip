@@ -65,14 +65,10 @@ struct StepAttendArgs {
   const void* v_new;
   int spin_limit;      // polls before a wait gives up
   uint32_t tag_bias;   // added to the awaited tag (tests: makes every wait give up)
-  // the combine + merge in the same launch (null o_out: partials only)
-  uint64_t* lse_tag;   // [batch * h_k][splits][R]: tagged log-normaliser of each partial row
-  uint32_t* done;      // per sequence, a 128-byte line: heads past their selection (never reset)
-  float* o_cache;      // output cache ring [batch][W][h_q][d] + [batch][W][h_q]
-  float* l_cache;
-  float* o_out;        // [batch][W + 1][h_q][d] + [batch][W + 1][h_q]
-  float* l_out;
-  int32_t* seq_lens;   // advanced past the token once every head of the sequence has read it
+  // the combine + merge in the same launch (m.o_out null: partials only)
+  MergeArgs m;
+  uint64_t* lse_tag;   // [batch * h_k][R][splits]: tagged log-normaliser of each partial row
+  uint64_t* head_tag;  // [batch * h_k]: tagged once the head's first workgroup has selected
 };
 
 template <typename T, int D, int PER, int SITERS>
@@ -123,15 +119,26 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   const bool publisher = wave == kWaves - 1;
 
   // this workgroup's own line: [0, 1] its launches (64 bits), [2] the geometry
-  // fingerprint; read first (no other workgroup touches the line)
+  // fingerprint, [3] the failure mark (set in every line when a wait of any
+  // workgroup gives up); read first (only failing workgroups write other
+  // workgroups' lines)
   uint32_t* line = ctl + ((size_t)bh * nw + j) * 32;
   uint64_t launches = 0;
-  uint32_t fp_seen = 0;
+  uint32_t fp_seen = 0, marked = 0;
   if (tid == 0) {
     launches = __hip_atomic_load(reinterpret_cast<uint64_t*>(line), __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_AGENT);
     fp_seen = __hip_atomic_load(line + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    marked = __hip_atomic_load(line + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  // a wait gave up (wavefront-uniform call): the sticky error word for the
+  // caller, and the failure mark in every workgroup's line, so that every later
+  // launch on this workspace fails from its start without a shared read
+  auto give_up = [&] {
+    if (lane == 0) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (uint32_t i = (uint32_t)lane; i < ngrid; i += 64)
+      __hip_atomic_store(ctl + (size_t)i * 32 + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
   int seq_len = 0, tok_lp = -1;
   StepToken<T> tok{-1, 0, nullptr, nullptr, nullptr, nullptr};
   T tok_kv[2][(D + 63) / 64];  // the publisher's lanes: the token's key and value elements
@@ -185,16 +192,20 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       [&] {
         thr_clear(L.u.thr);
         if (tid == 0) {
-          const bool bad = fp_seen != 0 && fp_seen != fingerprint;
-          if (bad) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const bool foreign = fp_seen != 0 && fp_seen != fingerprint;
+          if (foreign) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           L.epoch = (uint32_t)launches + 1u;
           L.fp_seen = fp_seen;
-          L.bad = bad;
+          L.bad = foreign || marked != 0;
         }
       },
       [&](int page, float v) { L.share[page - page0] = v; }, L.dig);
 
   const int n = min((seq_len + g.P - 1) / g.P, (int)mp);
+  // Every load of caller state this workgroup makes (seq_lens, last_loaded, the
+  // page table) has returned before its first tagged store below: a workgroup
+  // that sees one of its tags may overwrite that state.
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();  // the share's scores and the token page's digest row are in LDS
 
   // ---- 2: the publisher stores: score words and the share's key range
@@ -237,6 +248,14 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
                          __HIP_MEMORY_SCOPE_AGENT);
       if (L.fp_seen == 0)
         __hip_atomic_store(line + 2, fingerprint, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (L.fp_seen == 0) {
+      // a fresh workspace: the fingerprint also goes into the lines no
+      // workgroup of this geometry owns (u + k * ngrid, k >= 1), so that a
+      // later launch of any other geometry finds it in its own line
+      for (uint32_t i = u + ngrid * (1u + (uint32_t)lane); i < (uint32_t)kCtlLines; i += 64u * ngrid)
+        __hip_atomic_store(ctl + (size_t)i * 32 + 2, fingerprint, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 
@@ -287,7 +306,8 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       for (int r = 0; r < HW; ++r) stale = stale || (hword(r) && (uint32_t)(hv[r] >> 32) != want);
       if (wave_ballot(stale) == 0 || bad) break;  // wavefront-uniform
       if (it >= sa.spin_limit) {
-        if (lane == 0) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        give_up();
+        if (lane == 0) L.bad = 1;
         break;
       }
       __builtin_amdgcn_s_sleep(2);
@@ -325,6 +345,11 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
 
     int32_t* sel_row = const_cast<int32_t*>(sa.a.sel) + (size_t)bh * g.k_max;
     int32_t* m_row = const_cast<int32_t*>(sa.a.msk) + (size_t)bh * g.k_max;
+    // Alg. 2's last_loaded update (with the combine: the whole step), by the
+    // head's writer once its wait succeeded: every workgroup of the head has
+    // read its stripe of the row by then (their tags are out)
+    int32_t* a_row = sa.A + (size_t)bh * mp;
+    const bool upd = writer && sa.m.o_out && L.bad == 0;
 #pragma unroll
     for (int jj = 0; jj < PER; ++jj) {
       const int p = jj * kPollThreads + tid;
@@ -344,6 +369,10 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
         }
         if (tid < kPollThreads && p == tok_lp) sa.tok_out[bh] = q < 0 ? p : -1;
       }
+      if (upd && tid < kPollThreads && p < n) {
+        if (q >= 0) a_row[p] = sa.a.step;
+        else if (p == tok_lp) a_row[p] = sa.a.step - 1;
+      }
     }
     if (writer) {
       for (int i = k + tid; i < g.k_max; i += kThreads) {
@@ -358,11 +387,96 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     __syncthreads();  // the split's page list is in LDS
   };
 
-  // ---- 5: the split's attention over the window rows
-  attend_role<T, D, 1, (Tiles<T, D>::PIECES + kThreads - 1) / kThreads, true, false>(
+  // ---- 5: the split's attention over the window rows; partial outputs
+  // written through (sc1), log-normalisers into LDS
+  attend_role<T, D, 1, (Tiles<T, D>::PIECES + kThreads - 1) / kThreads, true, true>(
       sa.a, b, h, rg, split, [&] { return seq_len; }, L.u.stage, L.s_phys, L.s_len, L.s_mask,
       &L.s_tok, tok_lp >= 0 ? seq_len - 1 : -1, select,
-      PresetList<T>{&k, tok_mine[0], tok_mine[1]});
+      PresetList<T>{&k, tok_mine[0], tok_mine[1], L.lse});
+
+  // ---- 6: once every wavefront's partial-output stores are acknowledged, the
+  // split's log-normalisers go out as tagged words (epoch, error bit)
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  const int rows0 = rg * g.tiles_per_group * 16;
+  const int nrows = min(g.tiles_per_group * 16, g.R - rows0);
+  const MergeArgs& m = sa.m;
+  if (!m.o_out) {  // partials only
+    float* lrow = sa.a.l_ws + ((size_t)bh * n_splits + split) * g.R + rows0;
+    for (int r = tid; r < nrows; r += kThreads) lrow[r] = L.lse[r];
+    return;
+  }
+  const bool failed = L.bad != 0;
+  if (publisher) {
+    const uint64_t hi = (uint64_t)(L.epoch | (failed ? 0x80000000u : 0u)) << 32;
+    for (int r = lane; r < nrows; r += 64)
+      __hip_atomic_store(sa.lse_tag + ((size_t)bh * g.R + rows0 + r) * n_splits + split,
+                         hi | __float_as_uint(L.lse[r]), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    if (writer && lane == 0)
+      __hip_atomic_store(sa.head_tag + bh, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
+  // ---- 7: combine + merge (merge_unit): unit ul of the head's G * max(W, 1)
+  // goes to workgroup ul % nw, wavefront ul / nw (the publisher last).  A unit
+  // waits until the tags of its rows carry the epoch in every split, then
+  // reads the partial rows device-coherently; a failure anywhere in its inputs
+  // makes its output rows NaN and leaves its cache slot as it was.
+  const uint32_t want = L.epoch + sa.tag_bias;
+  auto current = [&](uint64_t w) { return ((uint32_t)(w >> 32) & 0x7FFFFFFFu) == want; };
+  auto broken = [&](uint64_t w) { return (w >> 63) != 0; };
+  const int xs = g.W > 0 ? g.W : 1;
+  const int units = g.G * xs;
+  for (int ul = (int)j + (int)nw * wave; ul < units; ul += (int)nw * kWaves) {  // wavefront-uniform
+    const int x = ul % xs, gq = ul / xs;
+    const bool two = g.W > 0 && x == 0;  // rows 0 and W
+    const uint64_t* t0 = sa.lse_tag + ((size_t)bh * g.R + x * g.G + gq) * n_splits;
+    const uint64_t* t1 = sa.lse_tag + ((size_t)bh * g.R + g.W * g.G + gq) * n_splits;
+    const bool l0 = lane < n_splits, l1 = two && lane < n_splits;
+    uint64_t w0 = l0 ? __hip_atomic_load(t0 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    uint64_t w1 = l1 ? __hip_atomic_load(t1 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    bool timed_out = false;
+    for (int it = 0;; ++it) {
+      const bool stale = (l0 && !current(w0)) || (l1 && !current(w1));
+      if (wave_ballot(stale) == 0) break;
+      if (it >= sa.spin_limit) {
+        timed_out = true;
+        give_up();
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      if (l0 && !current(w0)) w0 = __hip_atomic_load(t0 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (l1 && !current(w1)) w1 = __hip_atomic_load(t1 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const int unit = (int)bh * units + ul;
+    if (failed || timed_out || wave_ballot((l0 && broken(w0)) || (l1 && broken(w1))) != 0) {
+      poison_unit<D>(m, unit);
+      continue;
+    }
+    const ZLanes zl{{__uint_as_float((uint32_t)w0), __uint_as_float((uint32_t)w1)}};
+    merge_unit<D, 32, true, true>(m, unit, zl);
+  }
+
+  // ---- 8: seq_lens advances past the token once the first workgroup of every
+  // head of the sequence has selected (every workgroup of the sequence has
+  // then read seq_lens) and none of them failed
+  if (g.token_pending && m.seq_lens && h == 0 && j == 0 && wave == kWaves - 2) {
+    const bool lh = lane < (int)hk;
+    const uint64_t* ht = sa.head_tag + (size_t)b * hk;
+    uint64_t w = lh ? __hip_atomic_load(ht + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    bool ok = !failed;
+    for (int it = 0; ok; ++it) {
+      if (wave_ballot(lh && !current(w)) == 0) break;
+      if (it >= sa.spin_limit) {
+        ok = false;
+        give_up();
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      if (lh && !current(w)) w = __hip_atomic_load(ht + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (ok && wave_ballot(lh && broken(w)) == 0 && lane == 0 && tok_lp >= 0) m.seq_lens[b] = seq_len;
+  }
 }
 
 template <typename T, int D, int PER, int SITERS, int GC>
@@ -427,10 +541,12 @@ bool step_attend_supported(const Geometry& g) {
   const int nw = g.n_splits * g.n_rgroups;
   const int ppb = (g.max_pages + nw - 1) / nw;
   if (g.rtw != 1 || g.max_pages > 5 * kPollThreads ||
-      ppb > kSiters * (kThreads / 64) * 4 || nw > 64)
+      ppb > kSiters * (kThreads / 64) * 4 || nw > 64 || g.hk > 64 || g.n_splits > 64)
     return false;
+  // partial outputs are read through a buffer resource of 2 GiB
+  if ((int64_t)g.batch * g.hk * g.n_splits * g.R * g.D * 4 >= (int64_t(1) << 31)) return false;
   const int grid = step_attend_workgroups(g);
-  if (grid >= (1 << 16)) return false;
+  if (grid > kCtlLines) return false;
   const int per_cu = dispatch(g, [](const void* fn, auto, auto, auto, auto) { return resident_per_cu(fn); });
   return per_cu >= 1 && (int64_t)grid <= (int64_t)per_cu * compute_units();
 }
@@ -439,8 +555,11 @@ hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window,
                               const void* v_new, const retro_kv_cache& c,
                               const retro_selection& sel, void* workspace, float* o_ws,
                               float* l_ws, int32_t* tok_out, int32_t* err, int spin_limit,
-                              uint32_t tag_bias, hipStream_t s) {
+                              uint32_t tag_bias, const retro_output_cache* oc, float* o_out,
+                              float* lse_out, hipStream_t s) {
   if (!step_attend_supported(g) || !tok_out || !err) return hipErrorInvalidValue;
+  if (o_out && (!lse_out || (g.W > 0 && (!oc || !oc->o_cache || !oc->lse_cache))))
+    return hipErrorInvalidValue;
   StepAttendArgs sa;
   sa.a = make_attend_args(g, step, q_window, c, sel, nullptr, o_ws, l_ws,
                           reinterpret_cast<const char*>(workspace) + g.ws_dummy);
@@ -455,6 +574,12 @@ hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window,
   sa.v_new = v_new;
   sa.spin_limit = spin_limit;
   sa.tag_bias = tag_bias;
+  sa.m = make_merge_args(g, step, 2, o_ws, l_ws, sel.num_selected, nullptr, nullptr, nullptr,
+                         nullptr, oc, o_out, lse_out);
+  sa.m.seq_lens = c.seq_lens;
+  sa.m.pt = c.page_table;
+  sa.lse_tag = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_lse_tag);
+  sa.head_tag = reinterpret_cast<uint64_t*>((char*)workspace + g.ws_head_tag);
   const uint32_t nw = (uint32_t)(g.n_splits * g.n_rgroups);
   const uint32_t ppb = (uint32_t)((g.max_pages + (int)nw - 1) / (int)nw);
   const uint32_t grid = (uint32_t)step_attend_workgroups(g);

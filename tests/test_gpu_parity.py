@@ -218,7 +218,12 @@ def test_workspace_of_another_geometry_is_refused():
     torch.cuda.synchronize()
     assert torch.isnan(lb.o_out).all() and torch.isnan(lb.lse_out).all()
     for n, v in before.items():
-        assert torch.equal(getattr(lb, n), v), f"{n} changed by a refused step"
+        now = getattr(lb, n)
+        diff = torch.nonzero(now != v)
+        assert diff.numel() == 0, (f"{n} changed by a refused step at {diff.shape[0]} entries "
+                                   f"(NaN before the step: {bool(torch.isnan(v).any()) if v.is_floating_point() else False}), "
+                                   f"first {diff[:4].tolist()}: {now[tuple(diff[:4].T)].tolist()} "
+                                   f"(was {v[tuple(diff[:4].T)].tolist()})")
 
 
 def test_page_pool_larger_than_the_tables_shuffled():
