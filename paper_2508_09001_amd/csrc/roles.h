@@ -830,15 +830,18 @@ AttendArgs make_attend_args(const Geometry& g, int step, const void* q_window,
 // of the split (-1 / 0 / 0 past the kept pages), *s_tok (the slot of the
 // token's page, -1 if not in the split), and gives the number of kept pages
 // and, for the first d threads, the token's key and value elements.
-// With COH, a PresetList's s_lse (16 floats of LDS per row tile of the group)
-// receives each row's log-normaliser, at the row's place in the group, instead
-// of the workspace (the caller publishes them once the partial outputs are
-// known to be complete).
+// With COH and a PresetList whose lse_tag is set, each wavefront publishes
+// its rows' log-normalisers itself once its partial-output stores are
+// acknowledged: one 64-bit word per (row, split), the launch's epoch (bit 31:
+// *bad, the workgroup failed) over the value's bits, at lse_tag[(b * h_k +
+// h) * R + row][split]; without lse_tag they go to l_ws as usual.
 template <typename T>
 struct PresetList {
   const int* k;  // read once wait() has returned
   T tok_k, tok_v;
-  float* s_lse;
+  uint64_t* lse_tag;
+  const uint32_t* epoch;  // read at the end
+  const int* bad;
 };
 template <typename L>
 struct is_preset : std::false_type {};
@@ -1288,9 +1291,21 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
           __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(orow + dt * 16 + 4 * g4));
         }
       }
-      if (g4 == 0) {
-        if constexpr (COH && is_preset<typename std::decay<List>::type>::value) list.s_lse[lt * 16 + ln16] = lse;
-        else if constexpr (COH) put_c<true>(a.l_ws + part + rho, lse);
+      if constexpr (COH && is_preset<typename std::decay<List>::type>::value) {
+        if (list.lse_tag) {
+          // the row's output words are acknowledged (written through) before
+          // its tag goes out: a reader that sees the tag finds them
+          __builtin_amdgcn_s_waitcnt(0);
+          if (g4 == 0) {
+            const uint64_t hi = (uint64_t)(*list.epoch | (*list.bad ? 0x80000000u : 0u)) << 32;
+            __hip_atomic_store(list.lse_tag + ((int64_t)bh * g.R + rho) * g.n_splits + split,
+                               hi | __float_as_uint(lse), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        } else if (g4 == 0) {
+          a.l_ws[part + rho] = lse;
+        }
+      } else if (g4 == 0) {
+        if constexpr (COH) put_c<true>(a.l_ws + part + rho, lse);
         else __builtin_nontemporal_store(lse, a.l_ws + part + rho);
       }
     }
@@ -1426,7 +1441,7 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
 }
 
 template <int D>
-__device__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
+__device__ __forceinline__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
   Row<D> r;
   const float m = fmaxf(x.z, y.z);
   if (m == -INFINITY) {
@@ -1444,7 +1459,7 @@ __device__ Row<D> lse_merge(const Row<D>& x, const Row<D>& y) {
 }
 
 template <int D>
-__device__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
+__device__ __forceinline__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
   const int e0 = (thread_index() & 63) * Row<D>::E;
 #pragma unroll
   for (int e = 0; e < Row<D>::E; ++e) o[idx * D + e0 + e] = v.o[e];
@@ -1452,7 +1467,7 @@ __device__ void put(float* o, float* z, int64_t idx, const Row<D>& v) {
 }
 
 template <int D>
-__device__ Row<D> get(const float* o, const float* z, int64_t idx) {
+__device__ __forceinline__ Row<D> get(const float* o, const float* z, int64_t idx) {
   Row<D> v;
   const int e0 = (thread_index() & 63) * Row<D>::E;
 #pragma unroll
@@ -1545,7 +1560,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const Z
 // The output rows merge unit `unit` writes, as NaN; nothing else is written
 // (the output cache keeps its rows).
 template <int D>
-__device__ void poison_unit(const MergeArgs& a, int unit) {
+__device__ __forceinline__ void poison_unit(const MergeArgs& a, int unit) {
   const Geometry& g = a.g;
   int u = unit;
   const int x = u % a.xs;

@@ -81,7 +81,10 @@ struct StepLds {
   float share[SITERS * kWaves * 4];  // this workgroup's scores
   T dig[2 * D];                   // the token page's widened digest row
   int s_phys[kMaxSplitPages], s_len[kMaxSplitPages], s_mask[kMaxSplitPages];
-  float lse[kWaves * 16];         // the split's partial log-normaliser of the group's rows
+  // the head writer's selection (page, mask value per kept slot) and the
+  // token's page if it is not kept (-1 otherwise), stored after the attention
+  int wsel[5 * (kThreads - 64)], wmsk[5 * (kThreads - 64)];  // up to the largest page count
+  int wtok;
   int s_tok;
   uint32_t epoch, fp_seen;
   int bad;                        // this workgroup failed (see StepAttendArgs::err)
@@ -343,13 +346,6 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     int pos[PER];
     threshold_select<PER, kWaves, kPollThreads, false>(L.u.thr, key, n, k, pos, kmn, kmx);
 
-    int32_t* sel_row = const_cast<int32_t*>(sa.a.sel) + (size_t)bh * g.k_max;
-    int32_t* m_row = const_cast<int32_t*>(sa.a.msk) + (size_t)bh * g.k_max;
-    // Alg. 2's last_loaded update (with the combine: the whole step), by the
-    // head's writer once its wait succeeded: every workgroup of the head has
-    // read its stripe of the row by then (their tags are out)
-    int32_t* a_row = sa.A + (size_t)bh * mp;
-    const bool upd = writer && sa.m.o_out && L.bad == 0;
 #pragma unroll
     for (int jj = 0; jj < PER; ++jj) {
       const int p = jj * kPollThreads + tid;
@@ -362,28 +358,15 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
         L.s_mask[q - first] = m;
         if (p == tok_lp && ph >= 0) L.s_tok = q - first;
       }
-      if (writer) {
+      if (writer) {  // into LDS: stores here would hold up the gather's loads behind them
         if (q >= 0) {
-          sel_row[q] = p;
-          m_row[q] = m;
+          L.wsel[q] = p;
+          L.wmsk[q] = m;
         }
-        if (tid < kPollThreads && p == tok_lp) sa.tok_out[bh] = q < 0 ? p : -1;
-      }
-      if (upd && tid < kPollThreads && p < n) {
-        if (q >= 0) a_row[p] = sa.a.step;
-        else if (p == tok_lp) a_row[p] = sa.a.step - 1;
+        if (tid < kPollThreads && p == tok_lp) L.wtok = q < 0 ? p : -1;
       }
     }
-    if (writer) {
-      for (int i = k + tid; i < g.k_max; i += kThreads) {
-        sel_row[i] = -1;
-        m_row[i] = -1;
-      }
-      if (tid == 0) {
-        const_cast<int32_t*>(sa.a.nsel)[bh] = k;
-        if (tok_lp < 0) sa.tok_out[bh] = -1;
-      }
-    }
+    if (writer && tid == 0 && tok_lp < 0) L.wtok = -1;
     __syncthreads();  // the split's page list is in LDS
   };
 
@@ -392,29 +375,44 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   attend_role<T, D, 1, (Tiles<T, D>::PIECES + kThreads - 1) / kThreads, true, true>(
       sa.a, b, h, rg, split, [&] { return seq_len; }, L.u.stage, L.s_phys, L.s_len, L.s_mask,
       &L.s_tok, tok_lp >= 0 ? seq_len - 1 : -1, select,
-      PresetList<T>{&k, tok_mine[0], tok_mine[1], L.lse});
+      PresetList<T>{&k, tok_mine[0], tok_mine[1], sa.m.o_out ? sa.lse_tag : nullptr, &L.epoch,
+                    &L.bad});
 
-  // ---- 6: once every wavefront's partial-output stores are acknowledged, the
-  // split's log-normalisers go out as tagged words (epoch, error bit)
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  const int rows0 = rg * g.tiles_per_group * 16;
-  const int nrows = min(g.tiles_per_group * 16, g.R - rows0);
+  // ---- 6: each wavefront has published its rows' log-normalisers (tagged)
   const MergeArgs& m = sa.m;
+  // the head writer's selection outputs (rows, mask values, count) and Alg.
+  // 2's last_loaded update (with the combine: the whole step), after the
+  // attention (stores before it would hold up the gather's loads), by
+  // wavefronts 0-3 (the combine's units start on wavefront 0 and wait for the
+  // other splits anyway).  Every workgroup of the head has read its stripe of
+  // last_loaded before its score tags went out, so the row may change now.
+  auto writer_outputs = [&](int t, int nt) {
+    int32_t* sel_row = const_cast<int32_t*>(sa.a.sel) + (size_t)bh * g.k_max;
+    int32_t* m_row = const_cast<int32_t*>(sa.a.msk) + (size_t)bh * g.k_max;
+    int32_t* a_row = sa.A + (size_t)bh * mp;
+    const bool upd = m.o_out && L.bad == 0;
+    for (int i = t; i < g.k_max; i += nt) {
+      const bool kept = i < k;
+      const int p = kept ? L.wsel[i] : -1;
+      sel_row[i] = p;
+      m_row[i] = kept ? L.wmsk[i] : -1;
+      if (upd && kept) a_row[p] = sa.a.step;
+    }
+    if (t == 0) {
+      const_cast<int32_t*>(sa.a.nsel)[bh] = k;
+      sa.tok_out[bh] = L.wtok;
+      if (upd && L.wtok >= 0) a_row[L.wtok] = sa.a.step - 1;
+    }
+  };
   if (!m.o_out) {  // partials only
-    float* lrow = sa.a.l_ws + ((size_t)bh * n_splits + split) * g.R + rows0;
-    for (int r = tid; r < nrows; r += kThreads) lrow[r] = L.lse[r];
+    if (writer) writer_outputs(tid, kThreads);
     return;
   }
   const bool failed = L.bad != 0;
-  if (publisher) {
+  if (publisher && writer && lane == 0) {
+    // the head has selected: every workgroup of it has read seq_lens
     const uint64_t hi = (uint64_t)(L.epoch | (failed ? 0x80000000u : 0u)) << 32;
-    for (int r = lane; r < nrows; r += 64)
-      __hip_atomic_store(sa.lse_tag + ((size_t)bh * g.R + rows0 + r) * n_splits + split,
-                         hi | __float_as_uint(L.lse[r]), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    if (writer && lane == 0)
-      __hip_atomic_store(sa.head_tag + bh, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(sa.head_tag + bh, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
   // ---- 7: combine + merge (merge_unit): unit ul of the head's G * max(W, 1)
@@ -427,8 +425,16 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   auto broken = [&](uint64_t w) { return (w >> 63) != 0; };
   const int xs = g.W > 0 ? g.W : 1;
   const int units = g.G * xs;
-  for (int ul = (int)j + (int)nw * wave; ul < units; ul += (int)nw * kWaves) {  // wavefront-uniform
-    const int x = ul % xs, gq = ul / xs;
+  const int nwi = (int)nw;
+  // the units in the order x * G + gq (the G two-row units of x = 0 first) to
+  // workgroups 1, 2, ..., nw - 1, 0 (the head's writer last), then to the next
+  // wavefront; the writer's outputs go out from the wavefronts without units
+  // (else the last, after its units)
+  const int uw = min(kWaves - 1, (units + nwi - 1) / nwi);
+  if (writer && wave >= uw && uw < kWaves - 1) writer_outputs(tid - 64 * uw, kThreads - 64 * uw);
+  for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
+    const int x = kk / g.G, gq = kk - x * g.G;
+    const int ul = gq * xs + x;
     const bool two = g.W > 0 && x == 0;  // rows 0 and W
     const uint64_t* t0 = sa.lse_tag + ((size_t)bh * g.R + x * g.G + gq) * n_splits;
     const uint64_t* t1 = sa.lse_tag + ((size_t)bh * g.R + g.W * g.G + gq) * n_splits;
@@ -456,6 +462,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     const ZLanes zl{{__uint_as_float((uint32_t)w0), __uint_as_float((uint32_t)w1)}};
     merge_unit<D, 32, true, true>(m, unit, zl);
   }
+  if (writer && uw == kWaves - 1 && wave == kWaves - 1) writer_outputs(lane, 64);
 
   // ---- 8: seq_lens advances past the token once the first workgroup of every
   // head of the sequence has selected (every workgroup of the sequence has

@@ -192,6 +192,7 @@ def test_workspace_of_another_geometry_is_refused():
     """A workspace last used by the one-launch step of another geometry (here the
     headline layer with W = 16, then W = 4) is refused: outputs NaN, the second
     layer's output cache, last_loaded and seq_lens untouched."""
+    import numpy as np
     import torch
     from gpu_harness import _gpu_layer
     spec_a = W.config(1)
@@ -216,14 +217,20 @@ def test_workspace_of_another_geometry_is_refused():
     print("[geometry] step 0 of W = 4 on a W = 16 workspace", flush=True)
     lb.step(0, qb.push(q).copy(), k_new[-1], v_new[-1])
     torch.cuda.synchronize()
-    assert torch.isnan(lb.o_out).all() and torch.isnan(lb.lse_out).all()
+    # the one-launch step's per-workgroup control lines (launch count,
+    # fingerprint, failure mark), for the failure messages: a workgroup that
+    # refused the workspace counts 3 launches, one that took it as fresh 1
+    lines = lb.workspace[:1024 * 128].view(torch.int32).view(1024, 32)[:, :4].cpu().numpy()
+    info = (f"launch counts {np.unique(lines[:, 0], return_counts=True)}, fingerprints "
+            f"{np.unique(lines[:, 2], return_counts=True)}, marks {np.unique(lines[:, 3])}")
+    assert torch.isnan(lb.o_out).all() and torch.isnan(lb.lse_out).all(), info
     for n, v in before.items():
         now = getattr(lb, n)
         diff = torch.nonzero(now != v)
         assert diff.numel() == 0, (f"{n} changed by a refused step at {diff.shape[0]} entries "
                                    f"(NaN before the step: {bool(torch.isnan(v).any()) if v.is_floating_point() else False}), "
                                    f"first {diff[:4].tolist()}: {now[tuple(diff[:4].T)].tolist()} "
-                                   f"(was {v[tuple(diff[:4].T)].tolist()})")
+                                   f"(was {v[tuple(diff[:4].T)].tolist()}); {info}")
 
 
 def test_page_pool_larger_than_the_tables_shuffled():
