@@ -53,7 +53,9 @@ typedef enum {
   RETRO_EINVAL = -1,        /* null pointer, negative size, inconsistent dimension */
   RETRO_EUNSUPPORTED = -2,  /* well-formed but outside the supported shapes */
   RETRO_EHIP = -3,          /* a HIP launch or query failed */
-  RETRO_EWORKSPACE = -4     /* workspace null or smaller than retro_workspace_size() */
+  RETRO_EWORKSPACE = -4,    /* workspace null or smaller than retro_workspace_size() */
+  RETRO_ESCRATCH = -5       /* retro_step_noalloc: the step needs more than the library's
+                               static scratch, or a clear of it would be captured */
 } retro_status;
 
 typedef enum { RETRO_F32 = 0, RETRO_BF16 = 1 } retro_dtype;
@@ -302,6 +304,25 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
                         const retro_selection* sel, const retro_output_cache* ocache,
                         float* o_out, float* lse_out, void* workspace, size_t ws_bytes,
                         void* stream);
+
+/* retro_step for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same step and
+ * results, with the workspace in a static device array of the library (64 MiB
+ * per GPU, held until the process ends) instead of a caller's buffer; the
+ * caller still passes every input and output.  No allocation is made.
+ * Steps whose retro_workspace_size exceeds 64 MiB return RETRO_ESCRATCH.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents: a call whose dims (flags aside) differ from the previous call's on
+ * the device first clears the part it uses, with a kernel on `stream`; if that
+ * stream is being captured the call returns RETRO_ESCRATCH instead (make the
+ * first call of a geometry outside the capture).  Calls that overlap on one
+ * GPU (other streams or host threads) race on the array.  After a wait that
+ * gives up (see retro_step), later calls fail until the dims change. */
+retro_status retro_step_noalloc(const retro_dims* dims, int32_t step, const void* q_window,
+                                const void* k_new, const void* v_new,
+                                const retro_kv_cache* cache, const retro_selection* sel,
+                                const retro_output_cache* ocache, float* o_out,
+                                float* lse_out, void* stream);
 
 /* ---- Projections of the multi-layer decode with re-embedding (Sec. 3.3) --------
  * Every layer projects the W+1 window rows of every sequence (rows = batch*(W+1),

@@ -15,7 +15,8 @@ from typing import Optional
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libretro_mi355x.so")
 
-RETRO_OK, RETRO_EINVAL, RETRO_EUNSUPPORTED, RETRO_EHIP, RETRO_EWORKSPACE = 0, -1, -2, -3, -4
+RETRO_OK, RETRO_EINVAL, RETRO_EUNSUPPORTED, RETRO_EHIP, RETRO_EWORKSPACE, RETRO_ESCRATCH = \
+    0, -1, -2, -3, -4, -5
 RETRO_F32, RETRO_BF16 = 0, 1
 RETRO_FLAG_SEPARATE_SCORES, RETRO_FLAG_SELECT_IN_SCORES, RETRO_FLAG_TEST_WAIT_TIMEOUT = 1, 2, 4
 
@@ -23,8 +24,8 @@ EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_worksp
             "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
             "retro_decode_attend",
             "retro_decode_attend_partials", "retro_step_attend_partials",
-            "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_pack_weight",
-            "retro_project_qkv",
+            "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_step_noalloc",
+            "retro_pack_weight", "retro_project_qkv",
             "retro_project_qkv_update", "retro_project_out")
 
 
@@ -94,6 +95,8 @@ def load_library(path: str = LIB_PATH):
         "retro_merge_output_cache": ([D, i32, P, P, C.POINTER(OutputCache), P, P, P], C.c_int),
         "retro_step": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
                         C.POINTER(OutputCache), P, P, P, C.c_size_t, P], C.c_int),
+        "retro_step_noalloc": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
+                                C.POINTER(OutputCache), P, P, P], C.c_int),
         "retro_pack_weight": ([P, i32, i32, P, P], C.c_int),
         "retro_project_qkv": ([P, i32, i32, P, i32, i32, P, P, P, P], C.c_int),
         "retro_project_out": ([P, i32, i32, P, i32, P, P, P], C.c_int),
@@ -218,6 +221,15 @@ def retro_step(dims: Dims, step: int, q_window, k_new, v_new, cache: KVCache, se
                                      C.byref(cache), C.byref(sel), C.byref(ocache), _ptr(o_out),
                                      _ptr(lse_out), _ptr(workspace), ws_bytes, _stream(stream)),
            "retro_step")
+
+
+def retro_step_noalloc(dims: Dims, step: int, q_window, k_new, v_new, cache: KVCache,
+                       sel: Selection, ocache: OutputCache, o_out, lse_out, stream=None) -> None:
+    _check(load_library().retro_step_noalloc(C.byref(dims), step, _ptr(q_window), _ptr(k_new),
+                                             _ptr(v_new), C.byref(cache), C.byref(sel),
+                                             C.byref(ocache), _ptr(o_out), _ptr(lse_out),
+                                             _stream(stream)),
+           "retro_step_noalloc")
 
 
 def retro_pack_weight(w, k: int, n: int, w_packed, stream=None) -> None:

@@ -179,6 +179,8 @@ const char* retro_status_string(int32_t status) {
     case RETRO_EUNSUPPORTED: return "RETRO_EUNSUPPORTED: shape outside the supported range";
     case RETRO_EHIP: return "RETRO_EHIP: HIP launch failed";
     case RETRO_EWORKSPACE: return "RETRO_EWORKSPACE: workspace missing or too small";
+    case RETRO_ESCRATCH:
+      return "RETRO_ESCRATCH: the step needs more than the static scratch, or its clear would be captured";
     default: return "unknown retro_status";
   }
 }

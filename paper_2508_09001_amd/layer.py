@@ -141,10 +141,17 @@ class RetroLayer:
         B.retro_merge_output_cache(self.dims, step, self.o_part, self.lse_part, self.ocache,
                                    self.o_out, self.lse_out, stream)
 
-    def step(self, step: int, q_window, k_new, v_new, stream=None) -> None:
+    def step(self, step: int, q_window, k_new, v_new, stream=None, noalloc: bool = False) -> None:
+        """One retro_step (noalloc: retro_step_noalloc, the library's static scratch in
+        place of this layer's workspace)."""
         q_window, k_new, v_new = self._dev(q_window), self._dev(k_new), self._dev(v_new)
-        B.retro_step(self.dims, step, q_window, k_new, v_new, self.cache, self.sel, self.ocache,
-                     self.o_out, self.lse_out, self.workspace, self.ws_bytes, stream)
+        if noalloc:
+            B.retro_step_noalloc(self.dims, step, q_window, k_new, v_new, self.cache, self.sel,
+                                 self.ocache, self.o_out, self.lse_out, stream)
+        else:
+            B.retro_step(self.dims, step, q_window, k_new, v_new, self.cache, self.sel,
+                         self.ocache, self.o_out, self.lse_out, self.workspace, self.ws_bytes,
+                         stream)
         for b in range(self.batch):
             self._lens[b] += 1
         self._keep = (q_window, k_new, v_new)
