@@ -15,8 +15,10 @@ replayed back to back in the timed region.
 
 Prints one JSON line with the throughput (effective HBM GB/s of the whole step,
 algorithmic bytes / time), microseconds per layer per step, the roofline of the
-dominant kernel (the step's scores + selection + page-gather attention
-kernel, timed alone with HIP events) and the CPU oracle's rate on a bounded sample.
+dominant kernel (where retro_step is one launch, that launch: the whole step;
+else its scores + selection + attention launch, timed alone with HIP events),
+the gather phase alone (the attention kernel over the step's selection, timed
+with HIP events) and the CPU oracle's rate on a bounded sample.
 """
 from __future__ import annotations
 
@@ -33,9 +35,9 @@ if ROOT not in sys.path:
 
 METRIC = "retro_step µs/layer/decode-step + effective HBM GB/s (% peak), 32K ctx B=2048 W=16"
 PEAK_HBM_GBS = 8000.0
-ATTEND_SRC = [os.path.join(ROOT, "paper_2508_09001_amd", "csrc", f)
-              for f in ("attend.hip", "roles.h", "internal.h")]
-COUNTERS = os.path.join(ROOT, "profiles", "attend_full_kernel_llama3-8b-32k_counters.json")
+STEP_SRC = [os.path.join(ROOT, "paper_2508_09001_amd", "csrc", f)
+            for f in ("step_attend.hip", "roles.h", "threshold.h", "internal.h")]
+COUNTERS = os.path.join(ROOT, "profiles", "step_attend_kernel_llama3-8b-32k_counters.json")
 
 
 def _args():
@@ -47,6 +49,8 @@ def _args():
     p.add_argument("--config", type=int, default=1, help="workload index (1 = headline)")
     p.add_argument("--window", type=int, default=None,
                    help="override the workload's window W (W = 0: no retrospection)")
+    p.add_argument("--budget", type=int, default=None,
+                   help="override the workload's token budget B")
     p.add_argument("--budget-permille", type=int, default=None,
                    help="relative budget in thousandths of the context (0: fixed budget)")
     p.add_argument("--update-kv", action="store_true",
@@ -78,12 +82,12 @@ def _sha(paths):
     return h.hexdigest()
 
 
-def _step_path(spec):
-    """The launch sequence retro_step takes for this workload on this GPU (no
-    flags: the library's own choice)."""
-    if spec.batch * spec.num_kv_heads <= 8:
-        return "two launches: scores + selection + attention, combine"
-    return "three or four launches: scores (+ selection), [selection +] attention, combine"
+def _step_path(launches):
+    """The launch sequence retro_step takes (the library's own choice, no flags)."""
+    if launches == 1:
+        return "one launch: scores, selection, attention, combine + merge"
+    return (f"{launches} launches: scores (+ selection), [selection +] attention, "
+            "combine + merge")
 
 
 def algorithmic_bytes(spec, seq_lens, num_selected):
@@ -146,6 +150,8 @@ def main():
     base_spec = W.config(args.config)
     if args.window is not None:
         base_spec = base_spec.replace(window=args.window)
+    if args.budget is not None:
+        base_spec = base_spec.replace(budget=args.budget)
     if args.budget_permille is not None:
         base_spec = base_spec.replace(budget_permille=args.budget_permille)
     need = args.warmup + 2 * args.steps
@@ -223,37 +229,53 @@ def main():
     torch.cuda.synchronize()
     ms_eager = ev0.elapsed_time(ev1)
 
-    # ---- dominant kernel: the step's scores + selection + attention launch
-    # alone, graph of L * reps launches
-    last = t1 + args.steps - 1
-    win_last = steps_in[last][0]
-    ga = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(ga):
-        for _ in range(args.attend_reps):
-            for lay in layers:
-                lay.step_attend_partials(last, win_last)
-    torch.cuda.synchronize()
-    ev0.record()
-    ga.replay()
-    ev1.record()
-    torch.cuda.synchronize()
-    n_att = args.attend_reps * L
-    us_attend = ev0.elapsed_time(ev1) * 1000.0 / n_att
+    def graph_us(fn):
+        """HIP-event time per launch of a graph of L * attend_reps launches of fn."""
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(args.attend_reps):
+                for lay in layers:
+                    fn(lay)
+        torch.cuda.synchronize()
+        ev0.record()
+        gr.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) * 1000.0 / (args.attend_reps * L)
 
+    from paper_2508_09001_amd import binding as B
+    launches = B.retro_step_launches(layers[0].dims)
     nbytes = algorithmic_bytes(spec, seq_mid, nsel)
     us_layer_step = ms_graph * 1000.0 / (args.steps * L)
     gbs = nbytes["total"] / (us_layer_step * 1e-6) / 1e9
-    # the dominant launch: digests -> scores -> selection -> gather, queries
-    kernel_bytes = (nbytes["digest"] + nbytes["gather"] + nbytes["queries"] +
-                    nbytes["select_reads"])
-    gather_gbs = kernel_bytes / (us_attend * 1e-6) / 1e9
-
+    last = t1 + args.steps - 1
+    win_last = steps_in[last][0]
+    n_att = args.attend_reps * L
     traffic = None
-    if os.path.exists(COUNTERS):
-        with open(COUNTERS) as f:
-            cnt = json.load(f)
-        if cnt.get("source_sha256") == _sha(ATTEND_SRC):
-            traffic = cnt.get("hbm_bytes_per_launch")
+    if launches == 1:
+        # the dominant kernel is the step itself: its launches in the timed
+        # graphs (one per layer-step), every algorithmic byte of the step
+        kernel, us_kernel, kernel_bytes, n_kernel = ("step_attend_kernel", us_layer_step,
+                                                     nbytes["total"], args.steps * L)
+        if os.path.exists(COUNTERS):
+            with open(COUNTERS) as f:
+                cnt = json.load(f)
+            if cnt.get("source_sha256") == _sha(STEP_SRC):
+                traffic = cnt.get("hbm_bytes_per_launch")
+    else:
+        # the step's scores + selection + attention launch alone: digests ->
+        # scores -> selection -> gather, queries
+        kernel = "scores + selection + attention launch"
+        us_kernel = graph_us(lambda lay: lay.step_attend_partials(last, win_last))
+        kernel_bytes = (nbytes["digest"] + nbytes["gather"] + nbytes["queries"] +
+                        nbytes["select_reads"])
+        n_kernel = n_att
+    kernel_gbs = kernel_bytes / (us_kernel * 1e-6) / 1e9
+    # the gather phase alone: the attention kernel over the step's selection
+    # (the pages' keys and values, the window's queries, the selection rows)
+    us_gather = graph_us(lambda lay: lay.attend_partials(last, win_last))
+    gather_bytes = nbytes["gather"] + nbytes["queries"] + nbytes["mask"]
+    gather_gbs = gather_bytes / (us_gather * 1e-6) / 1e9
 
     result = {
         "metric": METRIC,
@@ -275,16 +297,20 @@ def main():
                    "window": spec.window, "update_kv": bool(upd is not None),
                    "layers_rotated": L,
                    "launch": "hip-graph per step",
-                   "step_path": _step_path(spec)},
+                   "step_path": _step_path(launches)},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
         "bytes_per_layer_step": nbytes,
-        "roofline": {"bound": "hbm", "kernel": "attend_full_kernel",
-                     "achieved": round(gather_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gather_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "bytes_per_launch": kernel_bytes, "us_per_launch": round(us_attend, 3),
-                     "launches": n_att},
+        "roofline": {"bound": "hbm", "kernel": kernel,
+                     "achieved": round(kernel_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(kernel_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                     "bytes_per_launch": kernel_bytes, "us_per_launch": round(us_kernel, 3),
+                     "launches": n_kernel},
+        "gather_phase": {"kernel": "attend_kernel (retro_decode_attend_partials)",
+                         "bytes_per_launch": gather_bytes, "us_per_launch": round(us_gather, 3),
+                         "achieved": round(gather_gbs, 1), "unit": "GB/s",
+                         "frac": round(gather_gbs / PEAK_HBM_GBS, 4), "launches": n_att},
     }
 
     if args.cpu_seconds > 0:
@@ -423,11 +449,13 @@ def cpu_baseline(spec, pre, budget_s):
         orc.prefill(b, k, v)
     qw = W.QueryWindow(spec)
     t = 0
-    for t in range(spec.window):
+    # the window's ramp-up, leaving at least a few steps to time
+    ramp = min(spec.window, spec.steps - 4)
+    for t in range(ramp):
         k_new, v_new, q = gen.step(t)
         orc.step(t, k_new, v_new, qw.push(q).copy())
     n, spent, last = 0, 0.0, None
-    while spent < budget_s and t + 1 < spec.steps:
+    while (spent < budget_s or n == 0) and t + 1 < spec.steps:
         t += 1
         k_new, v_new, q = gen.step(t)
         win = qw.push(q).copy()
@@ -441,8 +469,8 @@ def cpu_baseline(spec, pre, budget_s):
             "us_per_layer_step": round(us, 1), "cores": oracle.num_threads(), "kind": "oracle",
             "cpu_model": _cpu_model(), "nproc": len(os.sched_getaffinity(0)),
             "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
-            "sample": f"{n} decode steps of one layer of {spec.name} with a full window "
-                      f"(steps {spec.window + 1}..{t}), fp64 attention, OpenMP"}
+            "sample": f"{n} decode steps of one layer of {spec.name} after {ramp} untimed "
+                      f"steps (steps {ramp + 1}..{t}), fp64 attention, OpenMP"}
 
 
 if __name__ == "__main__":

@@ -305,6 +305,11 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
                         float* o_out, float* lse_out, void* workspace, size_t ws_bytes,
                         void* stream);
 
+/* The number of kernel launches retro_step makes for these dims on the current
+ * device (1: scores, selection, attention and merge in one launch; 3 or 4:
+ * see retro_step), in *launches.  Host only: nothing is enqueued. */
+retro_status retro_step_launches(const retro_dims* dims, int32_t* launches);
+
 /* retro_step for callers that cannot allocate (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation): the same step and
  * results, with the workspace in a static device array of the library (64 MiB

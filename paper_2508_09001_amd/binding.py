@@ -22,10 +22,9 @@ RETRO_FLAG_SEPARATE_SCORES, RETRO_FLAG_SELECT_IN_SCORES, RETRO_FLAG_TEST_WAIT_TI
 
 EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_workspace_size",
             "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
-            "retro_decode_attend",
-            "retro_decode_attend_partials", "retro_step_attend_partials",
+            "retro_decode_attend", "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_step_noalloc",
-            "retro_pack_weight", "retro_project_qkv",
+            "retro_step_launches", "retro_pack_weight", "retro_project_qkv",
             "retro_project_qkv_update", "retro_project_out")
 
 
@@ -97,6 +96,7 @@ def load_library(path: str = LIB_PATH):
                         C.POINTER(OutputCache), P, P, P, C.c_size_t, P], C.c_int),
         "retro_step_noalloc": ([D, i32, P, P, P, C.POINTER(KVCache), C.POINTER(Selection),
                                 C.POINTER(OutputCache), P, P, P], C.c_int),
+        "retro_step_launches": ([D, C.POINTER(C.c_int32)], C.c_int),
         "retro_pack_weight": ([P, i32, i32, P, P], C.c_int),
         "retro_project_qkv": ([P, i32, i32, P, i32, i32, P, P, P, P], C.c_int),
         "retro_project_out": ([P, i32, i32, P, i32, P, P, P], C.c_int),
@@ -221,6 +221,13 @@ def retro_step(dims: Dims, step: int, q_window, k_new, v_new, cache: KVCache, se
                                      C.byref(cache), C.byref(sel), C.byref(ocache), _ptr(o_out),
                                      _ptr(lse_out), _ptr(workspace), ws_bytes, _stream(stream)),
            "retro_step")
+
+
+def retro_step_launches(dims: Dims) -> int:
+    """Kernel launches retro_step makes for dims on the current device."""
+    n = C.c_int32(0)
+    _check(load_library().retro_step_launches(C.byref(dims), C.byref(n)), "retro_step_launches")
+    return n.value
 
 
 def retro_step_noalloc(dims: Dims, step: int, q_window, k_new, v_new, cache: KVCache,

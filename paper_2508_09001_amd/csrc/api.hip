@@ -334,6 +334,23 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
                                               (char*)workspace + g.ws_dummy, (hipStream_t)stream));
 }
 
+retro_status retro_step_launches(const retro_dims* dims, int32_t* launches) {
+  Geometry g;
+  if (!launches) return RETRO_EINVAL;
+  retro_status st = retro::make_geometry(dims, &g);
+  if (st != RETRO_OK) return st;
+  Geometry gp = g;
+  gp.token_pending = 1;
+  if (one_launch(gp)) {
+    *launches = 1;
+  } else if (retro::attend_selects(gp) && !(g.flags & RETRO_FLAG_SELECT_IN_SCORES)) {
+    *launches = 3;
+  } else {
+    *launches = retro::score_selects(gp) ? 3 : 4;
+  }
+  return RETRO_OK;
+}
+
 retro_status retro_copy_scores(const retro_dims* dims, const void* workspace, size_t ws_bytes,
                                float* scores, void* stream) {
   Geometry g;
