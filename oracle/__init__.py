@@ -104,8 +104,14 @@ class Oracle:
 
     def __init__(self, batch: int, num_kv_heads: int, group: int, head_dim: int,
                  page_size: int, budget: int, window: int, max_tokens: int,
-                 sm_scale: Optional[float] = None, budget_permille: int = 0):
+                 sm_scale: Optional[float] = None, budget_permille: int = 0,
+                 reuse_interval: int = 0):
         self.lib = _load()
+        # top-k reuse (the selection-reuse baseline of the motivational study,
+        # Table 4): the page selection is refreshed on steps t with t mod f == 0
+        # and kept, unscored, on the others; 0 or 1: every step
+        self.reuse_interval = reuse_interval
+        self._kept = None
         if sm_scale is None:
             sm_scale = float(np.float32(1.0 / np.sqrt(head_dim)))
         self.dims = _Dims(batch, num_kv_heads, group, head_dim, page_size, budget, window,
@@ -131,7 +137,7 @@ class Oracle:
         kw = dict(batch=spec.batch, num_kv_heads=spec.num_kv_heads, group=spec.group,
                   head_dim=spec.head_dim, page_size=spec.page_size, budget=spec.budget,
                   window=spec.window, max_tokens=spec.max_tokens, sm_scale=sm_scale,
-                  budget_permille=spec.budget_permille)
+                  budget_permille=spec.budget_permille, reuse_interval=spec.reuse_interval)
         kw.update(over)
         return cls(**kw)
 
@@ -175,6 +181,12 @@ class Oracle:
         self.lib.oracle_select(self._d, _p(scores), _p(self.seq_lens), _p(sel), _p(num))
         return sel, num
 
+    def refreshes(self, step: int) -> bool:
+        """Whether PageSelect runs at this step (always, unless top-k reuse keeps the
+        selection of the last refresh step: steps t with t mod f != 0)."""
+        f = self.reuse_interval
+        return f < 2 or step % f == 0 or self._kept is None
+
     def build_mask(self, step: int, sel: np.ndarray, num: np.ndarray) -> np.ndarray:
         M = np.zeros_like(sel)
         self.lib.oracle_build_mask(self._d, step, _p(sel), _p(num), _p(self.A), _p(M))
@@ -209,8 +221,15 @@ class Oracle:
             k_new, v_new = k_new[None], v_new[None]
         for j in range(k_new.shape[0]):
             self.append(t, k_new[j], v_new[j])
-        scores = self.score(q_window[:, -1])
-        sel, num = self.select(scores)
+        if self.refreshes(t):
+            scores = self.score(q_window[:, -1])
+            sel, num = self.select(scores)
+            self._kept = (sel.copy(), num.copy())
+        else:
+            # top-k reuse: the pages of the last refresh step, as they were selected;
+            # Alg. 2's mask and last_loaded update apply to them unchanged
+            scores = None
+            sel, num = self._kept[0].copy(), self._kept[1].copy()
         M = self.build_mask(t, sel, num)
         out = dict(scores=scores, selected=sel, num_selected=num, mask=M,
                    seq_lens=self.seq_lens.copy())

@@ -412,3 +412,63 @@ def test_window_zero_is_plain_quest_sparse_attention():
                                       o.dims.sm_scale)
                 np.testing.assert_allclose(out["o_out"][b, 0, qh], O, atol=1e-10)
                 assert abs(out["lse_out"][b, 0, qh] - Z) < 1e-10
+
+
+# ----------------------------------------------------------------------------- top-k reuse
+def test_topk_reuse_golden_walk():
+    """The selection-reuse baseline (Table 4, f = 2) on a hand-worked walk: refresh
+    steps select as PageSelect does, reuse steps keep the last refresh's pages
+    whatever the scores say, and Alg. 2's mask runs on the pages in use."""
+    gold = _load("topk_reuse_walk.json")
+    P = gold["page_size"]
+    keys = np.array(gold["prefill_keys"], np.float32).reshape(-1, 1, 2)
+    n_steps = len(gold["steps"])
+    for f in (gold["reuse_interval"], 1):
+        o = oracle.Oracle(batch=1, num_kv_heads=1, group=1, head_dim=2, page_size=P,
+                          budget=gold["budget_pages"] * P, window=gold["window"],
+                          max_tokens=len(keys) + n_steps, reuse_interval=f)
+        o.prefill(0, keys, np.zeros_like(keys))
+        for st in gold["steps"]:
+            t = st["t"]
+            win = np.zeros((1, 2, 1, 2), np.float32)
+            win[0, 1, 0] = st["q"]
+            tok = np.zeros((1, 1, 2), np.float32)
+            out = o.step(t, tok, tok, win, attend=False)
+            want = st["selected"] if f == gold["reuse_interval"] else st["fresh_selected"]
+            k = int(out["num_selected"][0, 0])
+            assert list(out["selected"][0, 0, :k]) == want, (f, t)
+            assert (out["scores"] is None) == (f == 2 and t % 2 == 1), (f, t)
+            if f == gold["reuse_interval"]:
+                assert list(out["mask"][0, 0, :k]) == st["mask"], (f, t)
+        if f == gold["reuse_interval"]:
+            assert list(o.A[0, 0, :len(gold["last_loaded_after"])]) == gold["last_loaded_after"]
+
+
+@pytest.mark.parametrize("f", [2, 3])
+def test_topk_reuse_steps_keep_the_pages_and_add_no_past_context(f):
+    """On a reuse step the pages are the last refresh's, every one of them was
+    loaded at the step before (mask t - 1), so no past query of the window gains
+    a page (eq. update-sup adds nothing), and its merged output is the cached one."""
+    spec = _tiny_spec(reuse_interval=f, steps=24)
+    _, o, outs = _run(spec)
+    for t, out in enumerate(outs):
+        if t % f == 0:
+            assert out["scores"] is not None
+            last = t
+            continue
+        assert out["scores"] is None
+        assert np.array_equal(out["selected"], outs[last]["selected"]), t
+        assert np.array_equal(out["num_selected"], outs[last]["num_selected"]), t
+        for b in range(spec.batch):
+            for h in range(spec.num_kv_heads):
+                k = out["num_selected"][b, h]
+                assert np.all(out["mask"][b, h, :k] == t - 1), (t, b, h)
+        # rows of past queries (not the one leaving, whose result is final) keep
+        # their previous merged output: nothing supplementary reached them
+        for r in range(1, spec.window):
+            tau = t - spec.window + r
+            if tau < 0:
+                continue
+            prev = outs[t - 1]
+            assert np.allclose(out["o_out"][:, r], prev["o_out"][:, r + 1], rtol=0, atol=0), (t, r)
+            assert np.array_equal(out["lse_out"][:, r], prev["lse_out"][:, r + 1]), (t, r)

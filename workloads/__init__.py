@@ -62,6 +62,7 @@ class Spec:
     drift_step: float = 0.0
     seed: int = 0
     budget_permille: int = 0  # relative budget: max(B, len * permille / 1000) tokens per step
+    reuse_interval: int = 0   # top-k reuse: selection refreshed on steps t % f == 0 (0, 1: every step)
 
     @property
     def num_q_heads(self) -> int:
