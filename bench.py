@@ -51,6 +51,8 @@ def _args():
                    help="override the workload's window W (W = 0: no retrospection)")
     p.add_argument("--budget", type=int, default=None,
                    help="override the workload's token budget B")
+    p.add_argument("--reuse-interval", type=int, default=None,
+                   help="top-k selection reuse: refresh the selection every f steps (f >= 2)")
     p.add_argument("--budget-permille", type=int, default=None,
                    help="relative budget in thousandths of the context (0: fixed budget)")
     p.add_argument("--update-kv", action="store_true",
@@ -154,6 +156,8 @@ def main():
         base_spec = base_spec.replace(budget=args.budget)
     if args.budget_permille is not None:
         base_spec = base_spec.replace(budget_permille=args.budget_permille)
+    if args.reuse_interval is not None:
+        base_spec = base_spec.replace(reuse_interval=args.reuse_interval)
     need = args.warmup + 2 * args.steps
     spec = base_spec if need <= base_spec.steps else base_spec.replace(steps=need)
     L = args.layers
@@ -295,6 +299,7 @@ def main():
                    "context": int(spec.prefill[0]), "page_size": spec.page_size,
                    "budget_tokens": spec.budget, "budget_permille": spec.budget_permille,
                    "window": spec.window, "update_kv": bool(upd is not None),
+                   "reuse_interval": spec.reuse_interval,
                    "layers_rotated": L,
                    "launch": "hip-graph per step",
                    "step_path": _step_path(launches)},

@@ -97,6 +97,13 @@ typedef struct retro_dims {
                               token included); 0: B_t = B.  k_max covers the largest
                               B_t of a full page-table row.                          */
   int32_t flags;           /* retro_flag bits; 0 for normal use                        */
+  int32_t reuse_interval;  /* top-k selection reuse, the baseline of the paper's
+                              motivational study (Appendix, Table 4) as an alternative
+                              PageSelect: with f = reuse_interval >= 2, steps t with
+                              t mod f != 0 keep the selection (rows and counts) that
+                              `sel` holds from the previous step, unscored, and run
+                              UpdateAndBuildMask (Alg. 2) on it; steps with t mod f
+                              == 0 select as usual.  0 or 1: every step selects.    */
 } retro_dims;
 
 /* The paged KV cache of one layer (Sec. 2.1; pages as in a vLLM-style pool).
@@ -214,6 +221,9 @@ retro_status retro_update_kv(const retro_dims* dims, const retro_kv_cache* cache
  *   order: mask = last_loaded[p]; last_loaded[p] = step.
  * Page selection is exact: it depends on no floating-point reduction order other
  * than the one stated. */
+/* (With dims->reuse_interval = f >= 2 and step mod f != 0 no score is computed:
+ * the rows and counts `sel` holds are kept, and only the mask / last_loaded
+ * loop above runs on them; q_cur is not read.) */
 retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void* q_cur,
                                 const retro_kv_cache* cache, const retro_selection* sel,
                                 void* workspace, size_t ws_bytes, void* stream);

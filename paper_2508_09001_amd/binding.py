@@ -39,7 +39,7 @@ class Dims(C.Structure):
                 ("head_dim", C.c_int32), ("page_size", C.c_int32), ("budget_tokens", C.c_int32),
                 ("window", C.c_int32), ("max_pages", C.c_int32), ("num_phys_pages", C.c_int32),
                 ("dtype", C.c_int32), ("sm_scale", C.c_float), ("budget_permille", C.c_int32),
-                ("flags", C.c_int32)]
+                ("flags", C.c_int32), ("reuse_interval", C.c_int32)]
 
 
 class KVCache(C.Structure):

@@ -85,6 +85,8 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
                      kMaxWaves);
   if ((int64_t)x.hk * x.n_rgroups > 65535) return RETRO_EUNSUPPORTED;
   x.flags = d->flags;
+  if (d->reuse_interval < 0) return RETRO_EINVAL;
+  x.reuse = d->reuse_interval;
 
   const size_t bhs = (size_t)bh;
   // per workgroup of the one-launch step: launch count, geometry fingerprint
@@ -264,6 +266,8 @@ retro_status retro_select_pages(const retro_dims* dims, int32_t step, const void
   if (!q_cur || !cache_ok(cache) || !sel_ok(sel)) return RETRO_EINVAL;
   if ((st = check_ws(g, workspace, ws_bytes)) != RETRO_OK) return st;
   hipStream_t s = (hipStream_t)stream;
+  if (retro::reuse_step(g, step))  // top-k reuse: Alg. 2 on the rows sel holds
+    return from_hip(retro::launch_reuse_mask(g, step, *cache, *sel, s));
   float* scores = ws_at(workspace, g.ws_scores);
   int32_t* counters = reinterpret_cast<int32_t*>((char*)workspace + g.ws_sel);
   hipError_t e = retro::launch_score(g, step, q_cur, (int64_t)g.hq * g.D, *cache, nullptr, nullptr,
@@ -402,6 +406,18 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
   int32_t* tok = reinterpret_cast<int32_t*>((char*)workspace + g.ws_tok);
   int32_t* err = reinterpret_cast<int32_t*>((char*)workspace + g.ws_err);
   const void* dummy = (char*)workspace + g.ws_dummy;
+  if (retro::reuse_step(g, step)) {
+    // top-k reuse: the token's append (with Alg. 2's current-page rule and the
+    // seq_lens advance), Alg. 2 on the kept selection, attention, combine + merge
+    hipError_t e = retro::launch_append(g, step, *cache, k_new, v_new, s);
+    if (e == hipSuccess) e = retro::launch_reuse_mask(g, step, *cache, *sel, s);
+    if (e == hipSuccess)
+      e = retro::launch_attend(g, step, q_window, *cache, *sel, nullptr, o_ws, l_ws, dummy, s);
+    if (e == hipSuccess)
+      e = retro::launch_combine_merge(g, step, 2, o_ws, l_ws, sel->num_selected, nullptr,
+                                      nullptr, nullptr, nullptr, ocache, o_out, lse_out, cache, s);
+    return from_hip(e);
+  }
   // the launches of this step append the token in their first launch and use
   // the length with it; the combine + merge launch advances seq_lens
   Geometry gp = g;

@@ -52,6 +52,7 @@ struct Geometry {
   int rtw;            // row tiles per wave
   int waves;          // waves per attention workgroup
   int flags;          // retro_dims.flags (RETRO_FLAG_*)
+  int reuse;          // retro_dims.reuse_interval (top-k reuse; < 2: every step selects)
   // workspace layout (bytes): page scores, physical ids of the selection,
   // split partials, the sticky error word, the score launch's counters, the
   // step token's page per head, the one-launch step's tagged score words and
@@ -96,6 +97,11 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
                         const retro_kv_cache& c, const void* k_new, const void* v_new,
                         float* scores, const retro_selection* sel, int32_t* sel_phys,
                         int32_t* counters, hipStream_t s);
+// Top-k reuse steps: UpdateAndBuildMask (Alg. 2) on the rows `sel` holds (mask
+// values from last_loaded, then last_loaded = step for the kept pages).
+bool reuse_step(const Geometry& g, int step);
+hipError_t launch_reuse_mask(const Geometry& g, int step, const retro_kv_cache& c,
+                             const retro_selection& sel, hipStream_t s);
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
                             const retro_kv_cache& c, const retro_selection& sel,
                             int32_t* sel_phys, hipStream_t s);

@@ -46,7 +46,40 @@ __global__ void __launch_bounds__(THREADS) topk_mask_kernel(TopkArgs ta,
       tok_lp, hist, small, [] {});
 }
 
+// Alg. 2 on the kept selection of a top-k reuse step: one wavefront per
+// (sequence, KV head); every mask value is read before any last_loaded entry
+// of the head changes (the rows hold distinct pages).
+__global__ void __launch_bounds__(64) reuse_mask_kernel(Geometry g, int step,
+                                                        const int32_t* __restrict__ sel,
+                                                        int32_t* __restrict__ msk,
+                                                        const int32_t* __restrict__ nsel,
+                                                        int32_t* __restrict__ A) {
+  const int bh = blockIdx.x;
+  const int k = min(max(nsel[bh], 0), g.k_max);
+  const int32_t* row = sel + (int64_t)bh * g.k_max;
+  int32_t* m = msk + (int64_t)bh * g.k_max;
+  int32_t* a = A + (int64_t)bh * g.max_pages;
+  for (int i = threadIdx.x; i < g.k_max; i += 64) {
+    const int p = i < k ? row[i] : -1;
+    m[i] = (p >= 0 && p < g.max_pages) ? a[p] : -1;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < k; i += 64) {
+    const int p = row[i];
+    if (p >= 0 && p < g.max_pages) a[p] = step;
+  }
+}
+
 }  // namespace
+
+bool reuse_step(const Geometry& g, int step) { return g.reuse >= 2 && step % g.reuse != 0; }
+
+hipError_t launch_reuse_mask(const Geometry& g, int step, const retro_kv_cache& c,
+                             const retro_selection& sel, hipStream_t s) {
+  reuse_mask_kernel<<<(unsigned)(g.batch * g.hk), 64, 0, s>>>(g, step, sel.selected, sel.mask,
+                                                             sel.num_selected, c.last_loaded);
+  return hipGetLastError();
+}
 
 hipError_t launch_topk_mask(const Geometry& g, int step, const float* scores,
                             const retro_kv_cache& c, const retro_selection& sel,

@@ -25,13 +25,14 @@ class RetroLayer:
                  budget: int, window: int, max_pages: int, dtype: str = "bf16",
                  num_phys_pages: Optional[int] = None, page_table: Optional[torch.Tensor] = None,
                  sm_scale: float = 0.0, budget_permille: int = 0, flags: int = 0,
+                 reuse_interval: int = 0,
                  device: str = "cuda"):
         self.device = torch.device(device)
         if num_phys_pages is None:
             num_phys_pages = batch * max_pages
         self.dims = B.Dims(batch, num_kv_heads, group, head_dim, page_size, budget, window,
                            max_pages, num_phys_pages, _RETRO_DTYPE[dtype], sm_scale,
-                           budget_permille, flags)
+                           budget_permille, flags, reuse_interval)
         self.k_max = B.retro_k_max(self.dims)
         self.ws_bytes = B.retro_workspace_size(self.dims)
         self.batch, self.hk, self.G, self.d = batch, num_kv_heads, group, head_dim
@@ -74,7 +75,8 @@ class RetroLayer:
         args = dict(batch=spec.batch, num_kv_heads=spec.num_kv_heads, group=spec.group,
                     head_dim=spec.head_dim, page_size=spec.page_size, budget=spec.budget,
                     window=spec.window, max_pages=spec.max_pages, dtype=spec.dtype,
-                    budget_permille=spec.budget_permille)
+                    budget_permille=spec.budget_permille,
+                    reuse_interval=getattr(spec, "reuse_interval", 0))
         args.update(kw)
         return cls(**args)
 

@@ -272,3 +272,22 @@ def test_update_kv_short_sequences_and_partial_pages():
     spec = W.Spec("edge-short", batch=3, num_kv_heads=2, group=3, head_dim=64, page_size=16,
                   budget=64, window=5, steps=20, dtype="bf16", prefill=(1, 17, 40), seed=9)
     run_parity(spec, 20, page_perm_seed=3, update_kv=True, label="edge short + UpdateKV")
+
+
+@pytest.mark.parametrize("f", [2, 3])
+def test_topk_reuse_tiny_fp32(f):
+    """The selection-reuse baseline (top-k refreshed every f steps): selection,
+    mask, last_loaded and seq_lens bit for bit, outputs within tolerance, on every
+    step of the tiny workload, through retro_step and through the separate calls."""
+    spec = W.config(0).replace(reuse_interval=f)
+    run_parity(spec, spec.steps, label=f"tiny fp32, top-k reuse f={f}")
+    run_parity(spec, 12, split_calls=True, page_perm_seed=3,
+               label=f"tiny fp32, top-k reuse f={f}, separate calls")
+
+
+def test_topk_reuse_llama_layer_32k():
+    """Top-k reuse with f = 2 at the 32K layer: refresh steps take the one-launch
+    step, reuse steps the append + mask + attention + merge launches."""
+    spec = W.config(1).replace(reuse_interval=2)
+    run_parity(spec, spec.window + 9, page_perm_seed=8, label="32k, top-k reuse f=2")
+
