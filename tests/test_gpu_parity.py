@@ -46,15 +46,22 @@ def test_llama_layer_32k_split_calls_shuffled():
     run_parity(spec, 20, split_calls=True, page_perm_seed=1, label="32k split+shuffled")
 
 
+@pytest.mark.timeout(900)
 def test_batched_serving_ragged():
+    """All 128 steps of the batch-16 workload (ragged 8K-32K contexts, shuffled
+    page table): selection, mask, last_loaded, seq_lens and page scores bit for
+    bit, every output row against the oracle's."""
     spec = W.config(2)
-    run_parity(spec, 12, page_perm_seed=2, label="batch16 ragged shuffled")
+    run_parity(spec, spec.steps, page_perm_seed=2, label="batch16 ragged shuffled, all steps")
 
 
+@pytest.mark.timeout(900)
 def test_long_generation_multi_token_steps():
-    # 8 tokens appended per step (16384 -> 49152 over 4096 steps); batch 2 of 4
-    spec = W.config(3).replace(batch=2, prefill=(16384, 16384))
-    run_parity(spec, 40, label="long-generation b2 8 tok/step")
+    """The long-generation workload at its full batch of 4, 8 tokens appended per
+    step (16384 -> 16896 tokens over these 64 steps), every output row against the
+    oracle's."""
+    spec = W.config(3)
+    run_parity(spec, 64, label="long-generation b4 8 tok/step, 64 steps")
 
 
 @pytest.mark.parametrize("budget,window", [(1024, 0), (2048, 4), (4096, 16), (8192, 64)])
