@@ -291,24 +291,28 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
 /* One whole step: retro_append_kv(k_new, v_new), retro_select_pages(row W of
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
  * semantics, without materialising o_part / lse_part.
- * Two launches where every workgroup of the first fits on the GPU at once (as
- * the occupancy of its kernel times the compute units tells; up to 2560 pages
- * per sequence, rtw 1): page scores (with the append), selection and attention,
- * the workgroups of a KV head exchanging their scores through tagged words in
- * `workspace`; then combine + merge (with the last_loaded update and the
- * seq_lens advance).  The exchange needs every workgroup of the first launch
- * resident at once: work of other streams or processes holding compute units
- * delays it until they free them; a wait that runs past its bound (tens of
- * milliseconds) sets the sticky error word in `workspace`: the outputs of that
- * step and of every later step with this workspace are then NaN, and the
- * output cache, last_loaded and seq_lens are left as they were, until the
- * workspace is zero-filled again (RETRO_FLAG_TEST_WAIT_TIMEOUT in dims->flags
- * makes every such wait give up at once, for tests of that path).
- * Otherwise, or with RETRO_FLAG_SEPARATE_SCORES, the scores take a launch of
- * their own first and every attention workgroup selects in front of its
- * attention; with RETRO_FLAG_SELECT_IN_SCORES, or for max_pages > 6144, the
- * selection runs at the end of the score launch (or in a launch of its own)
- * instead. */
+ * One launch where every workgroup of it fits on the GPU at once (as the
+ * occupancy of its kernel times the compute units tells; up to 2240 pages per
+ * sequence, at most 64 KV heads per launch, at most 1024 workgroups, rtw 1):
+ * page scores (with the append), selection, attention, combine + merge, the
+ * last_loaded update and the seq_lens advance, the workgroups of a KV head
+ * handing each other scores and partial results through tagged words in
+ * `workspace` (each word carries the launch's epoch; no counters, no fences).
+ * That needs every workgroup resident at once: work of other streams or
+ * processes holding compute units delays it until they free them; a wait that
+ * runs past its bound (tens of milliseconds) sets the sticky error word in
+ * `workspace`: the outputs of that step and of every later step with this
+ * workspace are then NaN, and the output cache, last_loaded and seq_lens are
+ * left as they were, until the workspace is zero-filled again
+ * (RETRO_FLAG_TEST_WAIT_TIMEOUT in dims->flags makes every such wait give up
+ * at once, for tests of that path).
+ * Otherwise, or with RETRO_FLAG_SEPARATE_SCORES, three launches: the scores
+ * (with the append), then attention with every attention workgroup selecting
+ * in front of it, then combine + merge; with RETRO_FLAG_SELECT_IN_SCORES, or
+ * for max_pages > 6144, the selection runs at the end of the score launch (or
+ * in a launch of its own) instead.  Steps that keep an earlier selection (top-k
+ * reuse, retro_dims.reuse_interval) run the append, Alg. 2 on the kept rows,
+ * attention and combine + merge as four launches. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,
@@ -316,8 +320,9 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
                         void* stream);
 
 /* The number of kernel launches retro_step makes for these dims on the current
- * device (1: scores, selection, attention and merge in one launch; 3 or 4:
- * see retro_step), in *launches.  Host only: nothing is enqueued. */
+ * device in a step that selects (1: scores, selection, attention and merge in
+ * one launch; 3 or 4: see retro_step; a top-k reuse step always makes 4), in
+ * *launches.  Host only: nothing is enqueued. */
 retro_status retro_step_launches(const retro_dims* dims, int32_t* launches);
 
 /* retro_step for callers that cannot allocate (code under HIP graph capture,

@@ -127,11 +127,11 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
 // with the output cache; the head's first workgroup applies the last_loaded
 // update, and the sequence's first advances seq_lens (with g.token_pending).
 // Only when every workgroup is resident at once (step_attend_supported:
-// occupancy times compute units; rtw == 1, max_pages <= 2560, at most 96 pages
-// scored per workgroup, at most 64 workgroups per head and 64 KV heads).  Uses
-// the workspace's tagged words and per-workgroup counter lines (zero-filled
-// once, then only grown; refused with the error word set if last used with
-// another geometry); err: set if a wait ran past spin_limit polls (tag_bias != 0
+// occupancy times compute units; rtw == 1, max_pages <= 2240, at most 96 pages
+// scored per workgroup, at most 64 workgroups per head and 64 KV heads, at most
+// kCtlLines workgroups).  Uses the workspace's tagged words and per-workgroup
+// control lines (zero-filled once, then holding the last launch's epoch;
+// refused with the error word set if last used with another geometry); err: set if a wait ran past spin_limit polls (tag_bias != 0
 // makes every wait give up, for tests).  Without o_out, only the partials are
 // written (o_ws, l_ws), with the selection, and last_loaded is left as it is.
 bool step_attend_supported(const Geometry& g);

@@ -1,7 +1,7 @@
-// Page scores, page selection and the attention of one decode step in a single
-// launch, for shapes whose workgroups all fit on the GPU at once (the Llama-class
-// single-sequence layers): Alg. 1's PageSelect and attention, Alg. 2's mask
-// values, eq. (quest_score), eq. (update-org) and eq. (update-sup).
+// A whole decode step in a single launch, for shapes whose workgroups all fit
+// on the GPU at once (the Llama-class layers): Alg. 1's AppendKV, PageSelect,
+// attention, MergeOutput and CacheOutput, Alg. 2, eq. (quest_score),
+// eq. (update-org), eq. (update-sup) and eq. (merged_attn_general).
 //
 // Each KV head (sequence b, head h) gets NW workgroups; workgroup j of the head
 //   1. scores the head's pages [j * ppb, (j + 1) * ppb), appending the step's
@@ -15,18 +15,33 @@
 //      barrier across workgroups);
 //   4. computes the head's selection by threshold (threshold.h) and writes the
 //      page list of its split of the kept pages into LDS; the head's writer
-//      workgroup also writes the selection rows, mask values and count;
+//      workgroup (j = 0) also keeps the whole selection there;
 //   5. runs the attention of its split (attend_role) and writes the split's
-//      partial (O, LSE) per window row, combined by the merge launch.
+//      partial output rows device-coherently; once a wavefront's rows are
+//      written through, it publishes their log-normalisers as tagged words;
+//   6. the head's writer workgroup stores the selection rows, mask values,
+//      count and Alg. 2's last_loaded update (after every workgroup of the
+//      head has read last_loaded: their score words say so) and a tagged
+//      head word (selection done);
+//   7. combine + merge units, spread over the head's workgroups, wait for the
+//      log-normaliser words of their rows in every split, then read the
+//      partial rows and merge them into the output cache (merge_unit);
+//   8. one wavefront per sequence advances seq_lens once every head of the
+//      sequence has published its head word (every reader of seq_lens in
+//      the launch has then read it).
 //
 // Epoch.  Every workgroup has a line of its own in the workspace holding the
-// number of launches it has run (and a fingerprint of the geometry); it reads
-// the line at its start and its publisher wavefront stores the count + 1.  All
-// workgroups of a launch run once per launch, so the counts agree, and the
-// epoch (count + 1) is the same in every workgroup of the launch and larger
-// than every tag an earlier launch wrote.  A workspace last used with another
-// geometry is refused by the fingerprint: the sticky error word is set and no
-// wait is entered.
+// epoch of the last launch it ran (and a fingerprint of the geometry); it reads
+// the line at its start and its publisher wavefront stores the next epoch.  All
+// workgroups of a launch run once per launch, so the lines agree, and the
+// epoch is the same in every workgroup of the launch.  Epochs count 1, 2, ...,
+// 2^31 - 1, then 1 again: 31 bits, because the log-normaliser and head words
+// keep their top bit for a failure flag, and never 0, the tag of a word no
+// launch has written.  A word written by an earlier launch carries another
+// epoch unless exactly a multiple of 2^31 - 1 launches on this workspace have
+// passed without rewriting it.  A workspace last used with another geometry is
+// refused by the fingerprint: the sticky error word is set and no wait is
+// entered.
 //
 // Coherence (without fences, which would write back or invalidate whole L2s):
 //   - a score word is written with one device-coherent (sc1) 64-bit store and
@@ -42,17 +57,29 @@
 //   - the gather uses plain loads of lines that no workgroup of this launch
 //     writes, apart from the token's bytes (replaced as above); no L2 holds a
 //     line from before the launch (the launch's acquire at its start), so no
-//     stale copy can be hit.
+//     stale copy can be hit;
+//   - the partial output rows go out as device-coherent 16-byte stores; each
+//     wavefront waits until they are acknowledged (s_waitcnt 0) before it
+//     stores its tagged log-normaliser words, and the combine reads the rows
+//     with device-coherent loads only after it has seen those tags;
+//   - the writer's plain stores (selection rows, mask, count, last_loaded) and
+//     the seq_lens advance are read by later launches only, except
+//     last_loaded and seq_lens, which every workgroup reads at its start: the
+//     writer stores last_loaded only after seeing every score word of its head
+//     (each issued after the issuing workgroup's loads had returned), and
+//     seq_lens advances only after every head word of the sequence;
+//   - each output-cache slot is read and written by one merge unit only.
 //
 // Waits are bounded: past spin_limit polls the sticky error word is set and the
-// workgroup goes on with what it has; the merge launch then writes NaN outputs
-// and leaves the output cache, last_loaded and seq_lens as they were.
+// workgroup goes on with what it has; the combine then writes NaN outputs and
+// leaves the output cache, last_loaded and seq_lens as they were.
 #include "threshold.h"
 
 namespace retro {
 namespace {
 
 constexpr int kThreads = 512;
+constexpr uint64_t kEpochs = 0x7FFFFFFFull;  // epochs 1 .. 2^31 - 1
 constexpr int kWaves = kThreads / 64;
 
 struct StepAttendArgs {
@@ -121,7 +148,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   const int gsize = GC > 0 ? GC : g.G;
   const bool publisher = wave == kWaves - 1;
 
-  // this workgroup's own line: [0, 1] its launches (64 bits), [2] the geometry
+  // this workgroup's own line: [0, 1] its last epoch (64 bits), [2] the geometry
   // fingerprint, [3] the failure mark (set in every line when a wait of any
   // workgroup gives up); read first (only failing workgroups write other
   // workgroups' lines)
@@ -197,7 +224,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
         if (tid == 0) {
           const bool foreign = fp_seen != 0 && fp_seen != fingerprint;
           if (foreign) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          L.epoch = (uint32_t)launches + 1u;
+          L.epoch = (uint32_t)(launches % kEpochs) + 1u;
           L.fp_seen = fp_seen;
           L.bad = foreign || marked != 0;
         }
@@ -246,7 +273,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       }
     }
     if (lane == 0) {
-      // the launch count of this launch: the epoch (thread 0 read the line)
+      // this launch's epoch, for the next launch (thread 0 read the line)
       __hip_atomic_store(reinterpret_cast<uint64_t*>(line), (uint64_t)L.epoch, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
       if (L.fp_seen == 0)

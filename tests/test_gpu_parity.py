@@ -240,6 +240,46 @@ def test_workspace_of_another_geometry_is_refused():
                                    f"(was {v[tuple(diff[:4].T)].tolist()}); {info}")
 
 
+def test_launch_epoch_wraps():
+    """The one-launch step's epochs run 1 .. 2^31 - 1 and then start again at 1.
+    A fresh workspace whose control lines (set from the host) say that the last
+    launch had epoch 2^31 - 2: the next steps run at epochs 2^31 - 1, 1, 2, ...
+    and must match the oracle bit for bit (selections) and within tolerance
+    (outputs) across the wrap."""
+    import numpy as np
+    import oracle
+    import torch
+    from gpu_harness import TOL, Stats, _gpu_layer, compare_step
+    from paper_2508_09001_amd import binding as B
+    for cfg in (0, 1):
+        spec = W.config(cfg)
+        gen = W.Generator(spec)
+        orc = oracle.Oracle.for_spec(spec)
+        layer = _gpu_layer(spec, None)
+        assert B.retro_step_launches(layer.dims) == 1
+        for b, (k, v) in enumerate(gen.prefill()):
+            orc.prefill(b, k, v)
+            layer.prefill(b, k, v)
+        lines = layer.workspace[:1024 * 128].view(torch.int32).view(1024, 32)
+        lines[:, 0] = 0x7FFFFFFE
+        lines[:, 1] = 0
+        qw = W.QueryWindow(spec)
+        stats = Stats()
+        for t in range(spec.window + 3):
+            k_new, v_new, q = gen.step(t)
+            win = qw.push(q).copy()
+            ref = orc.step(t, k_new, v_new, win)
+            ref["A"] = orc.A
+            print(f"[epoch wrap] {spec.name} step {t}", flush=True)
+            layer.step(t, win, k_new[-1], v_new[-1])
+            compare_step(t, layer, ref, TOL[spec.dtype], stats)
+            # the lines of the launch's workgroups hold its epoch; the rest
+            # (no workgroup of this geometry) keep the preset value
+            epochs = set(np.unique(lines[:, 0].cpu().numpy()).tolist())
+            want = 0x7FFFFFFF if t == 0 else t
+            assert int(lines[0, 0]) == want and epochs <= {want, 0x7FFFFFFE}, (t, epochs)
+
+
 def test_page_pool_larger_than_the_tables_shuffled():
     """Physical pages drawn at random from a pool larger than batch * max_pages
     (digests stay per logical page): the headline layer and a ragged batch."""
