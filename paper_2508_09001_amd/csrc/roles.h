@@ -15,11 +15,6 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMaxPieces = 4;       // 16-byte staging registers per thread per chunk (attention kernel)
 constexpr int kMaxSplitPages = 64;  // selected pages per attention split
 
-
-// The thread's index in the workgroup, as a value the compiler cannot move:
-// roles run inside the fused kernel's task loop, and values computed from the
-// index alone would otherwise be hoisted out of it and kept live (in registers
-// every role then lacks) across all roles.
 // Device-coherent accesses (sc1: written through / read past the per-XCD L2s)
 // for data handed between workgroups of one launch without fences.  Vector
 // forms go through a buffer resource over [base, base + 2 GiB) (byte offsets;
@@ -41,6 +36,20 @@ __device__ __forceinline__ V get_c(const V* p) {
   else return *p;
 }
 
+// A load through the scalar data cache (constant address space) from an
+// address that is the same for the whole wavefront.  Its completion is counted
+// apart from the vector loads', so waiting for it does not wait for the vector
+// loads issued before it.  Only for memory that no workgroup of the launch
+// writes before the read: the scalar cache is not kept coherent within a
+// launch (it starts empty at every launch).
+template <typename V>
+__device__ __forceinline__ V sload(const V* p) {
+  return *(const __attribute__((address_space(4))) V*)p;
+}
+
+// The thread's index in the workgroup, as a value the compiler cannot move:
+// values computed from the index alone would otherwise be hoisted and kept
+// live (in registers the later phases of a kernel then lack) across phases.
 __device__ __forceinline__ int thread_index() {
   int t = threadIdx.x;
   asm volatile("" : "+v"(t));
@@ -312,8 +321,21 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
   const int nthreads = NT > 0 ? NT : (int)blockDim.x;
   const int lane = tid & 63, wave = tid >> 6, nw = nthreads >> 6;
   const int c = lane % S::LPP;
-  // every load before any wait: digest rows (in bounds of the [max_pages] row
-  // whatever the sequence length), the queries, the token's key
+  // every load before any wait: the group's queries (first: they are staged
+  // before the barrier, and loads complete in order), digest rows (in bounds
+  // of the [max_pages] row whatever the sequence length), the token's key.
+  // Queries as 16-byte pieces, QR per thread (G * d <= 16 d elements), all
+  // requested before any is converted, without a branch (threads past the
+  // group's queries load its last piece and store nothing)
+  constexpr int QV = 16 / sizeof(T);
+  constexpr int QR = NT > 0 ? (16 * D + NT * QV - 1) / (NT * QV) : 2;
+  const int gd = (GC > 0 ? GC : g.G) * D;
+  uint4 qraw[QR];
+#pragma unroll
+  for (int r = 0; r < QR; ++r) {
+    const int e = (tid + r * nthreads) * QV;
+    qraw[r] = *reinterpret_cast<const uint4*>(q + min(e, gd - QV));
+  }
   uint32_t raw[ITERS][2][S::WORDS];
   const int last_row = max(page_end - 1, 0);
 #pragma unroll
@@ -322,16 +344,6 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
     const T* row = drow + (int64_t)page * 2 * D + c * S::VEC;
     load_words<S::WORDS>(row, raw[it][0]);
     load_words<S::WORDS>(row + D, raw[it][1]);
-  }
-  // the group's queries: 16-byte pieces, at most two per thread (G * d <= 2048
-  // elements for 256 threads), all requested before any is converted
-  constexpr int QV = 16 / sizeof(T);
-  const int gd = (GC > 0 ? GC : g.G) * D;
-  uint4 qraw[2];
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int e = (tid + r * nthreads) * QV;
-    if (e < gd) qraw[r] = *reinterpret_cast<const uint4*>(q + e);
   }
   int n_pages = 0;
   const StepToken<T> tok = tok_of(n_pages);
@@ -345,14 +357,11 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
     tok_k = tok.k[min(tid, D - 1)];
     tok_v = tok.v[min(tid, D - 1)];
   }
-  float kv[S::VEC];
-  if (has_tok) {
-    uint32_t kw[S::WORDS];
-    load_words<S::WORDS>(tok.k + c * S::VEC, kw);
-    words_to_f32<T, S::WORDS>(kw, kv);
-  }
+  // (converted where the token's page is scored, after the barrier)
+  uint32_t kw[S::WORDS] = {};
+  if (has_tok) load_words<S::WORDS>(tok.k + c * S::VEC, kw);
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
+  for (int r = 0; r < QR; ++r) {
     const int e = (tid + r * nthreads) * QV;
     if (e < gd) {
       const uint32_t w[4] = {qraw[r].x, qraw[r].y, qraw[r].z, qraw[r].w};
@@ -377,6 +386,8 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
     words_to_f32<T, S::WORDS>(raw[it][0], lo);
     words_to_f32<T, S::WORDS>(raw[it][1], hi);
     if (has_tok && page == tok.lp) {  // widen (or start) the digest with the new key
+      float kv[S::VEC];
+      words_to_f32<T, S::WORDS>(kw, kv);
 #pragma unroll
       for (int v = 0; v < S::VEC; ++v) {
         if (tok.slot == 0) {

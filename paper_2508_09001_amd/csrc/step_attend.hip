@@ -126,17 +126,34 @@ struct StepLds {
 // their write-through.
 constexpr int kPollThreads = kThreads - 64;
 
-// Leading arguments (the pointers and sizes the first loads need: digests,
-// then queries) come before the argument block so that they can be preloaded
-// into scalar registers: the digest loads then go out without waiting for the
-// kernel-argument segment.
+// The kernel's parameters in order: the layout of its kernel-argument segment.
+template <typename T>
+struct StepParams {
+  T* dg;
+  uint32_t mp, ppb, nw, ngrid;
+  const T* q_cur;
+  uint32_t hk, q_bstride;
+  uint32_t* ctl;
+  uint64_t* tagged;
+  uint32_t fingerprint;
+  StepAttendArgs sa;
+};
+
+// Leading arguments (the pointers and sizes the first loads need: queries and
+// digests) come before the argument block so that they can be preloaded into
+// scalar registers: those loads then go out without waiting for the
+// kernel-argument segment.  The argument block itself is read through the
+// segment pointer, passed through an empty asm statement once those loads are
+// out (tok_of): the compiler would otherwise load its fields (and wait for
+// them, several scalar round trips) ahead of the first vector loads.
 template <typename T, int D, int PER, int SITERS, int GC>
 __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     T* __restrict__ dg, uint32_t mp, uint32_t ppb, uint32_t nw, uint32_t ngrid,
     const T* __restrict__ q_cur, uint32_t hk, uint32_t q_bstride, uint32_t* __restrict__ ctl,
-    uint64_t* __restrict__ tagged, uint32_t fingerprint, StepAttendArgs sa) {
+    uint64_t* __restrict__ tagged, uint32_t fingerprint, StepAttendArgs sa_param) {
   __shared__ __attribute__((aligned(16))) StepLds<T, D, PER, SITERS> L;
-  const Geometry& g = sa.a.g;
+  auto kseg = __builtin_amdgcn_kernarg_segment_ptr();
+  const StepAttendArgs* sap = nullptr;  // set by tok_of
   const int tid = thread_index();
   const int wave = tid >> 6, lane = tid & 63;
   const uint32_t u = (uint32_t)xcd_remap(blockIdx.x, ngrid);
@@ -145,30 +162,16 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   const int page0 = (int)(j * ppb);
   const int page_end = min(page0 + (int)ppb, (int)mp);
   const int b = (int)(bh / hk), h = (int)bh - b * (int)hk;
-  const int gsize = GC > 0 ? GC : g.G;
+  const int gsize = GC > 0 ? GC : sa_param.a.g.G;
   const bool publisher = wave == kWaves - 1;
 
   // this workgroup's own line: [0, 1] its last epoch (64 bits), [2] the geometry
   // fingerprint, [3] the failure mark (set in every line when a wait of any
-  // workgroup gives up); read first (only failing workgroups write other
-  // workgroups' lines)
+  // workgroup gives up); read once the score phase's first loads are out
+  // (only failing workgroups write other workgroups' lines)
   uint32_t* line = ctl + ((size_t)bh * nw + j) * 32;
   uint64_t launches = 0;
   uint32_t fp_seen = 0, marked = 0;
-  if (tid == 0) {
-    launches = __hip_atomic_load(reinterpret_cast<uint64_t*>(line), __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-    fp_seen = __hip_atomic_load(line + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    marked = __hip_atomic_load(line + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  // a wait gave up (wavefront-uniform call): the sticky error word for the
-  // caller, and the failure mark in every workgroup's line, so that every later
-  // launch on this workspace fails from its start without a shared read
-  auto give_up = [&] {
-    if (lane == 0) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (uint32_t i = (uint32_t)lane; i < ngrid; i += 64)
-      __hip_atomic_store(ctl + (size_t)i * 32 + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  };
   int seq_len = 0, tok_lp = -1;
   StepToken<T> tok{-1, 0, nullptr, nullptr, nullptr, nullptr};
   T tok_kv[2][(D + 63) / 64];  // the publisher's lanes: the token's key and value elements
@@ -176,13 +179,28 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   int32_t a_old[PER], phys[PER];
   uint64_t* trow = tagged + (size_t)bh * (mp + 2 * nw);
   uint64_t* hrow = trow + mp;  // per workgroup: the key range of its share
-  float* srow = sa.scores + (size_t)bh * mp;
 
   // ---- 1: this workgroup's share of the head's scores, into LDS
   score_role<T, D, SITERS, true, GC, kThreads>(
-      g, page0, page_end,
+      sa_param.a.g, page0, page_end,
       q_cur + (size_t)b * q_bstride + (size_t)h * gsize * D, dg + (size_t)bh * mp * 2 * D, L.sq,
       [&](int& np) {
+        asm volatile("" : "+s"(kseg) : : "memory");
+        sap = (const StepAttendArgs*)((const __attribute__((address_space(4))) char*)kseg +
+                                      offsetof(StepParams<T>, sa));
+        const StepAttendArgs& sa = *sap;
+        const Geometry& g = sa.a.g;
+        // Scalar loads (counted apart from the vector loads in flight, so
+        // that their waits do not wait for the digests): the control line,
+        // the sequence length and then the token's page-table entry.  No
+        // workgroup of the launch writes them before these reads: the line
+        // is written by its own workgroup afterwards (or by a failing one),
+        // seq_lens only once every workgroup of the sequence has read it.
+        const uint32_t cl0 = sload(line), cl1 = sload(line + 1);
+        fp_seen = sload(line + 2);
+        marked = sload(line + 3);
+        launches = (uint64_t)cl1 << 32 | cl0;
+        const int pos = sload(sa.a.seq_lens + b);
         // the selection's stripe of last_loaded and page-table entries, with
         // the digests (no load here depends on another)
         const int32_t* arow = sa.A + (size_t)bh * mp;
@@ -193,10 +211,11 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
           a_old[jj] = arow[idx];
           phys[jj] = prow[idx];
         }
-        const int pos = sa.a.seq_lens[b];
         seq_len = pos;
         if (g.token_pending) {
-          const int ph = token_phys(g, sa.a.pt, b, pos);
+          const int lp = pos / g.P;
+          int ph = (pos >= 0 && lp < (int)mp) ? sload(prow + lp) : -1;
+          if (ph >= g.num_phys) ph = -1;
           if (ph >= 0) {
             seq_len = pos + 1;
             tok = make_step_token<T>(g, b, h, pos, ph, sa.k_new, sa.v_new,
@@ -223,7 +242,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
         thr_clear(L.u.thr);
         if (tid == 0) {
           const bool foreign = fp_seen != 0 && fp_seen != fingerprint;
-          if (foreign) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (foreign) __hip_atomic_store(sap->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           L.epoch = (uint32_t)(launches % kEpochs) + 1u;
           L.fp_seen = fp_seen;
           L.bad = foreign || marked != 0;
@@ -231,6 +250,17 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       },
       [&](int page, float v) { L.share[page - page0] = v; }, L.dig);
 
+  const StepAttendArgs& sa = *sap;
+  const Geometry& g = sa.a.g;
+  float* srow = sa.scores + (size_t)bh * mp;
+  // a wait gave up (wavefront-uniform call): the sticky error word for the
+  // caller, and the failure mark in every workgroup's line, so that every later
+  // launch on this workspace fails from its start without a shared read
+  auto give_up = [&] {
+    if (lane == 0) __hip_atomic_store(sa.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (uint32_t i = (uint32_t)lane; i < ngrid; i += 64)
+      __hip_atomic_store(ctl + (size_t)i * 32 + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
   const int n = min((seq_len + g.P - 1) / g.P, (int)mp);
   // Every load of caller state this workgroup makes (seq_lens, last_loaded, the
   // page table) has returned before its first tagged store below: a workgroup
