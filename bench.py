@@ -84,12 +84,17 @@ def _sha(paths):
     return h.hexdigest()
 
 
-def _step_path(launches):
+def _step_path(launches, reuse=0):
     """The launch sequence retro_step takes (the library's own choice, no flags)."""
     if launches == 1:
-        return "one launch: scores, selection, attention, combine + merge"
-    return (f"{launches} launches: scores (+ selection), [selection +] attention, "
-            "combine + merge")
+        path = "one launch: scores, selection, attention, combine + merge"
+    else:
+        path = (f"{launches} launches: scores (+ selection), [selection +] attention, "
+                "combine + merge")
+    if reuse >= 2:
+        path = (f"refresh steps (t mod {reuse} == 0): {path}; other steps keep the selection: "
+                "4 launches: append, mask, attention, combine + merge")
+    return path
 
 
 def algorithmic_bytes(spec, seq_lens, num_selected):
@@ -99,7 +104,10 @@ def algorithmic_bytes(spec, seq_lens, num_selected):
         spec.page_size, spec.window
     n_pages = sum(-(-int(L) // P) for L in seq_lens)
     k_sum = int(sum(int(x) for x in num_selected.reshape(-1)))     # over (b, h)
-    digest = n_pages * hk * 2 * d * elt
+    # with top-k reuse (refresh every f steps) only the refresh steps scan the
+    # digests and select: their bytes averaged over the steps
+    f = spec.reuse_interval if spec.reuse_interval >= 2 else 1
+    digest = n_pages * hk * 2 * d * elt // f
     gather = k_sum * P * 2 * d * elt
     queries = b * (W + 1) * hq * d * elt
     ring = 2 * b * W * hq * (d + 1) * 4
@@ -107,7 +115,7 @@ def algorithmic_bytes(spec, seq_lens, num_selected):
     mask = 12 * k_sum
     append = b * hk * d * elt * 2 + b * hk * 2 * d * elt * 2
     # what the selection reads besides the scores: last_loaded per (b, h), the page table per b
-    select_reads = n_pages * hk * 4 + n_pages * 4
+    select_reads = (n_pages * hk * 4 + n_pages * 4) // f
     return dict(total=digest + gather + queries + ring + out + mask + append, digest=digest,
                 gather=gather, queries=queries, ring=ring, out=out, mask=mask, append=append,
                 select_reads=select_reads)
@@ -256,7 +264,7 @@ def main():
     win_last = steps_in[last][0]
     n_att = args.attend_reps * L
     traffic = None
-    if launches == 1:
+    if launches == 1 and spec.reuse_interval < 2:
         # the dominant kernel is the step itself: its launches in the timed
         # graphs (one per layer-step), every algorithmic byte of the step
         kernel, us_kernel, kernel_bytes, n_kernel = ("step_attend_kernel", us_layer_step,
@@ -302,7 +310,7 @@ def main():
                    "reuse_interval": spec.reuse_interval,
                    "layers_rotated": L,
                    "launch": "hip-graph per step",
-                   "step_path": _step_path(launches)},
+                   "step_path": _step_path(launches, spec.reuse_interval)},
         "us_per_layer_step": round(us_layer_step, 3),
         "us_per_layer_step_eager": round(ms_eager * 1000.0 / (args.steps * L), 3),
         "frac_of_peak_hbm": round(gbs / PEAK_HBM_GBS, 4),
