@@ -396,6 +396,16 @@ retro_status retro_project_qkv_update(const retro_dims* dims, const retro_kv_cac
 retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const void* w_packed,
                                int32_t n, float* h, void* x_next, void* stream);
 
+/* The projections of the multi-layer decode (Sec. 3.3) for fp32 stacks:
+ * y = x . w (accumulate == 0) or y += x . w (accumulate != 0: the output
+ * projection added into the residual stream in place) for x [rows][k] and w
+ * [k][n] fp32 row-major (not packed), y [rows][n] fp32; x and y must not
+ * overlap.  Each output element is one fp32 fused multiply-add chain over
+ * i = 0 .. k-1 in order, so results repeat exactly from run to run.  rows == 0
+ * does nothing; rows > 65535 or rows * n >= 2^31 is RETRO_EUNSUPPORTED. */
+retro_status retro_project_f32(const float* x, int32_t rows, int32_t k, const float* w,
+                               int32_t n, float* y, int32_t accumulate, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

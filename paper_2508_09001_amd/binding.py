@@ -25,7 +25,7 @@ EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_worksp
             "retro_decode_attend", "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_step_noalloc",
             "retro_step_launches", "retro_pack_weight", "retro_project_qkv",
-            "retro_project_qkv_update", "retro_project_out")
+            "retro_project_qkv_update", "retro_project_out", "retro_project_f32")
 
 
 class RetroError(RuntimeError):
@@ -100,6 +100,7 @@ def load_library(path: str = LIB_PATH):
         "retro_pack_weight": ([P, i32, i32, P, P], C.c_int),
         "retro_project_qkv": ([P, i32, i32, P, i32, i32, P, P, P, P], C.c_int),
         "retro_project_out": ([P, i32, i32, P, i32, P, P, P], C.c_int),
+        "retro_project_f32": ([P, i32, i32, P, i32, P, i32, P], C.c_int),
         "retro_project_qkv_update": ([D, C.POINTER(KVCache), P, i32, P, i32, P, P, P, P],
                                      C.c_int),
     }
@@ -254,6 +255,13 @@ def retro_project_qkv(x, rows: int, k: int, w_packed, n_q: int, n_kv: int, q, k_
 def retro_project_out(o, rows: int, k: int, w_packed, n: int, h, x_next, stream=None) -> None:
     _check(load_library().retro_project_out(_ptr(o), rows, k, _ptr(w_packed), n, _ptr(h),
                                             _ptr(x_next), _stream(stream)), "retro_project_out")
+
+
+def retro_project_f32(x, rows: int, k: int, w, n: int, y, accumulate: bool = False,
+                      stream=None) -> None:
+    _check(load_library().retro_project_f32(_ptr(x), rows, k, _ptr(w), n, _ptr(y),
+                                            1 if accumulate else 0, _stream(stream)),
+           "retro_project_f32")
 
 
 def retro_project_qkv_update(dims: Dims, cache: KVCache, x, k: int, w_packed, n_update: int, q,

@@ -352,6 +352,41 @@ bool project_qkv_update_supported(const Geometry& g, int k) {
 
 }  // namespace retro
 
+namespace {
+
+// fp32 projections (fp32 stacks): one thread per output element (row r =
+// blockIdx.y, column j), an in-order fused multiply-add chain over the k inputs;
+// the row's inputs staged through LDS 1024 at a time, the weight read by
+// consecutive columns (coalesced).
+constexpr int kF32Threads = 256;
+constexpr int kF32Chunk = 1024;
+__global__ void __launch_bounds__(kF32Threads) project_f32_kernel(const float* __restrict__ x,
+                                                                  int K, const float* __restrict__ w,
+                                                                  int N, float* __restrict__ y,
+                                                                  int accumulate) {
+  __shared__ float xs[kF32Chunk];
+  const int r = blockIdx.y;
+  const int j = blockIdx.x * kF32Threads + threadIdx.x;
+  const float* xr = x + (int64_t)r * K;
+  float acc = 0.f;
+  for (int i0 = 0; i0 < K; i0 += kF32Chunk) {
+    const int cnt = min(kF32Chunk, K - i0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < cnt; i += kF32Threads) xs[i] = xr[i0 + i];
+    __syncthreads();
+    if (j < N) {
+      const float* wc = w + (int64_t)i0 * N + j;
+      for (int i = 0; i < cnt; ++i) acc = fmaf(xs[i], wc[(int64_t)i * N], acc);
+    }
+  }
+  if (j < N) {
+    float* yo = y + (int64_t)r * N + j;
+    *yo = accumulate ? *yo + acc : acc;
+  }
+}
+
+}  // namespace
+
 extern "C" {
 
 retro_status retro_pack_weight(const void* w, int32_t k, int32_t n, void* w_packed,
@@ -407,6 +442,17 @@ retro_status retro_project_out(const float* o, int32_t rows, int32_t k, const vo
   a.h = h;
   a.x_next = static_cast<retro::bf16_t*>(x_next);
   return retro::status_of(retro::launch_proj<true, false>(a, (hipStream_t)stream));
+}
+
+retro_status retro_project_f32(const float* x, int32_t rows, int32_t k, const float* w,
+                               int32_t n, float* y, int32_t accumulate, void* stream) {
+  if (!x || !w || !y || rows < 0 || k <= 0 || n <= 0) return RETRO_EINVAL;
+  if (rows == 0) return RETRO_OK;
+  if (rows > 65535 || (int64_t)rows * n >= (int64_t(1) << 31)) return RETRO_EUNSUPPORTED;
+  const dim3 grid((unsigned)((n + kF32Threads - 1) / kF32Threads), (unsigned)rows);
+  project_f32_kernel<<<grid, kF32Threads, 0, (hipStream_t)stream>>>(
+      x, k, w, n, y, accumulate ? 1 : 0);
+  return retro::status_of(hipGetLastError());
 }
 
 }  // extern "C"

@@ -15,7 +15,9 @@ the weights.  In bf16 they run in the library too (``retro_project_qkv``: one
 launch for the query, key and value projections of a layer, weights pre-tiled by
 ``retro_pack_weight``; ``retro_project_out``: the output projection fused with the
 residual add and the next layer's bf16 input), both bf16 in, fp32 accumulation,
-bf16 out.  fp32 stacks (small test shapes) use torch.matmul for the products.
+bf16 out.  fp32 stacks use ``retro_project_f32`` (fp32 fused multiply-add
+chains on the unpacked weights, the output projection added into the residual
+stream in place).
 Feed-forward blocks and normalisation are left out: they do not touch the KV
 cache.
 """
@@ -93,6 +95,17 @@ class RetroDecoder:
             self.k_new = torch.zeros(self.batch, self.hk, self.d, dtype=td, device=dev)
             self.v_new = torch.zeros_like(self.k_new)
         self.fuse_update = self.fused and fuse_update
+        # fp32: library projections on the unpacked weights (retro_project_f32)
+        self.f32_library = library_projections and self.dtype == torch.float32
+        if self.f32_library:
+            dev = self.device
+            self.h = torch.zeros(self.batch, self.W + 1, self.d_model, dtype=torch.float32,
+                                 device=dev)
+            self.q = torch.zeros(self.batch, self.W + 1, self.hq, self.d, dtype=torch.float32,
+                                 device=dev)
+            self.k = torch.zeros(self.batch, self.W + 1, self.hk, self.d, dtype=torch.float32,
+                                 device=dev)
+            self.v = torch.zeros_like(self.k)
 
     def prefill(self, layer: int, seq: int, k, v, stream=None) -> None:
         """Prompt keys and values [n][h_k][d] of one sequence in one layer."""
@@ -119,6 +132,8 @@ class RetroDecoder:
         n_upd = self.n_update()
         if self.fused:
             return self._step_fused(t, emb_window, n_upd, trace)
+        if self.f32_library:
+            return self._step_f32(t, emb_window, n_upd, trace)
         h = emb_window.to(device=self.device, dtype=torch.float32)
         for lay, w in zip(self.layers, self.weights):
             x = h.to(self.dtype)
@@ -137,6 +152,29 @@ class RetroDecoder:
             h = h + y.float()
         self.decoded += 1
         return h
+
+    def _step_f32(self, t, emb_window, n_upd, trace):
+        """fp32 stack: every product in the library (retro_project_f32), the
+        residual stream itself the next layer's input."""
+        b, rows, W = self.batch, self.W + 1, self.W
+        nq, nkv, r = self.hq * self.d, self.hk * self.d, self.batch * (self.W + 1)
+        self.h.copy_(emb_window)
+        for lay, w in zip(self.layers, self.weights):
+            h_in = self.h.clone() if trace is not None else None
+            B.retro_project_f32(self.h, r, self.d_model, w["wq"], nq, self.q)
+            B.retro_project_f32(self.h, r, self.d_model, w["wk"], nkv, self.k)
+            B.retro_project_f32(self.h, r, self.d_model, w["wv"], nkv, self.v)
+            if n_upd > 0:
+                lay.update_kv(self.k[:, W - n_upd:W], self.v[:, W - n_upd:W])
+            lay.step(t, self.q, self.k[:, W], self.v[:, W])
+            B.retro_project_f32(lay.o_out, r, nq, w["wo"], self.d_model, self.h, accumulate=True)
+            if trace is not None:
+                trace.append(dict(x=h_in, q=self.q.clone(), k=self.k.clone(), v=self.v.clone(),
+                                  o_out=lay.o_out.clone(), lse_out=lay.lse_out.clone(),
+                                  selected=lay.selected.clone(), mask=lay.mask.clone(),
+                                  num_selected=lay.num_selected.clone(), y=self.h - h_in))
+        self.decoded += 1
+        return self.h
 
     def _step_fused(self, t, emb_window, n_upd, trace):
         b, rows, W = self.batch, self.W + 1, self.W

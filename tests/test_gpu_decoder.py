@@ -234,6 +234,37 @@ def test_project_out_adds_the_residual(rows, K, n):
     np.testing.assert_array_equal(xn.float().cpu().numpy(), round_to(hn, "bf16"))
 
 
+@pytest.mark.parametrize("rows,K,n,accumulate", [(1, 256, 512, False), (5, 1000, 96, False),
+                                                 (18, 2500, 300, True), (40, 64, 1024, True)])
+def test_project_f32_matches_fp64_products(rows, K, n, accumulate):
+    """fp32 projections of fp32 stacks: each element is an fp32 fused
+    multiply-add chain, within the textbook bound gamma_K * sum |x| |w| of the
+    fp64 product (plus one rounding of the residual add), and the same bits on a
+    second call."""
+    import torch
+    from paper_2508_09001_amd import binding as B
+    print(f"[proj] f32 rows={rows} K={K} n={n} accumulate={accumulate}", flush=True)
+    rng = np.random.default_rng(rows * 131 + K + n)
+    x = rng.standard_normal((rows, K)).astype(np.float32)
+    w = (rng.standard_normal((K, n)) * K ** -0.5).astype(np.float32)
+    h0 = rng.standard_normal((rows, n)).astype(np.float32) if accumulate else \
+        np.zeros((rows, n), np.float32)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.from_numpy(h0).cuda()
+    B.retro_project_f32(xd, rows, K, wd, n, y, accumulate=accumulate)
+    y2 = torch.from_numpy(h0).cuda()
+    B.retro_project_f32(xd, rows, K, wd, n, y2, accumulate=accumulate)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().astype(np.float64)
+    ref = h0.astype(np.float64) + x.astype(np.float64) @ w.astype(np.float64)
+    u = 2.0 ** -24
+    gamma = K * u / (1 - K * u)
+    bound = gamma * (np.abs(x).astype(np.float64) @ np.abs(w).astype(np.float64)) + \
+        u * np.abs(ref) * (2 if accumulate else 0)
+    assert np.all(np.abs(got - ref) <= bound + 1e-30)
+    assert torch.equal(y, y2)
+
+
 def test_projection_shape_errors_are_reported_before_any_launch():
     import torch
     from paper_2508_09001_amd import binding as B
