@@ -292,8 +292,9 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
  * q_window), retro_decode_attend, retro_merge_output_cache, with the same
  * semantics, without materialising o_part / lse_part.
  * One launch where every workgroup of it fits on the GPU at once (as the
- * occupancy of its kernel times the compute units tells; up to 2240 pages per
- * sequence, at most 64 KV heads per launch, at most 1024 workgroups, rtw 1):
+ * occupancy of its kernel times the compute units tells; up to 4480 pages per
+ * sequence and 160 per workgroup, (window + 1) * group <= 128 rows, at most 64
+ * KV heads and 1024 workgroups):
  * page scores (with the append), selection, attention, combine + merge, the
  * last_loaded update and the seq_lens advance, the workgroups of a KV head
  * handing each other scores and partial results through tagged words in

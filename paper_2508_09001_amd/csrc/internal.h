@@ -127,7 +127,7 @@ hipError_t launch_attend_select(const Geometry& g, int step, const void* q_windo
 // with the output cache; the head's first workgroup applies the last_loaded
 // update, and the sequence's first advances seq_lens (with g.token_pending).
 // Only when every workgroup is resident at once (step_attend_supported:
-// occupancy times compute units; rtw == 1, max_pages <= 2240, at most 96 pages
+// occupancy times compute units; rtw == 1, max_pages <= 4480, at most 160 pages
 // scored per workgroup, at most 64 workgroups per head and 64 KV heads, at most
 // kCtlLines workgroups).  Uses the workspace's tagged words and per-workgroup
 // control lines (zero-filled once, then holding the last launch's epoch;

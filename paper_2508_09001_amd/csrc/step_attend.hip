@@ -110,7 +110,7 @@ struct StepLds {
   int s_phys[kMaxSplitPages], s_len[kMaxSplitPages], s_mask[kMaxSplitPages];
   // the head writer's selection (page, mask value per kept slot) and the
   // token's page if it is not kept (-1 otherwise), stored after the attention
-  int wsel[5 * (kThreads - 64)], wmsk[5 * (kThreads - 64)];  // up to the largest page count
+  int wsel[PER * (kThreads - 64)], wmsk[PER * (kThreads - 64)];  // up to the largest page count
   int wtok;
   int s_tok;
   uint32_t epoch, fp_seen;
@@ -548,20 +548,37 @@ const void* kernel_ptr() {
   return reinterpret_cast<const void*>(&step_attend_kernel<T, D, PER, SITERS, GC>);
 }
 
-constexpr int kSiters = 3;  // score passes: at most 3 * 32 pages per workgroup
+// An instantiation's shape: PER pages of the head per polling thread (the
+// selection's stripes) and SITERS score passes of 32 pages per workgroup.
+template <int PER_, int SITERS_>
+struct Shape {
+  static constexpr int PER = PER_, SITERS = SITERS_;
+};
+constexpr int kMaxPer = 10, kMaxSiters = 5;  // the long-context shape
 
-// The instantiation for g: (dtype, d, stripes per thread, unrolled group).
+// Score passes a geometry needs: 3 up to 96 pages per workgroup, else 5 (160).
+bool long_shape(const Geometry& g) {
+  const int nw = g.n_splits * g.n_rgroups;
+  const int ppb = (g.max_pages + nw - 1) / nw;
+  return g.max_pages > 5 * kPollThreads || ppb > 3 * kWaves * 4;
+}
+
+// The instantiation for g: (dtype, d, shape, unrolled group).
 template <typename F>
 auto dispatch(const Geometry& g, F&& f) {
   const bool g4 = g.G == 4;
+  const bool lng = long_shape(g);
   auto per = [&](auto t, auto d) {
     using T = typename decltype(t)::type;
     constexpr int DD = decltype(d)::value;
-    if (g.max_pages <= 2 * kPollThreads)
-      return g4 ? f(kernel_ptr<T, DD, 2, kSiters, 4>(), std::integral_constant<int, 2>{}, t, d, std::integral_constant<int, 4>{})
-                : f(kernel_ptr<T, DD, 2, kSiters, 0>(), std::integral_constant<int, 2>{}, t, d, std::integral_constant<int, 0>{});
-    return g4 ? f(kernel_ptr<T, DD, 5, kSiters, 4>(), std::integral_constant<int, 5>{}, t, d, std::integral_constant<int, 4>{})
-              : f(kernel_ptr<T, DD, 5, kSiters, 0>(), std::integral_constant<int, 5>{}, t, d, std::integral_constant<int, 0>{});
+    auto go = [&](auto shape) {
+      using S = decltype(shape);
+      return g4 ? f(kernel_ptr<T, DD, S::PER, S::SITERS, 4>(), shape, t, d, std::integral_constant<int, 4>{})
+                : f(kernel_ptr<T, DD, S::PER, S::SITERS, 0>(), shape, t, d, std::integral_constant<int, 0>{});
+    };
+    if (lng) return go(Shape<kMaxPer, kMaxSiters>{});
+    if (g.max_pages <= 2 * kPollThreads) return go(Shape<2, 3>{});
+    return go(Shape<5, 3>{});
   };
   struct BF { using type = bf16_t; };
   struct F32 { using type = float; };
@@ -604,8 +621,9 @@ int step_attend_workgroups(const Geometry& g) { return g.n_splits * g.n_rgroups 
 bool step_attend_supported(const Geometry& g) {
   const int nw = g.n_splits * g.n_rgroups;
   const int ppb = (g.max_pages + nw - 1) / nw;
-  if (g.rtw != 1 || g.max_pages > 5 * kPollThreads ||
-      ppb > kSiters * (kThreads / 64) * 4 || nw > 64 || g.hk > 64 || g.n_splits > 64)
+  if (g.rtw != 1 || g.max_pages > kMaxPer * kPollThreads ||
+      ppb > (long_shape(g) ? kMaxSiters : 3) * kWaves * 4 || nw > 64 || g.hk > 64 ||
+      g.n_splits > 64)
     return false;
   // partial outputs are read through a buffer resource of 2 GiB
   if ((int64_t)g.batch * g.hk * g.n_splits * g.R * g.D * 4 >= (int64_t(1) << 31)) return false;
@@ -651,11 +669,12 @@ hipError_t launch_step_attend(const Geometry& g, int step, const void* q_window,
   uint32_t* ctl = reinterpret_cast<uint32_t*>((char*)workspace + g.ws_heads);
   const uint32_t fp = fingerprint_of(g);
   const uint32_t q_bstride = (uint32_t)((g.W + 1) * g.hq * g.D);
-  return dispatch(g, [&](const void*, auto per, auto t, auto d, auto gc) {
+  return dispatch(g, [&](const void*, auto shape, auto t, auto d, auto gc) {
     using T = typename decltype(t)::type;
+    using S = decltype(shape);
     constexpr int DD = decltype(d)::value;
     const T* q_cur = reinterpret_cast<const T*>(q_window) + (size_t)g.W * g.hq * g.D;
-    step_attend_kernel<T, DD, decltype(per)::value, kSiters, decltype(gc)::value>
+    step_attend_kernel<T, DD, S::PER, S::SITERS, decltype(gc)::value>
         <<<grid, kThreads, 0, s>>>(reinterpret_cast<T*>(c.digest), (uint32_t)g.max_pages, ppb,
                                    nw, grid, q_cur, (uint32_t)g.hk, q_bstride, ctl, tagged, fp,
                                    sa);
