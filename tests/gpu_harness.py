@@ -13,15 +13,18 @@ TOL = {"bf16": 2e-3, "f32": 1e-5}   # max-abs on outputs and log-normalisers
 
 
 def _gpu_layer(spec, page_perm_seed: Optional[int], device="cuda", flags: int = 0,
-               pool_pages: Optional[int] = None):
+               pool_pages: Optional[int] = None, page_table: Optional[np.ndarray] = None):
     """A RetroLayer for spec.  page_perm_seed: logical pages map to a seeded random
     choice of distinct physical pages (a shuffled table) from a pool of pool_pages
-    physical pages (default batch * max_pages)."""
+    physical pages (default batch * max_pages); page_table: that table given
+    explicitly, [batch][max_pages]."""
     import torch
     from paper_2508_09001_amd.layer import RetroLayer
     pt = None
     pool = spec.batch * spec.max_pages if pool_pages is None else pool_pages
-    if page_perm_seed is not None:
+    if page_table is not None:
+        pt = torch.from_numpy(np.ascontiguousarray(page_table, np.int32))
+    elif page_perm_seed is not None:
         rng = np.random.default_rng(page_perm_seed)
         perm = rng.permutation(pool)[:spec.batch * spec.max_pages].astype(np.int32)
         pt = torch.from_numpy(perm.reshape(spec.batch, spec.max_pages))
@@ -112,7 +115,8 @@ def reembedded_kv(orc, n: int, rng, dtype: str):
 def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_calls=False,
                check_outputs_from: int = 0, tol: Optional[float] = None, label: str = "",
                update_kv: bool = False, flags: int = 0,
-               pool_pages: Optional[int] = None) -> Stats:
+               pool_pages: Optional[int] = None,
+               page_table: Optional[np.ndarray] = None) -> Stats:
     """Run `steps` decode steps on GPU and oracle; compare every step's selection,
     mask and A exactly, and the outputs of the steps >= check_outputs_from (the
     oracle runs attention only from check_outputs_from - W on, which is enough
@@ -126,7 +130,8 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
           flush=True)
     gen = W.Generator(spec)
     orc = oracle.Oracle.for_spec(spec)
-    layer = _gpu_layer(spec, page_perm_seed, flags=flags, pool_pages=pool_pages)
+    layer = _gpu_layer(spec, page_perm_seed, flags=flags, pool_pages=pool_pages,
+                       page_table=page_table)
     for b, (k, v) in enumerate(gen.prefill()):
         orc.prefill(b, k, v)
         layer.prefill(b, k, v)

@@ -280,6 +280,30 @@ def test_launch_epoch_wraps():
             assert int(lines[0, 0]) == want and epochs <= {want, 0x7FFFFFFE}, (t, epochs)
 
 
+def test_token_page_on_physical_page_zero_with_a_grid_off_the_xcd_count():
+    """Three KV heads of three splits each (9 workgroups: not a multiple of the 8
+    XCDs, so workgroups keep their dispatch order), the step's token pages mapped
+    to physical page 0 and its neighbour, the rest shuffled: the token's key and
+    value reach the gather of their own step from the step's input, whatever the
+    cache line of physical page 0 holds."""
+    import numpy as np
+    from paper_2508_09001_amd import binding as B
+    from gpu_harness import _gpu_layer
+    spec = W.Spec(name="grid9", batch=1, num_kv_heads=3, group=2, head_dim=64, page_size=16,
+                  budget=80, window=3, steps=24, dtype="bf16", prefill=(400,), seed=41)
+    mp = spec.max_pages
+    rng = np.random.default_rng(5)
+    pt = rng.permutation(mp).astype(np.int32)
+    first = spec.prefill[0] // spec.page_size  # the page the first steps append to
+    for lp, ph in ((first, 0), (first + 1, 1)):
+        j = int(np.where(pt == ph)[0][0])
+        pt[j], pt[lp] = pt[lp], pt[j]
+    layer = _gpu_layer(spec, None, page_table=pt[None])
+    assert B.retro_step_launches(layer.dims) == 1
+    del layer
+    run_parity(spec, spec.steps, page_table=pt[None], label="9 workgroups, token on page 0")
+
+
 def test_page_pool_larger_than_the_tables_shuffled():
     """Physical pages drawn at random from a pool larger than batch * max_pages
     (digests stay per logical page): the headline layer and a ragged batch."""
