@@ -401,17 +401,22 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     }
     k = min(min(budget_pages(g, seq_len), n), g.k_max);
     int pos[PER];
+    // the arguments the page lists need, read once into vector registers
+    // before the selection (the compiler would otherwise reload them in every
+    // stripe, each reload waiting for the LDS stores before it)
+    int step_m1 = sa.a.step - 1, pps = g.pages_per_split, nphys = g.num_phys, psz = g.P;
+    asm volatile("" : "+v"(step_m1), "+v"(pps), "+v"(nphys), "+v"(psz));
     threshold_select<PER, kWaves, kPollThreads, false>(L.u.thr, key, n, k, pos, kmn, kmx);
 
 #pragma unroll
     for (int jj = 0; jj < PER; ++jj) {
       const int p = jj * kPollThreads + tid;
       const int q = pos[jj];
-      const int m = p == tok_lp ? sa.a.step - 1 : a_old[jj];  // Alg. 2's current-page rule
-      if (q >= first && q < first + g.pages_per_split) {
-        const int ph = (phys[jj] >= 0 && phys[jj] < g.num_phys) ? phys[jj] : -1;
+      const int m = p == tok_lp ? step_m1 : a_old[jj];  // Alg. 2's current-page rule
+      if (q >= first && q < first + pps) {
+        const int ph = (phys[jj] >= 0 && phys[jj] < nphys) ? phys[jj] : -1;
         L.s_phys[q - first] = ph;
-        L.s_len[q - first] = ph >= 0 ? min(g.P, seq_len - p * g.P) : 0;
+        L.s_len[q - first] = ph >= 0 ? min(psz, seq_len - p * psz) : 0;
         L.s_mask[q - first] = m;
         if (p == tok_lp && ph >= 0) L.s_tok = q - first;
       }
