@@ -304,6 +304,23 @@ def test_token_page_on_physical_page_zero_with_a_grid_off_the_xcd_count():
     run_parity(spec, spec.steps, page_table=pt[None], label="9 workgroups, token on page 0")
 
 
+@pytest.mark.parametrize("budget,prefill,hk", [(512, 32000, 8), (512, 40000, 2)])
+def test_long_context_shape_of_the_one_launch_step(budget, prefill, hk):
+    """The one-launch step's long-context shape (ten selection stripes per
+    thread, five score passes) away from the 131K workload: a small budget that
+    leaves few splits, so that each workgroup scores more than 96 pages of a
+    2000-page sequence, and a 2500-page sequence on two KV heads."""
+    from paper_2508_09001_amd import binding as B
+    from gpu_harness import _gpu_layer
+    spec = W.Spec(name=f"long-shape-{budget}", batch=1, num_kv_heads=hk, group=4, head_dim=128,
+                  page_size=16, budget=budget, window=8, steps=10, dtype="bf16",
+                  prefill=(prefill,), seed=budget + hk)
+    layer = _gpu_layer(spec, None)
+    assert B.retro_step_launches(layer.dims) == 1
+    del layer
+    run_parity(spec, spec.steps, page_perm_seed=7, label=f"long shape B={budget} hk={hk}")
+
+
 def test_page_pool_larger_than_the_tables_shuffled():
     """Physical pages drawn at random from a pool larger than batch * max_pages
     (digests stay per logical page): the headline layer and a ragged batch."""
