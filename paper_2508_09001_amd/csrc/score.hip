@@ -76,6 +76,12 @@ __global__ void __launch_bounds__(score_threads(PER)) score_kernel(Geometry g, c
   const int page0 = blockIdx.x * ppb, page_end = min(page0 + ppb, g.max_pages);
   const int b = blockIdx.z, h = blockIdx.y;
   const int64_t bh = (int64_t)b * g.hk + h;
+  if constexpr (PER == 0) {
+    // a workgroup whose pages all lie past the sequence (the step's token
+    // included) has nothing to score: with sequences of mixed lengths the grid,
+    // sized for the longest, would otherwise load their stale digests
+    if (page0 * g.P > sload(seq_lens + b)) return;  // uniform
+  }
   // the step's token and the sequence's pages (after the digest loads are issued)
   int n_pages = 0, tok_lp = -1, live_len = 0;
   auto tok_of = [&](int& np) {
