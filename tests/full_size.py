@@ -48,8 +48,8 @@ def run_full(spec, steps: Optional[int] = None, *, check_steps=None, rows_per_ch
              graph: bool = True, label: str = "", flags: int = 0) -> int:
     import torch
     steps = spec.steps if steps is None else steps
-    if check_steps is None:
-        check_steps = {steps - 1, min(steps - 1, spec.window), steps // 2}
+    if check_steps is None:  # the window's ramp-up, eight evenly spaced steps, the last
+        check_steps = {steps - 1, min(steps - 1, spec.window)} | {i * steps // 8 for i in range(1, 8)}
     check_steps = set(check_steps)
     tol = TOL[spec.dtype]
     print(f"[full] {label or spec.name}: batch={spec.batch} hk={spec.num_kv_heads} G={spec.group} "
