@@ -111,3 +111,12 @@ def test_null_pointers_and_small_workspace_rejected_before_any_launch(lib):
     assert raw.retro_prefill_kv(C.byref(d), C.byref(cache), 0, 2080 * 16 - 2, 4, 1, 1,
                                 None) == lib.RETRO_EINVAL
     assert raw.retro_k_max(None, C.byref(S())) == lib.RETRO_EINVAL
+
+
+def test_project_f32_arguments_checked_on_the_host(lib):
+    raw = lib.load_library()
+    assert raw.retro_project_f32(None, 1, 4, 1, 4, 1, 0, None) == lib.RETRO_EINVAL
+    assert raw.retro_project_f32(1, -1, 4, 1, 4, 1, 0, None) == lib.RETRO_EINVAL
+    assert raw.retro_project_f32(1, 1, 0, 1, 4, 1, 0, None) == lib.RETRO_EINVAL
+    assert raw.retro_project_f32(1, 0, 4, 1, 4, 1, 0, None) == lib.RETRO_OK  # no rows: nothing to do
+    assert raw.retro_project_f32(1, 70000, 4, 1, 4, 1, 1, None) == lib.RETRO_EUNSUPPORTED
