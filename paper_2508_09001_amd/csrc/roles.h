@@ -1406,8 +1406,10 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
       for (int j = 0; j < GS; ++j) {
         const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
         if constexpr (COH && E == 2) {
+          // the row's offset (uniform) as the scalar offset, the lane's as the vector one
           const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(
-              coherent_rsrc(a.o_ws), (uint32_t)((row * D + e0) * sizeof(float)), 0, kCpolSc1);
+              coherent_rsrc(a.o_ws), (uint32_t)(e0 * sizeof(float)),
+              (uint32_t)(row * D * sizeof(float)), kCpolSc1);
           v[r][j][0] = __uint_as_float(w[0]);
           v[r][j][1] = __uint_as_float(w[1]);
         } else {
@@ -1505,13 +1507,36 @@ __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int g
   combine_splits<D, NR, GS, COH, ZPRE>(a, b * g.hk + h, rho, res, zl);
 }
 
+// The output-cache row merge unit `unit` merges its partial with (see
+// merge_unit), or -1 if it has none: row x > 0 of a step whose query exists,
+// and for x = 0 the slot of the row leaving the window.
+__device__ __forceinline__ int64_t unit_cache_row(const MergeArgs& a, int unit) {
+  const Geometry& g = a.g;
+  const int W = g.W;
+  int u = unit;
+  const int x = u % a.xs;
+  u /= a.xs;
+  const int gq = u % g.G;
+  u /= g.G;
+  const int h = u % g.hk, b = u / g.hk;
+  const int qh = h * g.G + gq;
+  if (a.mode == 0 || x == W) return -1;
+  const int tau0 = a.step - W + x;
+  if (tau0 < 0) return -1;
+  const int slot = x > 0 ? tau0 % W : a.step % W;  // (t - W) mod W == t mod W
+  return ((int64_t)b * W + slot) * g.hq + qh;
+}
+
 // One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
 // executed by one wavefront; no barriers inside.  The unit of row 0 also
 // handles the current row W, whose cache slot is the one row 0 leaves.  GS:
 // splits whose loads are in flight together (at most 64).  ZPRE: the splits'
 // log-normalisers of the unit's rows (x, then W for x == 0 < W) are in zl.
-template <int D, int GS, bool COH = false, bool ZPRE = false>
-__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const ZLanes& zl = ZLanes{}) {
+// PRE: `pre` is the row unit_cache_row names, loaded by the caller (it may
+// load it early: no other unit reads or writes it), instead of here.
+template <int D, int GS, bool COH = false, bool ZPRE = false, bool PRE = false>
+__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const ZLanes& zl = ZLanes{},
+                                           Row<D> pre = Row<D>{}) {
   const Geometry& g = a.g;
   const int W = g.W;
   int u = unit;
@@ -1544,7 +1569,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const Z
       return;
     }
     const int64_t ci = ((int64_t)b * W + tau0 % W) * g.hq + qh;
-    const Row<D> cached = get<D>(a.o_cache, a.l_cache, ci);
+    const Row<D> cached = PRE ? pre : get<D>(a.o_cache, a.l_cache, ci);
     Row<D> p[1];
     partials<D, 1, GS, COH, ZPRE>(a, b, h, gq, {x}, p, zl);
     const Row<D> merged = lse_merge<D>(cached, p[0]);
@@ -1556,7 +1581,7 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const Z
   // (t - W) mod W == t mod W.
   const int64_t slot = ((int64_t)b * W + a.step % W) * g.hq + qh;
   Row<D> cached = zero;
-  if (tau0 >= 0) cached = get<D>(a.o_cache, a.l_cache, slot);
+  if (tau0 >= 0) cached = PRE ? pre : get<D>(a.o_cache, a.l_cache, slot);
   Row<D> p[2];
   partials<D, 2, GS, COH, ZPRE>(a, b, h, gq, {0, W}, p, zl);
   const Row<D> merged = tau0 >= 0 ? lse_merge<D>(cached, p[0]) : zero;

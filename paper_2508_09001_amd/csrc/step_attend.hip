@@ -494,13 +494,23 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   // (else the last, after its units)
   const int uw = min(kWaves - 1, (units + nwi - 1) / nwi);
   if (writer && wave >= uw && uw < kWaves - 1) writer_outputs(tid - 64 * uw, kThreads - 64 * uw);
-  for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
+  // the wavefront index as a uniform (scalar) value: every index and row
+  // offset of the units below then stays in scalar registers
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave_s; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
     const int x = kk / g.G, gq = kk - x * g.G;
     const int ul = gq * xs + x;
     const bool two = g.W > 0 && x == 0;  // rows 0 and W
     const uint64_t* t0 = sa.lse_tag + ((size_t)bh * g.R + x * g.G + gq) * n_splits;
     const uint64_t* t1 = sa.lse_tag + ((size_t)bh * g.R + g.W * g.G + gq) * n_splits;
     const bool l0 = lane < n_splits, l1 = two && lane < n_splits;
+    const int unit = (int)bh * units + ul;
+    // the unit's output-cache row, loaded while the tags are awaited (merge_unit
+    // would load it just ahead of the partial rows, and the compiler waits for
+    // it before their loads go out: a second round trip)
+    const int64_t ci = unit_cache_row(m, unit);
+    Row<D> pre{};
+    if (ci >= 0) pre = get<D>(m.o_cache, m.l_cache, ci);  // wavefront-uniform
     uint64_t w0 = l0 ? __hip_atomic_load(t0 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
     uint64_t w1 = l1 ? __hip_atomic_load(t1 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
     bool timed_out = false;
@@ -516,13 +526,12 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       if (l0 && !current(w0)) w0 = __hip_atomic_load(t0 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (l1 && !current(w1)) w1 = __hip_atomic_load(t1 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    const int unit = (int)bh * units + ul;
     if (failed || timed_out || wave_ballot((l0 && broken(w0)) || (l1 && broken(w1))) != 0) {
       poison_unit<D>(m, unit);
       continue;
     }
     const ZLanes zl{{__uint_as_float((uint32_t)w0), __uint_as_float((uint32_t)w1)}};
-    merge_unit<D, 32, true, true>(m, unit, zl);
+    merge_unit<D, 32, true, true, true>(m, unit, zl, pre);
   }
   if (writer && uw == kWaves - 1 && wave == kWaves - 1) writer_outputs(lane, 64);
 
