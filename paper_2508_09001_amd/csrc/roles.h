@@ -319,7 +319,7 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
   using S = ScoreShape<T, D>;
   const int tid = thread_index();
   const int nthreads = NT > 0 ? NT : (int)blockDim.x;
-  const int lane = tid & 63, wave = tid >> 6, nw = nthreads >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = nthreads >> 6;
   const int c = lane % S::LPP;
   // every load before any wait: the group's queries (first: they are staged
   // before the barrier, and loads complete in order), digest rows (in bounds
@@ -870,7 +870,7 @@ __device__ __forceinline__ void attend_role(const AttendArgs& a, int b, int h, i
   const int bh = b * g.hk + h;
   const int nthreads = blockDim.x;
   const int tid = thread_index();
-  const int lane = tid & 63, wave = tid >> 6, nwaves = nthreads >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nwaves = nthreads >> 6;
   const int ln16 = lane & 15, g4 = lane >> 4;
 
   // ---- per-row-tile state -------------------------------------------------

@@ -155,7 +155,9 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   auto kseg = __builtin_amdgcn_kernarg_segment_ptr();
   const StepAttendArgs* sap = nullptr;  // set by tok_of
   const int tid = thread_index();
-  const int wave = tid >> 6, lane = tid & 63;
+  // the wavefront index as a uniform (scalar) value: indices and offsets
+  // derived from it (the merge units' rows) stay in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const uint32_t u = (uint32_t)xcd_remap(blockIdx.x, ngrid);
   const uint32_t bh = u / nw;
   const uint32_t j = u - bh * nw;
@@ -494,10 +496,7 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   // (else the last, after its units)
   const int uw = min(kWaves - 1, (units + nwi - 1) / nwi);
   if (writer && wave >= uw && uw < kWaves - 1) writer_outputs(tid - 64 * uw, kThreads - 64 * uw);
-  // the wavefront index as a uniform (scalar) value: every index and row
-  // offset of the units below then stays in scalar registers
-  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave_s; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
+  for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
     const int x = kk / g.G, gq = kk - x * g.G;
     const int ul = gq * xs + x;
     const bool two = g.W > 0 && x == 0;  // rows 0 and W
