@@ -57,10 +57,10 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
   const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + (threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
   if (failed) {
-    poison_unit<D>(a, u);
+    poison_unit<D>(a, unit_pos(a, u));
     return;
   }
-  merge_unit<D, 32>(a, u);
+  merge_unit<D, 32>(a, unit_pos(a, u));
   if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
     // after the unit's own loads (the two lookups here are dependent): the
     // first wavefront advances every sequence; no other workgroup of this

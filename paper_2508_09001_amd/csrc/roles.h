@@ -1397,19 +1397,24 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
     for (int r = 0; r < NR; ++r) {
       const int64_t base = (int64_t)bh * g.n_splits * g.R + rho[r];
       if constexpr (ZPRE) {
-        const float zs = __shfl(zl.z[r], min(s0 + lane, 63));
+        const float zs = s0 == 0 ? zl.z[r] : __shfl(zl.z[r], min(s0 + lane, 63));
         z[r] = lane < cnt ? zs : -INFINITY;
       } else {
         z[r] = lane < cnt ? get_c<COH>(a.l_ws + base + (int64_t)(s0 + lane) * g.R) : -INFINITY;
       }
+      // COH, E == 2: split s0 + j's row at byte offset o_j = o_0 + j * stride
+      // (uniform: the scalar offset of the load, the lane's part the vector
+      // one), clamped to the group's last split; two scalar operations a row
+      const uint32_t stride = (uint32_t)(g.R * D * sizeof(float));
+      uint32_t o = (uint32_t)((base + (int64_t)s0 * g.R) * D * sizeof(float));
+      const uint32_t o_last = o + (uint32_t)(cnt - 1) * stride;
 #pragma unroll
       for (int j = 0; j < GS; ++j) {
         const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
         if constexpr (COH && E == 2) {
-          // the row's offset (uniform) as the scalar offset, the lane's as the vector one
           const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(
-              coherent_rsrc(a.o_ws), (uint32_t)(e0 * sizeof(float)),
-              (uint32_t)(row * D * sizeof(float)), kCpolSc1);
+              coherent_rsrc(a.o_ws), (uint32_t)(e0 * sizeof(float)), min(o, o_last), kCpolSc1);
+          o += stride;
           v[r][j][0] = __uint_as_float(w[0]);
           v[r][j][1] = __uint_as_float(w[1]);
         } else {
@@ -1507,24 +1512,32 @@ __device__ __forceinline__ void partials(const MergeArgs& a, int b, int h, int g
   combine_splits<D, NR, GS, COH, ZPRE>(a, b * g.hk + h, rho, res, zl);
 }
 
-// The output-cache row merge unit `unit` merges its partial with (see
-// merge_unit), or -1 if it has none: row x > 0 of a step whose query exists,
-// and for x = 0 the slot of the row leaving the window.
-__device__ __forceinline__ int64_t unit_cache_row(const MergeArgs& a, int unit) {
+// Where merge unit `unit` = ((b * h_k + h) * G + gq) * xs + x works: window
+// row x of query head gq of (sequence b, KV head h).
+struct UnitPos {
+  int x, gq, h, b;
+};
+__device__ __forceinline__ UnitPos unit_pos(const MergeArgs& a, int unit) {
   const Geometry& g = a.g;
-  const int W = g.W;
   int u = unit;
   const int x = u % a.xs;
   u /= a.xs;
   const int gq = u % g.G;
   u /= g.G;
-  const int h = u % g.hk, b = u / g.hk;
-  const int qh = h * g.G + gq;
-  if (a.mode == 0 || x == W) return -1;
-  const int tau0 = a.step - W + x;
+  return UnitPos{x, gq, u % g.hk, u / g.hk};
+}
+
+// The output-cache row the merge unit at p merges its partial with (see
+// merge_unit), or -1 if it has none: row x > 0 of a step whose query exists,
+// and for x = 0 the slot of the row leaving the window.
+__device__ __forceinline__ int64_t unit_cache_row(const MergeArgs& a, const UnitPos& p) {
+  const Geometry& g = a.g;
+  const int W = g.W;
+  if (a.mode == 0 || p.x == W) return -1;
+  const int tau0 = a.step - W + p.x;
   if (tau0 < 0) return -1;
-  const int slot = x > 0 ? tau0 % W : a.step % W;  // (t - W) mod W == t mod W
-  return ((int64_t)b * W + slot) * g.hq + qh;
+  const int slot = p.x > 0 ? tau0 % W : a.step % W;  // (t - W) mod W == t mod W
+  return ((int64_t)p.b * W + slot) * g.hq + p.h * g.G + p.gq;
 }
 
 // One work unit of the combine + merge: unit = ((b * h_k + h) * G + gq) * xs + x,
@@ -1535,16 +1548,11 @@ __device__ __forceinline__ int64_t unit_cache_row(const MergeArgs& a, int unit) 
 // PRE: `pre` is the row unit_cache_row names, loaded by the caller (it may
 // load it early: no other unit reads or writes it), instead of here.
 template <int D, int GS, bool COH = false, bool ZPRE = false, bool PRE = false>
-__device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const ZLanes& zl = ZLanes{},
-                                           Row<D> pre = Row<D>{}) {
+__device__ __forceinline__ void merge_unit(const MergeArgs& a, const UnitPos& up,
+                                           const ZLanes& zl = ZLanes{}, Row<D> pre = Row<D>{}) {
   const Geometry& g = a.g;
   const int W = g.W;
-  int u = unit;
-  const int x = u % a.xs;
-  u /= a.xs;
-  const int gq = u % g.G;
-  u /= g.G;
-  const int h = u % g.hk, b = u / g.hk;
+  const int x = up.x, gq = up.gq, h = up.h, b = up.b;
   const int qh = h * g.G + gq;
   const int64_t out_row = (int64_t)b * (W + 1);
 
@@ -1596,14 +1604,9 @@ __device__ __forceinline__ void merge_unit(const MergeArgs& a, int unit, const Z
 // The output rows merge unit `unit` writes, as NaN; nothing else is written
 // (the output cache keeps its rows).
 template <int D>
-__device__ __forceinline__ void poison_unit(const MergeArgs& a, int unit) {
+__device__ __forceinline__ void poison_unit(const MergeArgs& a, const UnitPos& up) {
   const Geometry& g = a.g;
-  int u = unit;
-  const int x = u % a.xs;
-  u /= a.xs;
-  const int gq = u % g.G;
-  u /= g.G;
-  const int h = u % g.hk, b = u / g.hk;
+  const int x = up.x, gq = up.gq, h = up.h, b = up.b;
   const int qh = h * g.G + gq;
   const int64_t out_row = (int64_t)b * (g.W + 1);
   Row<D> p;

@@ -479,8 +479,8 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
     __hip_atomic_store(sa.head_tag + bh, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
-  // ---- 7: combine + merge (merge_unit): unit ul of the head's G * max(W, 1)
-  // goes to workgroup ul % nw, wavefront ul / nw (the publisher last).  A unit
+  // ---- 7: combine + merge (merge_unit): the head's G * max(W, 1) units
+  // (window row x of query head gq), spread over its workgroups.  A unit
   // waits until the tags of its rows carry the epoch in every split, then
   // reads the partial rows device-coherently; a failure anywhere in its inputs
   // makes its output rows NaN and leaves its cache slot as it was.
@@ -498,16 +498,15 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
   if (writer && wave >= uw && uw < kWaves - 1) writer_outputs(tid - 64 * uw, kThreads - 64 * uw);
   for (int kk = ((int)j + nwi - 1) % nwi + nwi * wave; kk < units; kk += nwi * kWaves) {  // wavefront-uniform
     const int x = kk / g.G, gq = kk - x * g.G;
-    const int ul = gq * xs + x;
     const bool two = g.W > 0 && x == 0;  // rows 0 and W
     const uint64_t* t0 = sa.lse_tag + ((size_t)bh * g.R + x * g.G + gq) * n_splits;
     const uint64_t* t1 = sa.lse_tag + ((size_t)bh * g.R + g.W * g.G + gq) * n_splits;
     const bool l0 = lane < n_splits, l1 = two && lane < n_splits;
-    const int unit = (int)bh * units + ul;
+    const UnitPos up{x, gq, h, b};  // merge unit (bh * G + gq) * xs + x
     // the unit's output-cache row, loaded while the tags are awaited (merge_unit
     // would load it just ahead of the partial rows, and the compiler waits for
     // it before their loads go out: a second round trip)
-    const int64_t ci = unit_cache_row(m, unit);
+    const int64_t ci = unit_cache_row(m, up);
     Row<D> pre{};
     if (ci >= 0) pre = get<D>(m.o_cache, m.l_cache, ci);  // wavefront-uniform
     uint64_t w0 = l0 ? __hip_atomic_load(t0 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
@@ -526,11 +525,11 @@ __global__ void __launch_bounds__(kThreads) step_attend_kernel(
       if (l1 && !current(w1)) w1 = __hip_atomic_load(t1 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     if (failed || timed_out || wave_ballot((l0 && broken(w0)) || (l1 && broken(w1))) != 0) {
-      poison_unit<D>(m, unit);
+      poison_unit<D>(m, up);
       continue;
     }
     const ZLanes zl{{__uint_as_float((uint32_t)w0), __uint_as_float((uint32_t)w1)}};
-    merge_unit<D, 32, true, true, true>(m, unit, zl, pre);
+    merge_unit<D, 32, true, true, true>(m, up, zl, pre);
   }
   if (writer && uw == kWaves - 1 && wave == kWaves - 1) writer_outputs(lane, 64);
 
