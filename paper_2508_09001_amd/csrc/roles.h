@@ -302,6 +302,8 @@ __device__ __forceinline__ StepToken<T> make_step_token(const Geometry& g, int b
 // The token and the number of pages of the sequence come from `tok_of(n_pages)`
 // (returns the StepToken, sets n_pages), called once the digest and query loads
 // are issued: its own loads (sequence length, page table) then overlap them.
+// sq: 2 * G * D floats of LDS, where the group's queries are staged as
+// max(q, 0) (first G * D) and min(q, 0) (the rest).
 // `pre_barrier()` runs in every thread just before the barrier that publishes
 // the staged queries to the workgroup; `publish(page, score)` hands each score
 // of a page below n_pages on (called by one lane per page).  NT > 0: the
@@ -368,8 +370,12 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
       float f[QV];
       words_to_f32<T, 4>(w, f);
 #pragma unroll
-      for (int i = 0; i < QV; i += 4)
-        *reinterpret_cast<float4*>(sq + e + i) = make_float4(f[i], f[i + 1], f[i + 2], f[i + 3]);
+      for (int i = 0; i < QV; i += 4) {
+        *reinterpret_cast<float4*>(sq + e + i) =
+            make_float4(fmaxf(f[i], 0.f), fmaxf(f[i + 1], 0.f), fmaxf(f[i + 2], 0.f), fmaxf(f[i + 3], 0.f));
+        *reinterpret_cast<float4*>(sq + gd + e + i) =
+            make_float4(fminf(f[i], 0.f), fminf(f[i + 1], 0.f), fminf(f[i + 2], 0.f), fminf(f[i + 3], 0.f));
+      }
     }
   }
   pre_barrier();
@@ -413,12 +419,15 @@ __device__ __forceinline__ void score_role(const Geometry& g, int page0, int pag
 #pragma unroll
       for (int v = 0; v < S::VEC; ++v) {
         // max(q*lo, q*hi) is the product with hi for q >= 0 and with lo for
-        // q < 0 (lo <= hi, and rounding is monotone): one product instead of
-        // two.  Only a zero term's sign can differ (q < 0, lo = -0, hi = +0),
+        // q < 0 (lo <= hi, and rounding is monotone).  With q+ = max(q, 0)
+        // and q- = min(q, 0) staged apart, that is fma(q-, lo, q+ * hi): one
+        // of the two products is a zero, so the fma rounds the other one once,
+        // as the plain product does.  Only a zero term's sign can differ,
         // which changes no sum with a nonzero term and is cleared by the
         // final + 0.0f otherwise, so the score is the same bit for bit.
-        const float qv = sq[gq * D + c * S::VEC + v];
-        t[v] = qv * (qv >= 0.f ? hi[v] : lo[v]);
+        const float qp = sq[gq * D + c * S::VEC + v];
+        const float qn = sq[gd + gq * D + c * S::VEC + v];
+        t[v] = __builtin_fmaf(qn, lo[v], qp * hi[v]);
       }
 #pragma unroll
       for (int w = 1; w < S::VEC; w *= 2)

@@ -158,7 +158,7 @@ hipError_t score_t(const Geometry& g, int step, const void* q, int64_t qbs,
                    const SelectArgs& sa, hipStream_t s) {
   if (sa.ppb < 1 || sa.ppb > score_pages_per_block(PER) || sa.nbh < 1) return hipErrorInvalidValue;
   dim3 grid(sa.nbh, g.hk, g.batch);
-  size_t lds = sizeof(float) * g.G * D;
+  size_t lds = sizeof(float) * 2 * g.G * D;  // the queries' q+ and q- halves
   if (PER > 0) lds = std::max(lds, sizeof(int32_t) * (kTopkHistWords + kTopkSmall));
   const TokenArgs ta{k_new, v_new, c.k_cache, c.v_cache, c.page_table};
   score_kernel<T, D, PER><<<grid, score_threads(PER), lds, s>>>(g, (const T*)q, qbs, (T*)c.digest, c.seq_lens,

@@ -104,7 +104,7 @@ struct StepLds {
     T stage[2 * Tiles<T, D>::BUF_ELEMS];
     ThrLds<PER, kWaves> thr;
   } u;
-  float sq[16 * D];               // the group's current queries (fp32) while scoring
+  float sq[2 * 16 * D];           // the group's current queries (fp32, q+ then q-) while scoring
   float share[SITERS * kWaves * 4];  // this workgroup's scores
   T dig[2 * D];                   // the token page's widened digest row
   int s_phys[kMaxSplitPages], s_len[kMaxSplitPages], s_mask[kMaxSplitPages];
