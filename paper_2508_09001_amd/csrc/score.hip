@@ -27,10 +27,13 @@ namespace {
 // workgroups as fit on the chip at once (one sixteen-wavefront workgroup per
 // compute unit), since a workgroup that waits for a free unit starts about
 // 1.3 us after one ends (and would hold up its head's selection); a wavefront
-// with no page in the second pass skips it.  (Without the epilogue this is
-// also 0.16 us per step faster than four-wavefront workgroups of 16 pages.)
-constexpr int score_threads(int) { return 1024; }
-constexpr int score_iters(int) { return 2; }
+// with no page in the second pass skips it.  Without the epilogue (PER == 0:
+// the selection runs in the attention launch), eight wavefronts of up to four
+// passes (the same 128 pages, more loads in flight per wavefront, two more
+// workgroups per compute unit): 70.2 against 71.5 us per layer-step at batch
+// 16, 144.9 against 146.6 at the batch-4 long-generation workload.
+constexpr int score_threads(int per) { return per == 0 ? 512 : 1024; }
+constexpr int score_iters(int per) { return per == 0 ? 4 : 2; }
 // most pages a workgroup scores
 constexpr int score_pages_per_block(int per) { return score_threads(per) / 64 * 4 * score_iters(per); }
 
@@ -207,8 +210,11 @@ hipError_t launch_score(const Geometry& g, int step, const void* q_cur, int64_t 
     select_split(g, &sa.nbh, &sa.ppb);
     // one counter per head up to 32 workgroups, else groups of at least 16
     sa.group = sa.nbh <= 32 ? sa.nbh : std::max(16, (sa.nbh + kSelMaxGroups - 1) / kSelMaxGroups);
-  } else {
-    select_split(g, &sa.nbh, &sa.ppb);
+  } else {  // the shape without the selection epilogue: no co-residency to aim for
+    const int ppb_max = score_pages_per_block(0);
+    const int n = (g.max_pages + ppb_max - 1) / ppb_max;
+    sa.ppb = (g.max_pages + n - 1) / n;
+    sa.nbh = (g.max_pages + sa.ppb - 1) / sa.ppb;
   }
   if (g.dtype == RETRO_BF16)
     return g.D == 128 ? score_d<bf16_t, 128>(g, step, q_cur, q_batch_stride, c, k_new, v_new, scores, sa, s)
