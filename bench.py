@@ -113,7 +113,7 @@ def algorithmic_bytes(spec, seq_lens, num_selected):
     ring = 2 * b * W * hq * (d + 1) * 4
     out = b * (W + 1) * hq * (d + 1) * 4
     mask = 12 * k_sum
-    append = b * hk * d * elt * 2 + b * hk * 2 * d * elt * 2
+    append = spec.tokens_per_step * (b * hk * d * elt * 2 + b * hk * 2 * d * elt * 2)
     # what the selection reads besides the scores: last_loaded per (b, h), the page table per b
     select_reads = (n_pages * hk * 4 + n_pages * 4) // f
     return dict(total=digest + gather + queries + ring + out + mask + append, digest=digest,
@@ -205,8 +205,8 @@ def main():
         for lay in layers:
             if upd is not None and t > 0:
                 lay.update_kv(*upd[t % len(upd)])
-            for j in range(k_new.shape[0] - 1):
-                lay.append(t, k_new[j], v_new[j])
+            if k_new.shape[0] > 1:  # the step's tokens before its last, in one launch
+                lay.append_tokens(t, k_new[:-1], v_new[:-1])
             lay.step(t, win, k_new[-1], v_new[-1])
 
     for t in range(args.warmup):

@@ -197,6 +197,21 @@ retro_status retro_prefill_kv(const retro_dims* dims, const retro_kv_cache* cach
 retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_kv_cache* cache,
                              const void* k_new, const void* v_new, void* stream);
 
+/* AppendKV (Alg. 1) of n_tokens tokens per sequence in order, with the result of
+ * n_tokens calls of retro_append_kv (token j of sequence b at position
+ * seq_lens[b] + j, digests widened, last_loaded of every page receiving a key set
+ * to step-1 for every head), in one launch per 64 tokens: for steps that add
+ * several tokens (e.g. the tokens before the last of a multi-token step, whose
+ * last token goes through retro_step).  k_new / v_new [n_tokens][batch][h_k][d]
+ * (dtype), device memory, read only.  The first token whose logical page is not
+ * mapped (page_table entry < 0 or >= num_phys_pages, or position >= max_pages*P)
+ * is dropped with every later token of the call, and seq_lens[b] advances by
+ * the number appended.  n_tokens = 0 does nothing; n_tokens < 0 or a null
+ * k_new / v_new (n_tokens > 0) is RETRO_EINVAL. */
+retro_status retro_append_kv_tokens(const retro_dims* dims, int32_t step,
+                                    const retro_kv_cache* cache, int32_t n_tokens,
+                                    const void* k_new, const void* v_new, void* stream);
+
 /* UpdateKV (Alg. 1; Sec. 3.3, retrospective KV cache update): the keys and values
  * of the n_tokens most recent stored tokens of every sequence b (positions
  * seq_lens[b] - n_tokens .. seq_lens[b] - 1; those below 0 are skipped) are

@@ -21,7 +21,8 @@ RETRO_F32, RETRO_BF16 = 0, 1
 RETRO_FLAG_SEPARATE_SCORES, RETRO_FLAG_SELECT_IN_SCORES, RETRO_FLAG_TEST_WAIT_TIMEOUT = 1, 2, 4
 
 EXPORTED = ("retro_version", "retro_status_string", "retro_k_max", "retro_workspace_size",
-            "retro_prefill_kv", "retro_append_kv", "retro_update_kv", "retro_select_pages",
+            "retro_prefill_kv", "retro_append_kv", "retro_append_kv_tokens", "retro_update_kv",
+            "retro_select_pages",
             "retro_decode_attend", "retro_decode_attend_partials", "retro_step_attend_partials",
             "retro_copy_scores", "retro_merge_output_cache", "retro_step", "retro_step_noalloc",
             "retro_step_launches", "retro_pack_weight", "retro_project_qkv",
@@ -81,6 +82,7 @@ def load_library(path: str = LIB_PATH):
         "retro_workspace_size": ([D, C.POINTER(C.c_size_t)], C.c_int),
         "retro_prefill_kv": ([D, C.POINTER(KVCache), i32, i32, i32, P, P, P], C.c_int),
         "retro_append_kv": ([D, i32, C.POINTER(KVCache), P, P, P], C.c_int),
+        "retro_append_kv_tokens": ([D, i32, C.POINTER(KVCache), i32, P, P, P], C.c_int),
         "retro_update_kv": ([D, C.POINTER(KVCache), i32, P, P, P], C.c_int),
         "retro_select_pages": ([D, i32, P, C.POINTER(KVCache), C.POINTER(Selection), P,
                                 C.c_size_t, P], C.c_int),
@@ -164,6 +166,13 @@ def retro_prefill_kv(dims: Dims, cache: KVCache, seq: int, start_pos: int, n_tok
 def retro_append_kv(dims: Dims, step: int, cache: KVCache, k_new, v_new, stream=None) -> None:
     _check(load_library().retro_append_kv(C.byref(dims), step, C.byref(cache), _ptr(k_new),
                                           _ptr(v_new), _stream(stream)), "retro_append_kv")
+
+
+def retro_append_kv_tokens(dims: Dims, step: int, cache: KVCache, n_tokens: int, k_new, v_new,
+                           stream=None) -> None:
+    _check(load_library().retro_append_kv_tokens(C.byref(dims), step, C.byref(cache), n_tokens,
+                                                 _ptr(k_new), _ptr(v_new), _stream(stream)),
+           "retro_append_kv_tokens")
 
 
 def retro_update_kv(dims: Dims, cache: KVCache, n_tokens: int, k_upd, v_upd, stream=None) -> None:

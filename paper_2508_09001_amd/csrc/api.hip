@@ -227,6 +227,19 @@ retro_status retro_append_kv(const retro_dims* dims, int32_t step, const retro_k
   return from_hip(retro::launch_append(g, step, *cache, k_new, v_new, (hipStream_t)stream));
 }
 
+retro_status retro_append_kv_tokens(const retro_dims* dims, int32_t step,
+                                    const retro_kv_cache* cache, int32_t n_tokens,
+                                    const void* k_new, const void* v_new, void* stream) {
+  Geometry g;
+  retro_status st = prepare(dims, step, &g);
+  if (st != RETRO_OK) return st;
+  if (!cache_ok(cache) || n_tokens < 0) return RETRO_EINVAL;
+  if (n_tokens == 0) return RETRO_OK;
+  if (!k_new || !v_new) return RETRO_EINVAL;
+  return from_hip(retro::launch_append_tokens(g, step, *cache, n_tokens, k_new, v_new,
+                                              (hipStream_t)stream));
+}
+
 retro_status retro_update_kv(const retro_dims* dims, const retro_kv_cache* cache,
                              int32_t n_tokens, const void* k_upd, const void* v_upd,
                              void* stream) {

@@ -81,6 +81,9 @@ int attend_min_waves(int dtype, int D);
 // ---- launchers (return hipSuccess or the launch error) ----
 hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, const void* k_new,
                          const void* v_new, hipStream_t s);
+// n_tok tokens per sequence, k_new / v_new [n_tok][batch][h_k][d], in order
+hipError_t launch_append_tokens(const Geometry& g, int step, const retro_kv_cache& c, int n_tok,
+                                const void* k_new, const void* v_new, hipStream_t s);
 hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
                           const void* k_src, const void* v_src, hipStream_t s);
 // UpdateKV: the n most recent stored tokens of every sequence get new keys and

@@ -1,6 +1,8 @@
 // KV storage: AppendKV (Alg. 1) and bulk prefill, keeping the Quest page digests
 // (element-wise key min / max of each page, Sec. 2.1) and, on append, the
 // retrospective-mask override of Alg. 2's current-page rule.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace retro {
@@ -70,6 +72,100 @@ __global__ void __launch_bounds__(256) append_kernel(Geometry g, int step, T* __
       A[((int64_t)b * g.hk + h) * g.max_pages + lp] = step - 1;
   __syncthreads();
   if (ok && threadIdx.x == 0) seq_lens[b] = pos + 1;
+}
+
+// Several tokens per sequence in one launch (AppendKV of Alg. 1 applied to
+// tokens 0, 1, ..., n_tok - 1 in order, as n_tok calls of the one-token append
+// would): token j goes to position seq_lens[b] + j.  One workgroup per
+// sequence, one thread per (KV head, element) of a token.  The page-table
+// entries of the pages the call touches are read once, in parallel, into LDS;
+// the first token whose page is not mapped (or lies past max_pages) is dropped
+// and so is every token after it (each would target the same position), as
+// with the one-token append.  Each thread reads the keys and values of up to
+// kChunk tokens before storing any, and the stored digest of the first page
+// (whose first new slot may be past 0) alongside.
+constexpr int kAppendMaxTokens = 64;   // tokens per launch (the host splits longer calls)
+constexpr int kAppendThreads = 1024;
+
+template <typename T>
+__global__ void __launch_bounds__(kAppendThreads) append_tokens_kernel(
+    Geometry g, int step, int n_tok, T* __restrict__ kc, T* __restrict__ vc, T* __restrict__ dg,
+    const int32_t* __restrict__ pt, int32_t* __restrict__ seq_lens, int32_t* __restrict__ A,
+    const T* __restrict__ k_new, const T* __restrict__ v_new) {
+  constexpr int kChunk = 8;
+  __shared__ int s_phys[kAppendMaxTokens + 1];
+  __shared__ int s_nok;
+  const int b = blockIdx.x;
+  const int n = g.hk * g.D;
+  const int pos0 = seq_lens[b];
+  const int lp0 = pos0 >= 0 ? pos0 / g.P : 0;
+  const int npages = pos0 >= 0 ? (pos0 + n_tok - 1) / g.P - lp0 + 1 : 0;
+  if (threadIdx.x == 0) s_nok = pos0 >= 0 ? n_tok : 0;
+  __syncthreads();
+  if ((int)threadIdx.x < npages) {
+    const int lp = lp0 + (int)threadIdx.x;
+    const int ph = lp < g.max_pages ? pt[(int64_t)b * g.max_pages + lp] : -1;
+    const bool ok = ph >= 0 && ph < g.num_phys;
+    s_phys[threadIdx.x] = ok ? ph : -1;
+    if (!ok) atomicMin(&s_nok, max(lp * g.P - pos0, 0));
+  }
+  __syncthreads();
+  const int n_ok = s_nok;
+  const int slot0 = pos0 - lp0 * g.P;
+  for (int e = threadIdx.x; e < n && n_ok > 0; e += blockDim.x) {
+    const int h = e / g.D, i = e - h * g.D;
+    T* d = dg + ((((int64_t)b * g.hk + h) * g.max_pages + lp0) * 2) * g.D + i;
+    T lo{}, hi{};
+    if (slot0 != 0) {  // the first page already holds keys: widen its digest
+      lo = d[0];
+      hi = d[g.D];
+    }
+    int lp_cur = lp0;
+    for (int j0 = 0; j0 < n_ok; j0 += kChunk) {
+      T kv[kChunk], vv[kChunk];
+#pragma unroll
+      for (int jj = 0; jj < kChunk; ++jj) {
+        const int j = min(j0 + jj, n_ok - 1);
+        const int64_t src = ((int64_t)j * g.batch + b) * n + e;  // [token][batch][h_k][d]
+        kv[jj] = k_new[src];
+        vv[jj] = v_new[src];
+      }
+#pragma unroll
+      for (int jj = 0; jj < kChunk; ++jj) {
+        const int j = j0 + jj;
+        if (j >= n_ok) break;
+        const int pos = pos0 + j, lp = pos / g.P, slot = pos - lp * g.P;
+        if (lp != lp_cur) {  // the previous page is complete: its digest goes out
+          d[0] = lo;
+          d[g.D] = hi;
+          lp_cur = lp;
+          d = dg + ((((int64_t)b * g.hk + h) * g.max_pages + lp) * 2) * g.D + i;
+        }
+        const int64_t ph = (int64_t)s_phys[lp - lp0] * g.hk + h;
+        kc[(ph * g.P + slot) * g.D + i] = kv[jj];
+        vc[(ph * g.D + i) * g.P + slot] = vv[jj];
+        if (slot == 0) {
+          lo = kv[jj];
+          hi = kv[jj];
+        } else {
+          if (less(kv[jj], lo)) lo = kv[jj];
+          if (less(hi, kv[jj])) hi = kv[jj];
+        }
+      }
+    }
+    d[0] = lo;
+    d[g.D] = hi;
+  }
+  // Alg. 2's current-page rule for every page that received a key, every head
+  if (n_ok > 0) {
+    const int nlp = (pos0 + n_ok - 1) / g.P - lp0 + 1;
+    for (int x = threadIdx.x; x < nlp * g.hk; x += blockDim.x) {
+      const int h = x % g.hk, lp = lp0 + x / g.hk;
+      A[((int64_t)b * g.hk + h) * g.max_pages + lp] = step - 1;
+    }
+  }
+  __syncthreads();  // every thread has read seq_lens[b]
+  if (n_ok > 0 && threadIdx.x == 0) seq_lens[b] = pos0 + n_ok;
 }
 
 // Prefill, pass 1: one workgroup per token copies its keys (token-major page) and
@@ -212,6 +308,21 @@ hipError_t append_t(const Geometry& g, int step, const retro_kv_cache& c, const 
 }
 
 template <typename T>
+hipError_t append_tokens_t(const Geometry& g, int step, const retro_kv_cache& c, int n_tok,
+                           const void* k_new, const void* v_new, hipStream_t s) {
+  const size_t tok_elems = (size_t)g.batch * g.hk * g.D;
+  for (int j0 = 0; j0 < n_tok; j0 += kAppendMaxTokens) {
+    const int nt = std::min(kAppendMaxTokens, n_tok - j0);
+    append_tokens_kernel<T><<<g.batch, kAppendThreads, 0, s>>>(
+        g, step, nt, (T*)c.k_cache, (T*)c.v_cache, (T*)c.digest, c.page_table, c.seq_lens,
+        c.last_loaded, (const T*)k_new + j0 * tok_elems, (const T*)v_new + j0 * tok_elems);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <typename T>
 hipError_t prefill_t(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,
                      const void* k_src, const void* v_src, hipStream_t s) {
   if (n <= 0) return hipSuccess;
@@ -234,6 +345,12 @@ hipError_t launch_append(const Geometry& g, int step, const retro_kv_cache& c, c
                          const void* v_new, hipStream_t s) {
   return g.dtype == RETRO_BF16 ? append_t<bf16_t>(g, step, c, k_new, v_new, s)
                                : append_t<float>(g, step, c, k_new, v_new, s);
+}
+
+hipError_t launch_append_tokens(const Geometry& g, int step, const retro_kv_cache& c, int n_tok,
+                                const void* k_new, const void* v_new, hipStream_t s) {
+  return g.dtype == RETRO_BF16 ? append_tokens_t<bf16_t>(g, step, c, n_tok, k_new, v_new, s)
+                               : append_tokens_t<float>(g, step, c, n_tok, k_new, v_new, s);
 }
 
 hipError_t launch_prefill(const Geometry& g, const retro_kv_cache& c, int seq, int start, int n,

@@ -98,6 +98,15 @@ class RetroLayer:
         B.retro_append_kv(self.dims, step, self.cache, k_new, v_new, stream)
         for b in range(self.batch):
             self._lens[b] += 1
+
+    def append_tokens(self, step: int, k_new, v_new, stream=None) -> None:
+        """Several tokens per sequence in one call: k_new / v_new [n][batch][h_k][d]."""
+        k_new, v_new = self._dev(k_new), self._dev(v_new)
+        n = int(k_new.shape[0])
+        B.retro_append_kv_tokens(self.dims, step, self.cache, n, k_new, v_new, stream)
+        for b in range(self.batch):
+            self._lens[b] += n
+        self._keep_append = (k_new, v_new)
         self._keep = (k_new, v_new)
 
     def select(self, step: int, q_cur, stream=None) -> None:

@@ -116,7 +116,7 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
                check_outputs_from: int = 0, tol: Optional[float] = None, label: str = "",
                update_kv: bool = False, flags: int = 0,
                pool_pages: Optional[int] = None,
-               page_table: Optional[np.ndarray] = None) -> Stats:
+               page_table: Optional[np.ndarray] = None, multi_append: bool = False) -> Stats:
     """Run `steps` decode steps on GPU and oracle; compare every step's selection,
     mask and A exactly, and the outputs of the steps >= check_outputs_from (the
     oracle runs attention only from check_outputs_from - W on, which is enough
@@ -126,7 +126,7 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
     print(f"[parity] {label or spec.name}: batch={spec.batch} hk={spec.num_kv_heads} "
           f"G={spec.group} d={spec.head_dim} P={spec.page_size} B={spec.budget} W={spec.window} "
           f"steps={steps} tps={spec.tokens_per_step} perm={page_perm_seed} split={split_calls} "
-          f"update_kv={update_kv} flags={flags} pool={pool_pages}",
+          f"update_kv={update_kv} flags={flags} pool={pool_pages} multi_append={multi_append}",
           flush=True)
     gen = W.Generator(spec)
     orc = oracle.Oracle.for_spec(spec)
@@ -150,8 +150,11 @@ def run_parity(spec, steps: int, *, page_perm_seed: Optional[int] = None, split_
         ref = orc.step(t, k_new, v_new, win, attend=t >= attend_from)
         ref["A"] = orc.A
         T = k_new.shape[0]
-        for j in range(T - 1):
-            layer.append(t, k_new[j], v_new[j])
+        if multi_append and T > 1:  # the tokens before the last in one call
+            layer.append_tokens(t, k_new[:-1], v_new[:-1])
+        else:
+            for j in range(T - 1):
+                layer.append(t, k_new[j], v_new[j])
         if split_calls:
             layer.append(t, k_new[-1], v_new[-1])
             layer.select(t, win[:, -1])

@@ -120,3 +120,16 @@ def test_project_f32_arguments_checked_on_the_host(lib):
     assert raw.retro_project_f32(1, 1, 0, 1, 4, 1, 0, None) == lib.RETRO_EINVAL
     assert raw.retro_project_f32(1, 0, 4, 1, 4, 1, 0, None) == lib.RETRO_OK  # no rows: nothing to do
     assert raw.retro_project_f32(1, 70000, 4, 1, 4, 1, 1, None) == lib.RETRO_EUNSUPPORTED
+
+
+def test_append_tokens_arguments_checked_on_the_host(lib):
+    d = _dims(lib)
+    cache = lib.KVCache(1, 1, 1, 1, 1, 1)
+    raw = lib.load_library()
+    assert raw.retro_append_kv_tokens(C.byref(d), -1, C.byref(cache), 2, 1, 1, None) == lib.RETRO_EINVAL
+    assert raw.retro_append_kv_tokens(C.byref(d), 0, C.byref(cache), -1, 1, 1, None) == lib.RETRO_EINVAL
+    assert raw.retro_append_kv_tokens(C.byref(d), 0, C.byref(cache), 2, None, 1, None) == lib.RETRO_EINVAL
+    bad = lib.KVCache(1, 1, None, 1, 1, 1)
+    assert raw.retro_append_kv_tokens(C.byref(d), 0, C.byref(bad), 2, 1, 1, None) == lib.RETRO_EINVAL
+    # no tokens: nothing to do, no launch
+    assert raw.retro_append_kv_tokens(C.byref(d), 0, C.byref(cache), 0, None, None, None) == lib.RETRO_OK
