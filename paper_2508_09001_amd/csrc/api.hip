@@ -73,6 +73,9 @@ retro_status make_geometry(const retro_dims* d, Geometry* g) {
   x.n_splits = (x.chunks_max + x.chunks_per_split - 1) / x.chunks_per_split;
   x.pages_per_split = x.chunks_per_split * x.chunk_pages;
   if (x.n_splits > 65535) return RETRO_EUNSUPPORTED;
+  // one KV head's split partials are read through a 2 GiB buffer window
+  if ((int64_t)x.n_splits * x.R * x.D * (int64_t)sizeof(float) >= (int64_t)1 << 31)
+    return RETRO_EUNSUPPORTED;
 
   x.row_tiles = (x.R + 15) / 16;
   x.n_rgroups = (x.row_tiles + kMaxWaves * kMaxRtw - 1) / (kMaxWaves * kMaxRtw);

@@ -54,7 +54,9 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
     if (bh < g.batch * g.hk && !failed) update_last_loaded(a, bh);
     return;
   }
-  const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + (threadIdx.x >> 6);
+  // the wavefront index as a uniform value: the unit's indices and row offsets
+  // then stay in scalar registers
+  const int u = xcd_remap(blockIdx.x, mblocks) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (u >= nunits) return;  // uniform per wavefront; no barrier follows
   if (failed) {
     poison_unit<D>(a, unit_pos(a, u));

@@ -1411,18 +1411,22 @@ __device__ __forceinline__ void combine_splits(const MergeArgs& a, int bh, const
       } else {
         z[r] = lane < cnt ? get_c<COH>(a.l_ws + base + (int64_t)(s0 + lane) * g.R) : -INFINITY;
       }
-      // COH, E == 2: split s0 + j's row at byte offset o_j = o_0 + j * stride
-      // (uniform: the scalar offset of the load, the lane's part the vector
-      // one), clamped to the group's last split; two scalar operations a row
+      // E == 2: split s0 + j's row at byte offset o_j = o_0 + j * stride in
+      // the head's block of partial rows (uniform: the scalar offset of the
+      // load, the lane's part the vector one), clamped to the group's last
+      // split; two scalar operations a row.  The host keeps a head's block
+      // below 2 GiB.
+      const float* hblk = a.o_ws + (int64_t)bh * g.n_splits * g.R * D;
       const uint32_t stride = (uint32_t)(g.R * D * sizeof(float));
-      uint32_t o = (uint32_t)((base + (int64_t)s0 * g.R) * D * sizeof(float));
+      uint32_t o = (uint32_t)(((int64_t)s0 * g.R + rho[r]) * D * sizeof(float));
       const uint32_t o_last = o + (uint32_t)(cnt - 1) * stride;
 #pragma unroll
       for (int j = 0; j < GS; ++j) {
         const int64_t row = base + (int64_t)(s0 + min(j, cnt - 1)) * g.R;
-        if constexpr (COH && E == 2) {
+        if constexpr (E == 2) {
           const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(
-              coherent_rsrc(a.o_ws), (uint32_t)(e0 * sizeof(float)), min(o, o_last), kCpolSc1);
+              coherent_rsrc(hblk), (uint32_t)(e0 * sizeof(float)), min(o, o_last),
+              COH ? kCpolSc1 : 0);
           o += stride;
           v[r][j][0] = __uint_as_float(w[0]);
           v[r][j][1] = __uint_as_float(w[1]);
