@@ -35,7 +35,9 @@ __device__ __forceinline__ void update_last_loaded(const MergeArgs& a, int bh) {
   if (lane == 0 && tok >= 0 && tok < g.max_pages) arow[tok] = a.step - 1;
 }
 
-template <int D>
+// GS: splits whose rows are loaded and folded in together, the smallest power
+// of two (at most 32) covering the launch's splits
+template <int D, int GS>
 __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a) {
   // units ordered (sequence, KV head, query head of the group, row slot), spread
   // so that a KV head's units share the XCD its attention splits ran on
@@ -62,7 +64,7 @@ __global__ void __launch_bounds__(64 * kWaves) combine_merge_kernel(MergeArgs a)
     poison_unit<D>(a, unit_pos(a, u));
     return;
   }
-  merge_unit<D, 32>(a, unit_pos(a, u));
+  merge_unit<D, GS>(a, unit_pos(a, u));
   if (blockIdx.x == 0 && threadIdx.x < 64 && g.token_pending && a.seq_lens) {
     // after the unit's own loads (the two lookups here are dependent): the
     // first wavefront advances every sequence; no other workgroup of this
@@ -129,10 +131,20 @@ hipError_t launch_combine_merge(const Geometry& g, int step, int mode, const flo
   }
   const int64_t units = (int64_t)g.batch * g.hq * a.xs;
   const unsigned blocks = (unsigned)((units + kWaves - 1) / kWaves + upd_blocks);
-  if (g.D == 128)
-    combine_merge_kernel<128><<<blocks, 64 * kWaves, 0, s>>>(a);
-  else
-    combine_merge_kernel<64><<<blocks, 64 * kWaves, 0, s>>>(a);
+  const int ns = g.n_splits;
+  if (g.D == 128) {
+    if (ns <= 2) combine_merge_kernel<128, 2><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 4) combine_merge_kernel<128, 4><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 8) combine_merge_kernel<128, 8><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 16) combine_merge_kernel<128, 16><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else combine_merge_kernel<128, 32><<<blocks, 64 * kWaves, 0, s>>>(a);
+  } else {
+    if (ns <= 2) combine_merge_kernel<64, 2><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 4) combine_merge_kernel<64, 4><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 8) combine_merge_kernel<64, 8><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else if (ns <= 16) combine_merge_kernel<64, 16><<<blocks, 64 * kWaves, 0, s>>>(a);
+    else combine_merge_kernel<64, 32><<<blocks, 64 * kWaves, 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 
