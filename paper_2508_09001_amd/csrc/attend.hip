@@ -212,6 +212,8 @@ hipError_t attend_select_d(const AttendArgs& a, const TopkArgs& ta, int32_t* tok
   const int mp = a.g.max_pages;
   if (mp <= 2 * kAttendThreads) return attend_select_p<T, D, 2>(a, ta, tok_out, s);
   if (mp <= 5 * kAttendThreads) return attend_select_p<T, D, 5>(a, ta, tok_out, s);
+  if (mp <= 6 * kAttendThreads) return attend_select_p<T, D, 6>(a, ta, tok_out, s);
+  if (mp <= 9 * kAttendThreads) return attend_select_p<T, D, 9>(a, ta, tok_out, s);
   return attend_select_p<T, D, 12>(a, ta, tok_out, s);
 }
 
