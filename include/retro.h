@@ -324,9 +324,10 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
  * at once, for tests of that path).
  * Otherwise, or with RETRO_FLAG_SEPARATE_SCORES, three launches: the scores
  * (with the append), then attention with every attention workgroup selecting
- * in front of it, then combine + merge; with RETRO_FLAG_SELECT_IN_SCORES, or
- * for max_pages > 6144, the selection runs at the end of the score launch (or
- * in a launch of its own) instead.  Steps that keep an earlier selection (top-k
+ * in front of it, then combine + merge; with RETRO_FLAG_SELECT_IN_SCORES, when
+ * the attention launch has 64 or more workgroups per KV head (each of which
+ * would repeat the selection), or for max_pages > 6144, the selection runs at
+ * the end of the score launch (or in a launch of its own) instead.  Steps that keep an earlier selection (top-k
  * reuse, retro_dims.reuse_interval) run the append, Alg. 2 on the kept rows,
  * attention and combine + merge as four launches. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,

@@ -354,6 +354,21 @@ retro_status retro_step_attend_partials(const retro_dims* dims, int32_t step,
                                               (char*)workspace + g.ws_dummy, (hipStream_t)stream));
 }
 
+namespace {
+// Attention workgroups per KV head from which the selection runs once per head
+// at the end of the score launch instead of in front of every attention
+// workgroup, which repeats it once per workgroup.  Measured per layer-step:
+// 64 per head (131K-token tables, W = 64: 32 splits x 2 row groups) 50.2 us
+// in the score launch vs 52.4 in the attention launch; 16 per head (the
+// long-generation workload) 115.2 vs 111.4; 2 per head (batch 16) 77.4 vs 63.8.
+constexpr int kSelectInScoresFrom = 64;
+
+bool select_in_attention(const Geometry& gp) {
+  if (!retro::attend_selects(gp) || (gp.flags & RETRO_FLAG_SELECT_IN_SCORES)) return false;
+  return !(retro::score_selects(gp) && gp.n_splits * gp.n_rgroups >= kSelectInScoresFrom);
+}
+}  // namespace
+
 retro_status retro_step_launches(const retro_dims* dims, int32_t* launches) {
   Geometry g;
   if (!launches) return RETRO_EINVAL;
@@ -363,7 +378,7 @@ retro_status retro_step_launches(const retro_dims* dims, int32_t* launches) {
   gp.token_pending = 1;
   if (one_launch(gp)) {
     *launches = 1;
-  } else if (retro::attend_selects(gp) && !(g.flags & RETRO_FLAG_SELECT_IN_SCORES)) {
+  } else if (select_in_attention(gp)) {
     *launches = 3;
   } else {
     *launches = retro::score_selects(gp) ? 3 : 4;
@@ -445,7 +460,7 @@ retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_wind
                                               workspace, o_ws, l_ws, tok, err, wait_limit(g),
                                               wait_bias(g), ocache, o_out, lse_out, s));
   }
-  if (retro::attend_selects(gp) && !(g.flags & RETRO_FLAG_SELECT_IN_SCORES)) {
+  if (select_in_attention(gp)) {
     // score (+ the token's append) -> attention with the selection in front ->
     // combine + merge (+ last_loaded update, + seq_lens advance)
     hipError_t e = retro::launch_score(gp, step, q_cur, qbs, *cache, k_new, v_new, scores,
