@@ -327,9 +327,10 @@ retro_status retro_merge_output_cache(const retro_dims* dims, int32_t step, cons
  * in front of it, then combine + merge; with RETRO_FLAG_SELECT_IN_SCORES, when
  * the attention launch has 64 or more workgroups per KV head (each of which
  * would repeat the selection), or for max_pages > 6144, the selection runs at
- * the end of the score launch (or in a launch of its own) instead.  Steps that keep an earlier selection (top-k
- * reuse, retro_dims.reuse_interval) run the append, Alg. 2 on the kept rows,
- * attention and combine + merge as four launches. */
+ * the end of the score launch (or in a launch of its own) instead.  Steps
+ * that keep an earlier selection (top-k reuse, retro_dims.reuse_interval) run
+ * the append, Alg. 2 on the kept rows, attention and combine + merge as four
+ * launches. */
 retro_status retro_step(const retro_dims* dims, int32_t step, const void* q_window,
                         const void* k_new, const void* v_new, const retro_kv_cache* cache,
                         const retro_selection* sel, const retro_output_cache* ocache,
